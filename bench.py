@@ -1,0 +1,151 @@
+"""Group-backward throughput of the JAGG hot path on one MI355X.
+
+Workload: one double-stream MMDiT block (hidden 3072, 24 heads x 128, MLP
+12288), 4096 image tokens (1024^2 image -> 128^2 latent, 16 channels, 2x2
+patches) + 512 text tokens, batch 1, bf16 storage with fp32 accumulation,
+window W = 4.  A "step" is the backward of one window: JAGG = composites +
+one VJP over the batched endpoint pair; per step = W VJPs with the same
+kernels.  Saved activations come from the forward, which runs before the
+timed region; parameter gradients accumulate (beta = 1) across windows.
+
+Prints one JSON line (value = JAGG denoising-step backward throughput).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK = 2.5e15     # dense bf16 MFMA, MI355X
+HBM_PEAK = 8.0e12
+
+
+def block_flops(D, F, N, nt, ni, B):
+    """Algorithmic FLOPs of one double-block parameter VJP for a batch of B.
+
+    GEMMs: per token 18 D^2 weights (qkv 3, out 1, fc1 4, fc2 4 ... per stream,
+    6 D^2 modulation excluded as it is per sample), forward 2 flops/MAC; the
+    backward does the input-gradient and weight-gradient products (2x forward).
+    Attention backward: 4 N^2 Dh per head (dV, dP, dQ, dK), backward-cost appendix."""
+    tok = B * N
+    gemm_fwd = 2.0 * tok * (3 * D * D + D * D + 2 * D * F)
+    attn_bwd = 4.0 * B * N * N * D
+    return 2.0 * gemm_fwd + attn_bwd
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    import paper_2607_17572_amd as pk
+    import synth
+
+    pk.lib()  # fails loudly if the HIP library is not built
+    cfg = pk.config("block")
+    D, F, nt, ni = cfg.hidden, cfg.mlp_hidden, cfg.n_txt, cfg.n_img
+    N = nt + ni
+    W, B = 4, 1
+    ctx = pk.Context(cfg)
+    dt = torch.bfloat16
+    theta = torch.zeros(ctx.n_params, dtype=dt, device="cuda")
+    theta.copy_(synth.device_normal((ctx.n_params,), synth.THETA_SEED, std=0.02, dtype=dt))
+    for name, off, numel, r, c in ctx.layout:
+        if name.endswith("_gain"):
+            theta[off:off + numel] = 1.0 + 0.02 * synth.device_normal((numel,), synth.THETA_SEED + off)
+    t = [1.0 - k / 16 for k in range(W)]  # first window of a T = 16 uniform grid
+    xs = [synth.device_normal((B * N, D), synth.DATA_SEED + j, dtype=dt) for j in range(W)]
+    adv = float(synth.device_normal((1,), synth.DATA_SEED + 99).item())
+    ss = [(synth.device_normal((B * N, D), synth.DATA_SEED + 100 + j) * adv).to(dt) for j in range(W)]
+
+    # forward: endpoint pair (batch 2B) for JAGG; every step (batch B) for the baseline
+    pair = torch.cat([xs[0][:B * nt], xs[-1][:B * nt], xs[0][B * nt:], xs[-1][B * nt:]], 0)
+    saved_pair = ctx.new_saved(2 * B)
+    ctx.forward_save(theta, pair, [t[0]] * B + [t[-1]] * B, None, saved=saved_pair, batch=2 * B)
+    saved = []
+    for j in range(W):
+        sv = ctx.new_saved(B)
+        ctx.forward_save(theta, xs[j], [t[j]] * B, None, saved=sv, batch=B)
+        saved.append(sv)
+    dth = torch.zeros(ctx.n_params, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    # forward (no graph) time, for the update-stage context number
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    vtmp = torch.empty_like(xs[0])
+    ev0.record()
+    for j in range(W):
+        ctx.forward_save(theta, xs[j], [t[j]] * B, None, saved=None, batch=B, v_out=vtmp)
+    ev1.record()
+    torch.cuda.synchronize()
+    fwd_ms = ev0.elapsed_time(ev1) / W
+
+    def run_jagg():
+        ctx.group_backward(theta, saved_pair, B, ss, t, dth, beta=1.0)
+
+    def run_perstep():
+        ctx.perstep_group_backward(theta, saved, B, ss, dth, beta=1.0)
+
+    def timed(fn, k):
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(k):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / 1e3
+
+    for _ in range(args.warmup):
+        run_jagg()
+        run_perstep()
+    t_jagg = timed(run_jagg, args.steps)
+    t_ps = timed(run_perstep, args.steps)
+    print(f"[bench] jagg {1e3 * t_jagg / args.steps:.3f} ms/window, per-step {1e3 * t_ps / args.steps:.3f} ms/window",
+          file=sys.stderr, flush=True)
+
+    ms_jagg = 1e3 * t_jagg / args.steps
+    ms_ps = 1e3 * t_ps / args.steps
+    steps_s = W * args.steps / t_jagg
+    fl_pair = block_flops(D, F, N, nt, ni, 2 * B)
+    fl_one = block_flops(D, F, N, nt, ni, B)
+    out = {
+        "metric": "denoising-step backward throughput (steps/s) + MFMA util, JAGG vs per-step bwd",
+        "value": steps_s,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_jagg,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "one double-stream MMDiT block, hidden 3072, 24x128 heads, MLP 12288, "
+                               "4096 image + 512 text tokens, batch 1, W=4 (JAGG joint endpoint pair)",
+                   "W": W, "batch": B, "tokens": N, "hidden": D},
+        "perstep": {"value": W * args.steps / t_ps, "ms_per_window": ms_ps},
+        "speedup_vs_perstep": t_ps / t_jagg,
+        "tflops_jagg": fl_pair / (ms_jagg * 1e-3) / 1e12,
+        "tflops_perstep": W * fl_one / (ms_ps * 1e-3) / 1e12,
+        "forward_ms_per_step": fwd_ms,
+    }
+    out["mfma_frac_whole_backward"] = out["tflops_jagg"] * 1e12 / MFMA_BF16_PEAK
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

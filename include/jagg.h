@@ -1,0 +1,170 @@
+/*
+ * JAGG group backward on one MI355X (gfx950) — C ABI.
+ *
+ * The library computes the parameter gradient of a DiT/MMDiT velocity network
+ * over a window of W consecutive denoising steps in two ways:
+ *
+ *   JAGG:     g = J_0^T s_base + J_{W-1}^T s_corr, one backward pass over the
+ *             batched endpoint pair (paper: JAGG, Phases 3 and 4; the
+ *             Corollary of Theorem 1), with
+ *             alpha_j = (t_0 - t_j) / (t_0 - t_{W-1})            (Eq. alpha)
+ *             s_base = sum_j (1 - alpha_j) s_j, s_corr = sum_j alpha_j s_j
+ *                                                      (Eq. s_base / s_corr)
+ *   per step: g = sum_j J_j^T s_j, one backward per step   (the exact baseline
+ *             with the same detach of z_j, Phase 2 remark)
+ *
+ * where J(z, t) = d v_theta(z, t) / d theta and s_j = dL_j / d v_j is the
+ * per-step upstream gradient on the velocity output (given as input).
+ *
+ * Conventions for every call:
+ *  - Status codes: 0 OK; 1 invalid argument (detected before any launch);
+ *    2 out of memory; 3 device/launch error; 4 unsupported shape/dtype.
+ *    jagg_last_error() returns a thread-local message for the last failure.
+ *  - Ownership: the caller owns every buffer (parameters, gradients, inputs,
+ *    saved activations, workspace).  The library never allocates device memory
+ *    in these calls and never frees a caller pointer.  Pointers named "device"
+ *    are device memory; "host" pointers are read before the call returns.
+ *  - Streams: device work is enqueued on the context's HIP stream and the call
+ *    returns without synchronising; results are valid after that stream is
+ *    synchronised.  Calls on one context must not overlap from two threads.
+ *  - Dtypes: JAGG_F32 or JAGG_BF16 (bf16 = raw uint16 bit pattern).  theta,
+ *    the inputs, activations and s_j use cfg.act_dtype; dtheta uses
+ *    cfg.grad_dtype.  All arithmetic accumulates in fp32.
+ *  - Token rows ("stream-major"): for a batch of B samples the text rows of
+ *    all samples come first (sample b's text tokens at rows b*n_txt ..), then
+ *    the image rows (sample b's image tokens at rows B*n_txt + b*n_img ..).
+ *    A block-only model takes and returns its token streams in this layout,
+ *    [B*(n_txt+n_img)][hidden]; for B = 1 it is the joint sequence [text; image].
+ */
+#ifndef JAGG_H
+#define JAGG_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { JAGG_OK = 0, JAGG_EINVAL = 1, JAGG_ENOMEM = 2, JAGG_EDEVICE = 3, JAGG_EUNSUPPORTED = 4 } jagg_status;
+typedef enum { JAGG_F32 = 0, JAGG_BF16 = 1 } jagg_dtype;
+
+/* Network shape.  The architecture is the MMDiT of the paper's experiments
+ * (double-stream blocks with joint attention, then single-stream blocks),
+ * written out in the oracle's module docstring: adaLN modulation from a
+ * time-embedding MLP, LayerNorm without affine, q/k RMSNorm with a learned
+ * gain, 2-D rotary embedding (text tokens at position (0,0)), tanh-GELU MLP.
+ * block_only = 1: no patch/text embedding and no final layer; the model maps
+ * the token streams (stream-major rows) to the token streams of the last
+ * double block (n_single must be 0). */
+typedef struct {
+  int n_double, n_single;
+  int hidden, heads, head_dim, mlp_hidden;
+  int in_ch, patch, lat_h, lat_w; /* latent (B, in_ch, lat_h, lat_w); image tokens (lat_h/patch)*(lat_w/patch) */
+  int n_txt, txt_dim;
+  int t_freq_dim;                  /* sinusoidal timestep embedding width (even) */
+  int block_only;
+  int act_dtype;                   /* jagg_dtype of theta, inputs, activations, s_j */
+  int grad_dtype;                  /* jagg_dtype of dtheta */
+  int checkpoint;                  /* 1: save block inputs only, recompute each block in the VJP */
+} dit_config;
+
+typedef struct {
+  char name[48];     /* e.g. "double.3.img.fc1.w" */
+  size_t offset;     /* element offset in the flat theta / dtheta (multiple of 128) */
+  size_t numel;
+  int rows, cols;    /* weights [out][in]; vectors rows = numel, cols = 1 */
+} jagg_tensor_desc;
+
+typedef struct jagg_ctx jagg_ctx;
+
+/* Thread-local message describing the last failure of any call (never NULL). */
+const char* jagg_last_error(void);
+
+/* Parameter layout.  *n_tensors receives the tensor count, *n_elems the flat
+ * length (padding between tensors is never read or written).  If out != NULL
+ * it receives min(cap, count) descriptors.  Host only; no device needed. */
+jagg_status dit_param_layout(const dit_config* cfg, size_t* n_tensors, size_t* n_elems, jagg_tensor_desc* out,
+                             size_t cap);
+
+/* Create a context bound to `hip_stream` (a hipStream_t, or NULL for the null
+ * stream) on the current device.  Validates the config.  Host only. */
+jagg_status jagg_ctx_create(const dit_config* cfg, void* hip_stream, jagg_ctx** out);
+void jagg_ctx_destroy(jagg_ctx* ctx);
+
+/* Bytes of the saved-activation buffer for a forward of `batch` samples, and
+ * of the workspace needed by any call on `batch` samples.  Host only. */
+jagg_status dit_saved_bytes(const jagg_ctx* ctx, int batch, size_t* bytes);
+jagg_status dit_workspace_bytes(const jagg_ctx* ctx, int batch, size_t* bytes);
+/* Bind a caller-owned device workspace (kept until replaced or the context is
+ * destroyed; the caller frees it).  Calls check that it is large enough. */
+jagg_status jagg_ctx_set_workspace(jagg_ctx* ctx, void* ws, size_t bytes);
+
+/* Forward v = v_theta(z, t) for `batch` samples (1 <= batch <= 64).
+ *   theta : device, flat parameters (act dtype)
+ *   z     : device, latent (batch, in_ch, lat_h, lat_w); block-only: token rows
+ *   t     : host, `batch` network-input timesteps
+ *   txt   : device, text embeddings (batch, n_txt, txt_dim); NULL for block-only
+ *   v_out : device, output with the shape of z
+ *   saved : device, dit_saved_bytes(batch) bytes that the VJP reads; NULL runs
+ *           without saving (the middle steps of a window: no graph).
+ * Paper: JAGG Phase 1 (forward passes, graph only at the endpoints). */
+jagg_status dit_forward_save(jagg_ctx* ctx, const void* theta, const void* z, const float* t, const void* txt,
+                             void* v_out, void* saved, int batch);
+
+/* Parameter VJP: dtheta = beta * dtheta + J^T s for the forward stored in
+ * `saved` (same batch).  s: device, shape of v_out.  beta is 0 (overwrite) or
+ * 1 (accumulate); padding entries of dtheta are left untouched.
+ * Paper: one transformer backward ("Transformer bwd" column of the cost table). */
+jagg_status dit_vjp(jagg_ctx* ctx, const void* theta, const void* saved, int batch, const void* s, void* dtheta,
+                    float beta);
+
+/* Eq. alpha on the host: alpha_j = (t_0 - t_j)/(t_0 - t_{W-1}) computed in fp64
+ * and rounded to fp32 (alpha_0 = 0 and alpha_{W-1} = 1 exactly).  EINVAL if
+ * W < 2, a pointer is NULL or t_0 == t_{W-1}. */
+jagg_status jagg_alpha(const float* t, int W, float* alpha_out);
+
+/* Eq. s_base / s_corr on the device: s_base = sum_j (1 - alpha_j) s_j,
+ * s_corr = sum_j alpha_j s_j over n elements; fp32 accumulation in j order,
+ * one rounding on store.  s: host array of W device pointers; t: host W
+ * timesteps (the weights come from jagg_alpha).  s_base/s_corr: device, n
+ * elements of `dtype` (same as the inputs).  1 <= W <= 64. */
+jagg_status jagg_aggregate(jagg_ctx* ctx, const void* const* s, const float* t, int W, size_t n, int dtype,
+                           void* s_base, void* s_corr);
+
+/* Routing score of one window: the mean over the W(W-1)/2 pairs (i < j) of the
+ * cosine similarity of the per-step vectors h_i, h_j (n elements each, `dtype`),
+ * accumulated in fp64.  h: host array of W device pointers, 2 <= W <= 8.
+ * score_out: host, receives the score (the call synchronises the stream).
+ * Uses the bound workspace. */
+jagg_status jagg_group_scores(jagg_ctx* ctx, const void* const* h, size_t n, int W, int dtype, double* score_out);
+
+/* Routing (high-noise vs low-noise scheduling; gradient-quality appendix).
+ * Groups are ordered from high to low noise.  frac >= 0: the first
+ * floor(frac * n_groups + 1e-6) groups use JAGG (static jagg_frac).  frac < 0:
+ * scores (host, n_groups) decide: the longest prefix of groups whose score is
+ * >= tau.  use_jagg_out: host, n_groups bytes (1 = JAGG, 0 = per-step);
+ * frac_out: host, realised fraction (may be NULL).  Host only, bit-exact. */
+jagg_status jagg_route(const double* scores, int n_groups, double tau, double frac, unsigned char* use_jagg_out,
+                       double* frac_out);
+
+/* JAGG group backward (Phases 3 and 4): aggregates the W upstream gradients
+ * into the composite cotangent of the endpoint pair and runs ONE VJP over the
+ * batched pair.  saved_pair: the forward of batch 2B on [z_0; z_{W-1}] with
+ * t = [t_0 (B times); t_{W-1} (B times)] (block-only: stream-major rows of the
+ * 2B samples, endpoint 0 first within each stream).  s: host array of W device
+ * pointers, each with the shape of a batch-B output.  t: host W timesteps.
+ * dtheta = beta * dtheta + g_jagg.  2 <= W <= 64. */
+jagg_status jagg_group_backward(jagg_ctx* ctx, const void* theta, const void* saved_pair, int batch,
+                                const void* const* s, const float* t, int W, void* dtheta, float beta);
+
+/* Per-step baseline: W VJPs, one per step, accumulated into dtheta
+ * (dtheta = beta * dtheta + sum_j J_j^T s_j).  saved: host array of W device
+ * pointers, each a batch-B forward. */
+jagg_status perstep_group_backward(jagg_ctx* ctx, const void* theta, const void* const* saved, int batch,
+                                   const void* const* s, int W, void* dtheta, float beta);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JAGG_H */

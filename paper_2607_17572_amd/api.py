@@ -1,0 +1,272 @@
+"""Thin Python binding over the JAGG C ABI (include/jagg.h).
+
+Argument marshalling only: every step of the path runs in libjagg.so.  PyTorch
+supplies device memory (tensors) and the HIP stream.  If the library is not
+built, every entry point raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import asdict, dataclass
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libjagg.so")
+
+F32, BF16 = 0, 1
+
+
+class _DitConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in (
+        "n_double", "n_single", "hidden", "heads", "head_dim", "mlp_hidden", "in_ch", "patch", "lat_h",
+        "lat_w", "n_txt", "txt_dim", "t_freq_dim", "block_only", "act_dtype", "grad_dtype", "checkpoint")]
+
+
+class _TensorDesc(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("offset", ctypes.c_size_t), ("numel", ctypes.c_size_t),
+                ("rows", ctypes.c_int), ("cols", ctypes.c_int)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises RuntimeError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2607_17572_amd.build.build() "
+                               "(there is no fallback path)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz, i, f, d = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_float, ctypes.c_double
+        pcfg = ctypes.POINTER(_DitConfig)
+        L.jagg_last_error.restype = ctypes.c_char_p
+        sig = {
+            "dit_param_layout": [pcfg, ctypes.POINTER(sz), ctypes.POINTER(sz), ctypes.POINTER(_TensorDesc), sz],
+            "jagg_ctx_create": [pcfg, vp, ctypes.POINTER(vp)],
+            "dit_saved_bytes": [vp, i, ctypes.POINTER(sz)],
+            "dit_workspace_bytes": [vp, i, ctypes.POINTER(sz)],
+            "jagg_ctx_set_workspace": [vp, vp, sz],
+            "dit_forward_save": [vp, vp, vp, ctypes.POINTER(f), vp, vp, vp, i],
+            "dit_vjp": [vp, vp, vp, i, vp, vp, f],
+            "jagg_alpha": [ctypes.POINTER(f), i, ctypes.POINTER(f)],
+            "jagg_aggregate": [vp, ctypes.POINTER(vp), ctypes.POINTER(f), i, sz, i, vp, vp],
+            "jagg_group_scores": [vp, ctypes.POINTER(vp), sz, i, i, ctypes.POINTER(d)],
+            "jagg_route": [ctypes.POINTER(d), i, d, d, ctypes.POINTER(ctypes.c_ubyte), ctypes.POINTER(d)],
+            "jagg_group_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, vp, f],
+            "perstep_group_backward": [vp, vp, ctypes.POINTER(vp), i, ctypes.POINTER(vp), i, vp, f],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        L.jagg_ctx_destroy.argtypes = [vp]
+        L.jagg_ctx_destroy.restype = None
+        _lib = L
+    return _lib
+
+
+class JaggError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"JAGG status {status}: {msg}")
+        self.status = status
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise JaggError(rc, lib().jagg_last_error().decode())
+
+
+@dataclass(frozen=True)
+class Config:
+    n_double: int
+    n_single: int
+    hidden: int
+    heads: int
+    head_dim: int
+    mlp_hidden: int
+    in_ch: int = 4
+    patch: int = 1
+    lat_h: int = 4
+    lat_w: int = 4
+    n_txt: int = 8
+    txt_dim: int = 64
+    t_freq_dim: int = 256
+    block_only: int = 0
+    act_dtype: int = F32
+    grad_dtype: int = F32
+    checkpoint: int = 0
+
+    def c(self) -> _DitConfig:
+        return _DitConfig(**{k: int(v) for k, v in asdict(self).items()})
+
+    @property
+    def n_img(self) -> int:
+        return (self.lat_h // self.patch) * (self.lat_w // self.patch)
+
+    @property
+    def n_tok(self) -> int:
+        return self.n_txt + self.n_img
+
+
+def param_layout(cfg: Config):
+    """[(name, offset, numel, rows, cols)], flat length."""
+    c = cfg.c()
+    nt, ne = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().dit_param_layout(ctypes.byref(c), ctypes.byref(nt), ctypes.byref(ne), None, 0))
+    arr = (_TensorDesc * nt.value)()
+    _check(lib().dit_param_layout(ctypes.byref(c), ctypes.byref(nt), ctypes.byref(ne), arr, nt.value))
+    return [(d.name.decode(), d.offset, d.numel, d.rows, d.cols) for d in arr], ne.value
+
+
+def alpha(t):
+    W = len(t)
+    tt = (ctypes.c_float * W)(*[float(x) for x in t])
+    out = (ctypes.c_float * W)()
+    _check(lib().jagg_alpha(tt, W, out))
+    return list(out)
+
+
+def route(n_groups: int, frac: float | None = None, scores=None, tau: float = 0.5):
+    """(list of 0/1 per group, realised fraction)."""
+    sc = None
+    if scores is not None:
+        sc = (ctypes.c_double * n_groups)(*[float(x) for x in scores])
+    mask = (ctypes.c_ubyte * n_groups)()
+    fr = ctypes.c_double()
+    _check(lib().jagg_route(sc, n_groups, float(tau), -1.0 if frac is None else float(frac), mask, ctypes.byref(fr)))
+    return list(mask), fr.value
+
+
+def _ptrs(tensors):
+    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+
+
+def _torch():
+    import torch
+    return torch
+
+
+class Context:
+    """One model configuration bound to a HIP stream, with a workspace tensor."""
+
+    def __init__(self, cfg: Config, stream=None):
+        torch = _torch()
+        self.cfg = cfg
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        h = ctypes.c_void_p()
+        c = cfg.c()
+        _check(lib().jagg_ctx_create(ctypes.byref(c), ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)))
+        self._h = h
+        self._ws = None
+        self._ws_batch = 0
+        self.layout, self.n_params = param_layout(cfg)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.jagg_ctx_destroy(h)
+            self._h = None
+
+    @property
+    def dtype(self):
+        torch = _torch()
+        return torch.bfloat16 if self.cfg.act_dtype == BF16 else torch.float32
+
+    @property
+    def grad_dtype(self):
+        torch = _torch()
+        return torch.bfloat16 if self.cfg.grad_dtype == BF16 else torch.float32
+
+    def saved_bytes(self, batch: int) -> int:
+        n = ctypes.c_size_t()
+        _check(lib().dit_saved_bytes(self._h, batch, ctypes.byref(n)))
+        return n.value
+
+    def workspace_bytes(self, batch: int) -> int:
+        n = ctypes.c_size_t()
+        _check(lib().dit_workspace_bytes(self._h, batch, ctypes.byref(n)))
+        return n.value
+
+    def ensure_workspace(self, batch: int):
+        if self._ws is not None and self._ws_batch >= batch:
+            return
+        torch = _torch()
+        nb = self.workspace_bytes(batch)
+        self._ws = torch.empty(nb + 256, dtype=torch.uint8, device="cuda")
+        base = self._ws.data_ptr()
+        off = (-base) % 256
+        _check(lib().jagg_ctx_set_workspace(self._h, ctypes.c_void_p(base + off), nb))
+        self._ws_batch = batch
+
+    def new_saved(self, batch: int):
+        torch = _torch()
+        return torch.empty(self.saved_bytes(batch), dtype=torch.uint8, device="cuda")
+
+    def forward_save(self, theta, z, t, txt=None, saved=None, batch=None, v_out=None):
+        """v = v_theta(z, t); `saved` (uint8 tensor of saved_bytes(batch)) or None (no graph)."""
+        torch = _torch()
+        B = len(t) if batch is None else batch
+        self.ensure_workspace(B)
+        if v_out is None:
+            v_out = torch.empty_like(z)
+        tt = (ctypes.c_float * B)(*[float(x) for x in t])
+        _check(lib().dit_forward_save(self._h, theta.data_ptr(), z.data_ptr(), tt,
+                                      None if txt is None else txt.data_ptr(), v_out.data_ptr(),
+                                      None if saved is None else saved.data_ptr(), B))
+        return v_out
+
+    def vjp(self, theta, saved, batch: int, s, dtheta, beta: float = 0.0):
+        self.ensure_workspace(batch)
+        _check(lib().dit_vjp(self._h, theta.data_ptr(), saved.data_ptr(), batch, s.data_ptr(), dtheta.data_ptr(),
+                             float(beta)))
+        return dtheta
+
+    def aggregate(self, s_list, t, s_base, s_corr):
+        W = len(s_list)
+        tt = (ctypes.c_float * W)(*[float(x) for x in t])
+        dt = BF16 if s_list[0].dtype == _torch().bfloat16 else F32
+        _check(lib().jagg_aggregate(self._h, _ptrs(s_list), tt, W, s_list[0].numel(), dt, s_base.data_ptr(),
+                                    s_corr.data_ptr()))
+        return s_base, s_corr
+
+    def group_score(self, h_list) -> float:
+        self.ensure_workspace(1)
+        out = ctypes.c_double()
+        dt = BF16 if h_list[0].dtype == _torch().bfloat16 else F32
+        _check(lib().jagg_group_scores(self._h, _ptrs(h_list), h_list[0].numel(), len(h_list), dt, ctypes.byref(out)))
+        return out.value
+
+    def group_backward(self, theta, saved_pair, batch: int, s_list, t, dtheta, beta: float = 0.0):
+        """JAGG: composites + one VJP over the batch-2B endpoint pair."""
+        W = len(s_list)
+        self.ensure_workspace(2 * batch)
+        tt = (ctypes.c_float * W)(*[float(x) for x in t])
+        _check(lib().jagg_group_backward(self._h, theta.data_ptr(), saved_pair.data_ptr(), batch, _ptrs(s_list), tt,
+                                         W, dtheta.data_ptr(), float(beta)))
+        return dtheta
+
+    def perstep_group_backward(self, theta, saved_list, batch: int, s_list, dtheta, beta: float = 0.0):
+        self.ensure_workspace(batch)
+        _check(lib().perstep_group_backward(self._h, theta.data_ptr(), _ptrs(saved_list), batch, _ptrs(s_list),
+                                            len(s_list), dtheta.data_ptr(), float(beta)))
+        return dtheta
+
+
+# ------------------------------------------------------------------ configs
+def config(name: str, **over) -> Config:
+    """The five workloads: tiny (C1), block (C2), slice (C3), flux (C4), qwen (C5)."""
+    big = dict(hidden=3072, heads=24, head_dim=128, mlp_hidden=12288, in_ch=16, patch=2, t_freq_dim=256,
+               act_dtype=BF16, grad_dtype=F32)
+    table = {
+        "tiny": dict(n_double=2, n_single=0, hidden=64, heads=4, head_dim=16, mlp_hidden=256, in_ch=4, patch=1,
+                     lat_h=4, lat_w=4, n_txt=8, txt_dim=64, t_freq_dim=256, act_dtype=F32, grad_dtype=F32),
+        "block": dict(big, n_double=1, n_single=0, lat_h=128, lat_w=128, n_txt=512, txt_dim=3072, block_only=1),
+        "slice": dict(big, n_double=4, n_single=8, lat_h=64, lat_w=64, n_txt=512, txt_dim=4096),
+        "flux": dict(big, n_double=19, n_single=38, lat_h=128, lat_w=128, n_txt=512, txt_dim=4096,
+                     grad_dtype=BF16, checkpoint=1),
+        "qwen": dict(big, n_double=60, n_single=0, lat_h=128, lat_w=128, n_txt=256, txt_dim=4096, checkpoint=1),
+    }
+    d = dict(table[name])
+    d.update(over)
+    return Config(**d)

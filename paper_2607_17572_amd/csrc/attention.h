@@ -1,0 +1,33 @@
+// Softmax attention forward/backward over the joint [text; image] sequence.
+#pragma once
+#include "ops.h"
+
+namespace jg {
+
+// Q, K, V: head-major [B][H][N][Dh] (act dtype).  O is written token-major
+// into rows of the stream-major row layout (ld_o elements per row, head h at
+// columns h*Dh ..), LSE [B][H][N] fp32 (natural log of sum exp of scaled scores).
+struct AttnFwd {
+  const void* Q; const void* K; const void* V;
+  void* O; int ld_o;
+  float* lse;
+  int B, H, N, Dh, dt;
+  RowMap rm;
+};
+int attention_fwd(const AttnFwd& a, hipStream_t s);
+
+// dO token-major (ld_do), O token-major (ld_o); dQ/dK/dV head-major (dt_d).
+// `delta` is workspace [B][H][N] fp32.
+struct AttnBwd {
+  const void* Q; const void* K; const void* V;
+  const void* O; int ld_o;
+  const void* dO; int ld_do;
+  const float* lse;
+  float* delta;
+  void* dQ; void* dK; void* dV; int dt_d;
+  int B, H, N, Dh, dt;
+  RowMap rm;
+};
+int attention_bwd(const AttnBwd& a, hipStream_t s);
+
+}  // namespace jg

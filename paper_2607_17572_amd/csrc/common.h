@@ -1,0 +1,107 @@
+// Shared device/host helpers of the JAGG HIP library (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+#include <string>
+
+namespace jg {
+
+enum DType { F32 = 0, BF16 = 1 };
+
+// ---------------------------------------------------------------- bf16 bits
+// bf16 is carried as raw uint16_t; conversions are round-to-nearest-even with
+// NaN kept quiet.
+__device__ __host__ inline float bf2f(uint16_t v) {
+  union { uint32_t u; float f; } c;
+  c.u = (uint32_t)v << 16;
+  return c.f;
+}
+__device__ __host__ inline uint16_t f2bf(float f) {
+  union { uint32_t u; float f; } c;
+  c.f = f;
+  uint32_t u = c.u;
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x7fffffu)) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static __device__ __host__ inline float ld(const float* p, size_t i) { return p[i]; }
+  static __device__ __host__ inline void st(float* p, size_t i, float v) { p[i] = v; }
+};
+template <> struct Elem<uint16_t> {
+  static __device__ __host__ inline float ld(const uint16_t* p, size_t i) { return bf2f(p[i]); }
+  static __device__ __host__ inline void st(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
+};
+template <typename T> __device__ inline float ldf(const T* p, size_t i) { return Elem<T>::ld(p, i); }
+template <typename T> __device__ inline void stf(T* p, size_t i, float v) { Elem<T>::st(p, i, v); }
+
+// dtype-erased load/store (used where a kernel's operand dtype is a runtime flag)
+__device__ inline float ld_any(const void* p, int dt, size_t i) {
+  return dt == BF16 ? bf2f(((const uint16_t*)p)[i]) : ((const float*)p)[i];
+}
+__device__ inline void st_any(void* p, int dt, size_t i, float v) {
+  if (dt == BF16) ((uint16_t*)p)[i] = f2bf(v); else ((float*)p)[i] = v;
+}
+
+inline size_t dsize(int dt) { return dt == BF16 ? 2 : 4; }
+
+// ------------------------------------------------------------- wave helpers
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+// Block-wide sum for blockDim.x a multiple of 64 (<= 1024); `sh` holds >= 16 floats.
+__device__ inline float block_sum(float v, float* sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  float r = 0.f;
+  for (int i = 0; i < nw; ++i) r += sh[i];
+  return r;
+}
+
+__device__ inline float gelu_tanh(float x) {
+  const float c = 0.7978845608028654f;
+  float u = c * (x + 0.044715f * x * x * x);
+  return 0.5f * x * (1.f + tanhf(u));
+}
+__device__ inline float gelu_tanh_grad(float x) {
+  const float c = 0.7978845608028654f;
+  float th = tanhf(c * (x + 0.044715f * x * x * x));
+  return 0.5f * (1.f + th) + 0.5f * x * (1.f - th * th) * c * (1.f + 3.f * 0.044715f * x * x);
+}
+__device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
+__device__ inline float silu_grad(float x) {
+  float s = 1.f / (1.f + expf(-x));
+  return s * (1.f + x * (1.f - s));
+}
+
+// ------------------------------------------------------------ host errors
+void set_error(const std::string& msg);
+const char* get_error();
+
+struct Status {
+  int code;  // 0 ok, 1 invalid argument, 2 no memory, 3 device error, 4 unsupported
+};
+
+}  // namespace jg
+
+#define JG_CHECK_LAUNCH(name)                                                   \
+  do {                                                                          \
+    hipError_t e_ = hipGetLastError();                                          \
+    if (e_ != hipSuccess) {                                                     \
+      ::jg::set_error(std::string(name) + ": " + hipGetErrorString(e_));        \
+      return 3;                                                                 \
+    }                                                                           \
+  } while (0)

@@ -1,0 +1,927 @@
+// MMDiT forward-with-save and parameter VJP on gfx950, plus the JAGG group
+// backward (Phases 3 and 4: composites, then one VJP over the batched endpoint
+// pair) and the per-step baseline.  Everything is stream-ordered on the
+// context's HIP stream; the caller owns every buffer.
+#include <array>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/jagg.h"
+#include "attention.h"
+#include "gemm.h"
+#include "ops.h"
+
+namespace jg {
+
+thread_local std::string g_err;
+void set_error(const std::string& m) { g_err = m; }
+const char* get_error() { return g_err.c_str(); }
+
+#define TRY(x)                 \
+  do {                         \
+    int rc_ = (x);             \
+    if (rc_) return rc_;       \
+  } while (0)
+
+struct Lin { size_t w = 0, b = 0; int out = 0, in = 0; };
+struct DStream { Lin mod, qkv, o, fc1, fc2; size_t qg = 0, kg = 0; };
+struct SBlock { Lin mod, in, out; size_t qg = 0, kg = 0; };
+
+struct Model {
+  dit_config c{};
+  int D = 0, H = 0, Dh = 0, F = 0, C = 0, p = 0, gh = 0, gw = 0, nt = 0, ni = 0, N = 0, pd = 0, dtxt = 0, tf = 0;
+  int act = F32, grad = F32;
+  Lin t_in, t_out, img_in, txt_in, fmod, fin;
+  std::vector<std::array<DStream, 2>> dbl;
+  std::vector<SBlock> sgl;
+  std::vector<jagg_tensor_desc> layout;
+  size_t total = 0;
+};
+
+static size_t add_t(Model& m, const std::string& name, int rows, int cols) {
+  jagg_tensor_desc d;
+  std::memset(&d, 0, sizeof(d));
+  std::strncpy(d.name, name.c_str(), sizeof(d.name) - 1);
+  d.offset = m.total;
+  d.numel = (size_t)rows * cols;
+  d.rows = rows;
+  d.cols = cols;
+  m.layout.push_back(d);
+  m.total += (d.numel + 127) / 128 * 128;
+  return d.offset;
+}
+static Lin add_lin(Model& m, const std::string& pre, int out, int in) {
+  Lin l;
+  l.out = out;
+  l.in = in;
+  l.w = add_t(m, pre + ".w", out, in);
+  l.b = add_t(m, pre + ".b", out, 1);
+  return l;
+}
+
+static int build_model(const dit_config& c, Model& m) {
+  auto bad = [](const char* msg) { set_error(std::string("dit_config: ") + msg); return 1; };
+  if (c.n_double < 0 || c.n_single < 0 || c.hidden <= 0 || c.heads <= 0 || c.head_dim <= 0 || c.mlp_hidden <= 0)
+    return bad("sizes must be positive");
+  if (c.hidden != c.heads * c.head_dim) return bad("hidden must equal heads * head_dim");
+  if (c.head_dim % 4 || c.head_dim > 128) return bad("head_dim must be a multiple of 4 and <= 128");
+  if (c.hidden > 4096) return bad("hidden must be <= 4096");
+  if (c.t_freq_dim <= 0 || c.t_freq_dim % 2) return bad("t_freq_dim must be positive and even");
+  if (c.patch <= 0 || c.lat_h % c.patch || c.lat_w % c.patch) return bad("latent size must be a multiple of patch");
+  if (c.in_ch <= 0 || c.lat_h <= 0 || c.lat_w <= 0 || c.n_txt <= 0) return bad("latent/text sizes must be positive");
+  if (!c.block_only && c.txt_dim <= 0) return bad("txt_dim must be positive");
+  if (c.block_only && c.n_single) return bad("a block-only model has double-stream blocks only");
+  if (c.n_double + c.n_single == 0 && c.block_only) return bad("no blocks");
+  if ((c.act_dtype != JAGG_F32 && c.act_dtype != JAGG_BF16) || (c.grad_dtype != JAGG_F32 && c.grad_dtype != JAGG_BF16))
+    return bad("unknown dtype");
+  m = Model();
+  m.c = c;
+  m.D = c.hidden; m.H = c.heads; m.Dh = c.head_dim; m.F = c.mlp_hidden;
+  m.C = c.in_ch; m.p = c.patch; m.gh = c.lat_h / c.patch; m.gw = c.lat_w / c.patch;
+  m.nt = c.n_txt; m.ni = m.gh * m.gw; m.N = m.nt + m.ni; m.pd = c.in_ch * c.patch * c.patch;
+  m.dtxt = c.txt_dim; m.tf = c.t_freq_dim; m.act = c.act_dtype; m.grad = c.grad_dtype;
+  const int D = m.D, F = m.F;
+  m.t_in = add_lin(m, "t_in", D, m.tf);
+  m.t_out = add_lin(m, "t_out", D, D);
+  if (!c.block_only) {
+    m.img_in = add_lin(m, "img_in", D, m.pd);
+    m.txt_in = add_lin(m, "txt_in", D, m.dtxt);
+  }
+  for (int i = 0; i < c.n_double; ++i) {
+    std::array<DStream, 2> st;
+    const char* nm[2] = {"txt", "img"};
+    for (int s = 0; s < 2; ++s) {
+      const std::string p = "double." + std::to_string(i) + "." + nm[s] + ".";
+      st[s].mod = add_lin(m, p + "mod", 6 * D, D);
+      st[s].qkv = add_lin(m, p + "qkv", 3 * D, D);
+      st[s].qg = add_t(m, p + "q_gain", m.Dh, 1);
+      st[s].kg = add_t(m, p + "k_gain", m.Dh, 1);
+      st[s].o = add_lin(m, p + "o", D, D);
+      st[s].fc1 = add_lin(m, p + "fc1", F, D);
+      st[s].fc2 = add_lin(m, p + "fc2", D, F);
+    }
+    m.dbl.push_back(st);
+  }
+  for (int i = 0; i < c.n_single; ++i) {
+    SBlock b;
+    const std::string p = "single." + std::to_string(i) + ".";
+    b.mod = add_lin(m, p + "mod", 3 * D, D);
+    b.in = add_lin(m, p + "in", 3 * D + F, D);
+    b.qg = add_t(m, p + "q_gain", m.Dh, 1);
+    b.kg = add_t(m, p + "k_gain", m.Dh, 1);
+    b.out = add_lin(m, p + "out", D, D + F);
+    m.sgl.push_back(b);
+  }
+  if (!c.block_only) {
+    m.fmod = add_lin(m, "final.mod", 2 * D, D);
+    m.fin = add_lin(m, "final", m.pd, D);
+  }
+  return 0;
+}
+
+// ------------------------------------------------------------------ buffers
+struct Arena {
+  char* base;
+  size_t off = 0;
+  explicit Arena(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off += (bytes + 255) / 256 * 256;
+    return p;
+  }
+  float* f32(size_t n) { return (float*)take(n * 4); }
+};
+
+struct DblAct {
+  void *x_in = nullptr, *a1 = nullptr, *qkv = nullptr, *Qh = nullptr, *Kh = nullptr, *Vh = nullptr, *O = nullptr,
+       *y1 = nullptr, *xm = nullptr, *a2 = nullptr, *pre = nullptr, *h = nullptr, *y2 = nullptr, *x_out = nullptr;
+  float *mod[2] = {nullptr, nullptr}, *m1 = nullptr, *r1 = nullptr, *rq = nullptr, *rk = nullptr, *lse = nullptr,
+        *m2 = nullptr, *r2 = nullptr;
+};
+struct SglAct {
+  void *x_in = nullptr, *a = nullptr, *proj = nullptr, *Qh = nullptr, *Kh = nullptr, *Vh = nullptr, *cat = nullptr,
+       *y = nullptr, *x_out = nullptr;
+  float *mod = nullptr, *m = nullptr, *r = nullptr, *rq = nullptr, *rk = nullptr, *lse = nullptr;
+};
+
+struct Global {
+  float *temb = nullptr, *h1 = nullptr, *sh1 = nullptr, *vec = nullptr, *mvec = nullptr;
+  void *patches = nullptr, *txt = nullptr, *x0 = nullptr;
+  float *fmod = nullptr, *fm = nullptr, *fr = nullptr;
+  void* fa = nullptr;
+};
+
+struct Saved {
+  Global g;
+  std::vector<DblAct> d;
+  std::vector<SglAct> s;
+};
+
+static void plan_dbl(const Model& m, Arena& a, int B, DblAct& A, bool full) {
+  const size_t rows = (size_t)B * m.N, es = dsize(m.act);
+  const size_t hn = (size_t)B * m.H * m.N;
+  if (full) {
+    A.mod[0] = a.f32((size_t)B * 6 * m.D);
+    A.mod[1] = a.f32((size_t)B * 6 * m.D);
+    A.m1 = a.f32(rows); A.r1 = a.f32(rows);
+    A.a1 = a.take(rows * m.D * es);
+    A.qkv = a.take(rows * 3 * m.D * es);
+    A.rq = a.f32(rows * m.H); A.rk = a.f32(rows * m.H);
+    A.Qh = a.take(hn * m.Dh * es); A.Kh = a.take(hn * m.Dh * es); A.Vh = a.take(hn * m.Dh * es);
+    A.O = a.take(rows * m.D * es);
+    A.lse = a.f32(hn);
+    A.y1 = a.take(rows * m.D * es);
+    A.xm = a.take(rows * m.D * es);
+    A.m2 = a.f32(rows); A.r2 = a.f32(rows);
+    A.a2 = a.take(rows * m.D * es);
+    A.pre = a.take(rows * m.F * es);
+    A.h = a.take(rows * m.F * es);
+    A.y2 = a.take(rows * m.D * es);
+  }
+  A.x_out = a.take(rows * m.D * es);
+}
+
+static void plan_sgl(const Model& m, Arena& a, int B, SglAct& A, bool full) {
+  const size_t rows = (size_t)B * m.N, es = dsize(m.act);
+  const size_t hn = (size_t)B * m.H * m.N;
+  if (full) {
+    A.mod = a.f32((size_t)B * 3 * m.D);
+    A.m = a.f32(rows); A.r = a.f32(rows);
+    A.a = a.take(rows * m.D * es);
+    A.proj = a.take(rows * (3 * m.D + m.F) * es);
+    A.rq = a.f32(rows * m.H); A.rk = a.f32(rows * m.H);
+    A.Qh = a.take(hn * m.Dh * es); A.Kh = a.take(hn * m.Dh * es); A.Vh = a.take(hn * m.Dh * es);
+    A.cat = a.take(rows * (m.D + m.F) * es);
+    A.lse = a.f32(hn);
+    A.y = a.take(rows * m.D * es);
+  }
+  A.x_out = a.take(rows * m.D * es);
+}
+
+static size_t plan_saved(const Model& m, int B, void* base, Saved& S) {
+  Arena a(base);
+  const size_t rows = (size_t)B * m.N, es = dsize(m.act);
+  S = Saved();
+  S.g.temb = a.f32((size_t)B * m.tf);
+  S.g.h1 = a.f32((size_t)B * m.D);
+  S.g.sh1 = a.f32((size_t)B * m.D);
+  S.g.vec = a.f32((size_t)B * m.D);
+  S.g.mvec = a.f32((size_t)B * m.D);
+  if (!m.c.block_only) {
+    S.g.patches = a.take((size_t)B * m.ni * m.pd * es);
+    S.g.txt = a.take((size_t)B * m.nt * m.dtxt * es);
+  }
+  S.g.x0 = a.take(rows * m.D * es);
+  const bool full = !m.c.checkpoint;
+  S.d.resize(m.c.n_double);
+  S.s.resize(m.c.n_single);
+  void* prev = S.g.x0;
+  for (auto& A : S.d) { plan_dbl(m, a, B, A, full); A.x_in = prev; prev = A.x_out; }
+  for (auto& A : S.s) { plan_sgl(m, a, B, A, full); A.x_in = prev; prev = A.x_out; }
+  if (!m.c.block_only) {
+    S.g.fmod = a.f32((size_t)B * 2 * m.D);
+    S.g.fm = a.f32(rows);
+    S.g.fr = a.f32(rows);
+    S.g.fa = a.take(rows * m.D * es);
+  }
+  return a.off;
+}
+
+struct Ws {
+  DblAct sd;
+  SglAct ss;
+  void *xa = nullptr, *xb = nullptr;
+  float* g = nullptr;
+  void* dY = nullptr;
+  void* dbig = nullptr;
+  float* dA = nullptr;
+  void* dO = nullptr;
+  void *dQh = nullptr, *dKh = nullptr, *dVh = nullptr;
+  float* delta = nullptr;
+  float *p1 = nullptr, *p2 = nullptr;
+  float* dmod[2] = {nullptr, nullptr};
+  float *dmvec = nullptr, *dvec = nullptr, *dsh1 = nullptr, *tmp = nullptr;
+  float* slpart = nullptr;
+  void* gact = nullptr;
+  void* fout = nullptr;
+  float* dfa = nullptr;
+  void* cot = nullptr;
+  double *spart = nullptr, *score = nullptr;
+  int maxcols = 0;
+};
+
+static size_t out_elems(const Model& m) {  // per sample
+  return m.c.block_only ? (size_t)m.N * m.D : (size_t)m.C * m.c.lat_h * m.c.lat_w;
+}
+
+static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
+  Arena a(base);
+  const size_t rows = (size_t)B * m.N, es = dsize(m.act);
+  const size_t hn = (size_t)B * m.H * m.N;
+  W = Ws();
+  // group-score buffers first: their offset does not depend on the batch
+  W.spart = (double*)a.take(score_part_doubles(8) * sizeof(double));
+  W.score = (double*)a.take(64);
+  if (m.c.n_double) plan_dbl(m, a, B, W.sd, true);
+  if (m.c.n_single) plan_sgl(m, a, B, W.ss, true);
+  W.xa = a.take(rows * m.D * es);
+  W.xb = a.take(rows * m.D * es);
+  W.g = a.f32(rows * m.D);
+  W.dY = a.take(rows * m.D * es);
+  const int big = std::max(m.F, 3 * m.D + (m.c.n_single ? m.F : 0));
+  W.dbig = a.take(rows * big * es);
+  W.dA = a.f32(rows * m.D);
+  W.dO = a.take(rows * m.D * es);
+  W.dQh = a.take(hn * m.Dh * es);
+  W.dKh = a.take(hn * m.Dh * es);
+  W.dVh = a.take(hn * m.Dh * es);
+  W.delta = a.f32(hn);
+  W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, 2 * m.Dh, m.pd});
+  const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
+  W.p1 = a.f32((size_t)nch * W.maxcols);
+  W.p2 = a.f32((size_t)nch * W.maxcols);
+  W.dmod[0] = a.f32((size_t)B * 6 * m.D);
+  W.dmod[1] = a.f32((size_t)B * 6 * m.D);
+  W.dmvec = a.f32((size_t)B * m.D);
+  W.dvec = a.f32((size_t)B * m.D);
+  W.dsh1 = a.f32((size_t)B * m.D);
+  W.tmp = a.f32((size_t)B * m.D);
+  W.slpart = a.f32(std::max(small_linear_bwd_part_floats(B, m.D, 6 * m.D), small_linear_bwd_part_floats(B, m.tf, m.D)));
+  W.gact = a.take(rows * m.D * es);
+  if (!m.c.block_only) {
+    W.fout = a.take((size_t)B * m.ni * m.pd * es);
+    W.dfa = a.f32(rows * m.D);
+  }
+  W.cot = a.take((size_t)B * out_elems(m) * es);
+  return a.off;
+}
+
+}  // namespace jg
+
+using namespace jg;
+
+struct jagg_ctx {
+  Model m;
+  hipStream_t stream = nullptr;
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+};
+
+namespace jg {
+
+// ------------------------------------------------------------ GEMM helpers
+struct Ctx {
+  const Model& m;
+  hipStream_t s;
+  const char* th;  // theta base
+  size_t es;       // theta element size
+  const void* P(size_t off) const { return th + off * es; }
+};
+
+// Y[M][:] = X[M][K] W[rows w_row0..][K]^T + b  (one linear layer or a row slice of it)
+static int lin_fwd(const Ctx& cx, const void* X, int ldx, int M, const Lin& L, int w_row0, int nout, void* Y,
+                   int ldy, int mode = EPI_STORE, void* aux = nullptr, int ldaux = 0) {
+  GemmArgs g;
+  g.A = X; g.lda = ldx; g.ta = 0; g.a_dt = cx.m.act;
+  g.B = (const char*)cx.P(L.w) + (size_t)w_row0 * L.in * cx.es; g.ldb = L.in; g.tb = 0; g.b_dt = cx.m.act;
+  g.M = M; g.N = nout; g.K = L.in;
+  g.epi.C = Y; g.epi.ldc = ldy; g.epi.c_dt = cx.m.act;
+  g.epi.bias = (const char*)cx.P(L.b) + (size_t)w_row0 * cx.es; g.epi.bias_dt = cx.m.act;
+  g.epi.mode = mode; g.epi.aux = aux; g.epi.ldaux = ldaux; g.epi.aux_dt = cx.m.act;
+  return gemm(g, cx.s);
+}
+
+// dW[Nout][Kin] = beta dW + dY[rows][Nout]^T X[rows][Kin]
+static int wgrad(const Ctx& cx, const void* dY, int ld_dy, int dy_dt, const void* X, int ldx, int rows, int Nout,
+                 int Kin, void* dW, float beta) {
+  GemmArgs g;
+  g.A = dY; g.lda = ld_dy; g.ta = 1; g.a_dt = dy_dt;
+  g.B = X; g.ldb = ldx; g.tb = 1; g.b_dt = cx.m.act;
+  g.M = Nout; g.N = Kin; g.K = rows;
+  g.epi.C = dW; g.epi.ldc = Kin; g.epi.c_dt = cx.m.grad; g.epi.beta = beta;
+  return gemm(g, cx.s);
+}
+
+// out[rows][Kin] = dY[rows][Nout] W[Nout][Kin] (W row-sliced via w_off/ldw) with epilogue
+static int dgrad(const Ctx& cx, const void* dY, int ld_dy, int rows, const void* W, int ldw, int Nout, int Kin,
+                 void* out, int ldo, int odt, int mode = EPI_STORE, void* aux = nullptr, int ldaux = 0) {
+  GemmArgs g;
+  g.A = dY; g.lda = ld_dy; g.ta = 0; g.a_dt = cx.m.act;
+  g.B = W; g.ldb = ldw; g.tb = 1; g.b_dt = cx.m.act;
+  g.M = rows; g.N = Kin; g.K = Nout;
+  g.epi.C = out; g.epi.ldc = ldo; g.epi.c_dt = odt;
+  g.epi.mode = mode; g.epi.aux = aux; g.epi.ldaux = ldaux; g.epi.aux_dt = cx.m.act;
+  return gemm(g, cx.s);
+}
+
+static void* G(void* dth, const Model& m, size_t off) { return (char*)dth + off * dsize(m.grad); }
+
+// -------------------------------------------------------------- forward
+static int dbl_fwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int B) {
+  const Model& m = cx.m;
+  const int D = m.D, F = m.F;
+  const RowMap rm{B, m.nt, m.ni};
+  const int rt = rm.rows_txt(), R = rm.rows();
+  const int r0[2] = {0, rt}, nr[2] = {rt, R - rt};
+  const size_t es = dsize(m.act);
+  auto row = [&](void* p, int r, int ld) { return (void*)((char*)p + (size_t)r * ld * es); };
+  const auto& st = m.dbl[i];
+  for (int s = 0; s < 2; ++s)
+    TRY(small_linear_fwd(mvec, 0, B, D, cx.P(st[s].mod.w), cx.P(st[s].mod.b), m.act, A.mod[s], 6 * D, cx.s));
+  TRY(ln_mod_fwd(A.x_in, m.act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 0, D, A.a1, A.m1, A.r1, cx.s));
+  for (int s = 0; s < 2; ++s)
+    TRY(lin_fwd(cx, row(A.a1, r0[s], D), D, nr[s], st[s].qkv, 0, 3 * D, row(A.qkv, r0[s], 3 * D), 3 * D));
+  Gains gn{{cx.P(st[0].qg), cx.P(st[1].qg)}, {cx.P(st[0].kg), cx.P(st[1].kg)}};
+  TRY(qk_norm_rope_fwd(A.qkv, 3 * D, m.act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.Qh, A.Kh, A.Vh, A.rq, A.rk,
+                       cx.s));
+  AttnFwd af{A.Qh, A.Kh, A.Vh, A.O, D, A.lse, B, m.H, m.N, m.Dh, m.act, rm};
+  TRY(attention_fwd(af, cx.s));
+  for (int s = 0; s < 2; ++s)
+    TRY(lin_fwd(cx, row(A.O, r0[s], D), D, nr[s], st[s].o, 0, D, row(A.y1, r0[s], D), D));
+  TRY(gated_residual(A.x_in, A.y1, m.act, D, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, A.xm, cx.s));
+  TRY(ln_mod_fwd(A.xm, m.act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 3 * D, 4 * D, A.a2, A.m2, A.r2, cx.s));
+  for (int s = 0; s < 2; ++s) {
+    TRY(lin_fwd(cx, row(A.a2, r0[s], D), D, nr[s], st[s].fc1, 0, F, row(A.h, r0[s], F), F, EPI_GELU_FWD,
+                row(A.pre, r0[s], F), F));
+    TRY(lin_fwd(cx, row(A.h, r0[s], F), F, nr[s], st[s].fc2, 0, D, row(A.y2, r0[s], D), D));
+  }
+  TRY(gated_residual(A.xm, A.y2, m.act, D, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, A.x_out, cx.s));
+  return 0;
+}
+
+static int sgl_fwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int B) {
+  const Model& m = cx.m;
+  const int D = m.D, F = m.F, LD = 3 * D + F, LC = D + F;
+  const RowMap rm{B, m.nt, m.ni};
+  const int R = rm.rows();
+  const size_t es = dsize(m.act);
+  const SBlock& sb = m.sgl[i];
+  TRY(small_linear_fwd(mvec, 0, B, D, cx.P(sb.mod.w), cx.P(sb.mod.b), m.act, A.mod, 3 * D, cx.s));
+  TRY(ln_mod_fwd(A.x_in, m.act, D, rm, 0, R, A.mod, A.mod, 3 * D, 0, D, A.a, A.m, A.r, cx.s));
+  TRY(lin_fwd(cx, A.a, D, R, sb.in, 0, 3 * D, A.proj, LD));
+  TRY(lin_fwd(cx, A.a, D, R, sb.in, 3 * D, F, (char*)A.cat + D * es, LC, EPI_GELU_FWD, (char*)A.proj + 3 * D * es,
+              LD));
+  Gains gn{{cx.P(sb.qg), cx.P(sb.qg)}, {cx.P(sb.kg), cx.P(sb.kg)}};
+  TRY(qk_norm_rope_fwd(A.proj, LD, m.act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.Qh, A.Kh, A.Vh, A.rq, A.rk,
+                       cx.s));
+  AttnFwd af{A.Qh, A.Kh, A.Vh, A.cat, LC, A.lse, B, m.H, m.N, m.Dh, m.act, rm};
+  TRY(attention_fwd(af, cx.s));
+  TRY(lin_fwd(cx, A.cat, LC, R, sb.out, 0, D, A.y, D));
+  TRY(gated_residual(A.x_in, A.y, m.act, D, D, rm, 0, R, A.mod, A.mod, 3 * D, 2 * D, A.x_out, cx.s));
+  return 0;
+}
+
+static int forward(jagg_ctx* ctx, const void* theta, const void* z, const float* t, const void* txt, void* v_out,
+                   void* saved, int B) {
+  const Model& m = ctx->m;
+  Ctx cx{m, ctx->stream, (const char*)theta, dsize(m.act)};
+  const size_t es = dsize(m.act);
+  const RowMap rm{B, m.nt, m.ni};
+  const int rt = rm.rows_txt(), R = rm.rows(), D = m.D;
+  Ws W;
+  plan_ws(m, B, ctx->ws, W);
+  Saved S;
+  Saved* SP = nullptr;
+  if (saved) { plan_saved(m, B, saved, S); SP = &S; }
+  // global activations live in `saved`, or in the workspace scratch otherwise
+  Global gl;
+  if (SP) gl = S.g;
+  else {
+    Saved tmp;
+    // no-grad: borrow workspace regions (gradient buffers are idle in a forward)
+    gl.temb = W.dA; gl.h1 = W.dvec; gl.sh1 = W.dsh1; gl.vec = W.tmp; gl.mvec = W.dmvec;
+    gl.patches = W.dbig;
+    gl.txt = (char*)W.dbig + (size_t)B * m.ni * m.pd * es;
+    gl.x0 = W.xa;
+    gl.fmod = W.dmod[0]; gl.fm = W.p1; gl.fr = W.p2; gl.fa = W.gact;
+    (void)tmp;
+  }
+  TVals tv;
+  for (int b = 0; b < B; ++b) tv.t[b] = t[b];
+  TRY(time_embed(tv, B, m.tf, gl.temb, cx.s));
+  TRY(small_linear_fwd(gl.temb, 0, B, m.tf, cx.P(m.t_in.w), cx.P(m.t_in.b), m.act, gl.h1, D, cx.s));
+  TRY(silu_fwd(gl.h1, gl.sh1, (size_t)B * D, cx.s));
+  TRY(small_linear_fwd(gl.sh1, 0, B, D, cx.P(m.t_out.w), cx.P(m.t_out.b), m.act, gl.vec, D, cx.s));
+  TRY(silu_fwd(gl.vec, gl.mvec, (size_t)B * D, cx.s));
+  if (m.c.block_only) {
+    if (hipMemcpyAsync(gl.x0, z, (size_t)R * D * es, hipMemcpyDeviceToDevice, cx.s) != hipSuccess) {
+      set_error("forward: copy of the input token rows failed");
+      return 3;
+    }
+  } else {
+    TRY(patchify(z, m.act, B, m.C, m.c.lat_h, m.c.lat_w, m.p, gl.patches, cx.s));
+    TRY(lin_fwd(cx, gl.patches, m.pd, B * m.ni, m.img_in, 0, D, (char*)gl.x0 + (size_t)rt * D * es, D));
+    if (hipMemcpyAsync(gl.txt, txt, (size_t)B * m.nt * m.dtxt * es, hipMemcpyDeviceToDevice, cx.s) != hipSuccess) {
+      set_error("forward: copy of the text embeddings failed");
+      return 3;
+    }
+    TRY(lin_fwd(cx, gl.txt, m.dtxt, rt, m.txt_in, 0, D, gl.x0, D));
+  }
+  const bool keep = SP && !m.c.checkpoint;
+  void* x = gl.x0;
+  int pp = 0;
+  for (int i = 0; i < m.c.n_double; ++i) {
+    DblAct A = keep ? S.d[i] : W.sd;
+    A.x_in = x;
+    if (SP) A.x_out = S.d[i].x_out;
+    else A.x_out = (pp++ % 2) ? W.xa : W.xb;
+    TRY(dbl_fwd(cx, i, A, gl.mvec, B));
+    x = A.x_out;
+  }
+  for (int i = 0; i < m.c.n_single; ++i) {
+    SglAct A = keep ? S.s[i] : W.ss;
+    A.x_in = x;
+    if (SP) A.x_out = S.s[i].x_out;
+    else A.x_out = (pp++ % 2) ? W.xa : W.xb;
+    TRY(sgl_fwd(cx, i, A, gl.mvec, B));
+    x = A.x_out;
+  }
+  if (m.c.block_only) {
+    if (hipMemcpyAsync(v_out, x, (size_t)R * D * es, hipMemcpyDeviceToDevice, cx.s) != hipSuccess) {
+      set_error("forward: copy of the output token rows failed");
+      return 3;
+    }
+    return 0;
+  }
+  TRY(small_linear_fwd(gl.mvec, 0, B, D, cx.P(m.fmod.w), cx.P(m.fmod.b), m.act, gl.fmod, 2 * D, cx.s));
+  TRY(ln_mod_fwd(x, m.act, D, rm, rt, R - rt, gl.fmod, gl.fmod, 2 * D, 0, D, gl.fa, gl.fm, gl.fr, cx.s));
+  TRY(lin_fwd(cx, (char*)gl.fa + (size_t)rt * D * es, D, B * m.ni, m.fin, 0, m.pd, W.fout, m.pd));
+  TRY(unpatchify(W.fout, m.act, B, m.C, m.c.lat_h, m.c.lat_w, m.p, v_out, cx.s));
+  return 0;
+}
+
+// ------------------------------------------------------------------ VJP
+static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int B, Ws& W, void* dth, float beta) {
+  const Model& m = cx.m;
+  const int D = m.D, F = m.F, act = m.act;
+  const RowMap rm{B, m.nt, m.ni};
+  const int rt = rm.rows_txt(), R = rm.rows();
+  const int r0[2] = {0, rt}, nr[2] = {rt, R - rt};
+  const size_t es = dsize(act);
+  auto row = [&](void* p, int r, int ld) { return (void*)((char*)p + (size_t)r * ld * es); };
+  auto rowf = [&](float* p, int r, int ld) { return p + (size_t)r * ld; };
+  const auto& st = m.dbl[i];
+  const int nchunk = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
+  for (int s = 0; s < 2; ++s) {
+    const DStream& L = st[s];
+    int c0, nc;
+    TRY(chunk_range(rm, r0[s], nr[s], &c0, &nc));
+    // MLP branch: x_out = xm + gate2 * y2
+    TRY(gate_bwd(W.g, A.y2, act, D, rm, r0[s], nr[s], A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, W.p1, W.p2, cx.s));
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 5 * D, cx.s));
+    TRY(reduce_to_grad(W.p2, D, c0, nc, D, G(dth, m, L.fc2.b), m.grad, beta, cx.s));
+    void* dY = row(W.dY, r0[s], D);
+    TRY(wgrad(cx, dY, D, act, row(A.h, r0[s], F), F, nr[s], D, F, G(dth, m, L.fc2.w), beta));
+    void* dpre = row(W.dbig, r0[s], F);
+    TRY(dgrad(cx, dY, D, nr[s], cx.P(L.fc2.w), F, D, F, dpre, F, act, EPI_GELU_BWD, row(A.pre, r0[s], F), F));
+    TRY(colsum_partials(W.dbig, act, F, F, rm, r0[s], nr[s], W.p1, cx.s));
+    TRY(reduce_to_grad(W.p1, F, c0, nc, F, G(dth, m, L.fc1.b), m.grad, beta, cx.s));
+    TRY(wgrad(cx, dpre, F, act, row(A.a2, r0[s], D), D, nr[s], F, D, G(dth, m, L.fc1.w), beta));
+    TRY(dgrad(cx, dpre, F, nr[s], cx.P(L.fc1.w), D, F, D, rowf(W.dA, r0[s], D), D, F32));
+    TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, r0[s], nr[s], A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, W.g, W.p1,
+                   W.p2, cx.s));
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D, cx.s));
+    TRY(reduce_per_sample(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D, cx.s));
+    // attention branch: xm = x + gate1 * y1
+    TRY(gate_bwd(W.g, A.y1, act, D, rm, r0[s], nr[s], A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, W.p1, W.p2, cx.s));
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 2 * D, cx.s));
+    TRY(reduce_to_grad(W.p2, D, c0, nc, D, G(dth, m, L.o.b), m.grad, beta, cx.s));
+    TRY(wgrad(cx, dY, D, act, row(A.O, r0[s], D), D, nr[s], D, D, G(dth, m, L.o.w), beta));
+    TRY(dgrad(cx, dY, D, nr[s], cx.P(L.o.w), D, D, D, row(W.dO, r0[s], D), D, act));
+  }
+  AttnBwd ab{A.Qh, A.Kh, A.Vh, A.O, D, W.dO, D, A.lse, W.delta, W.dQh, W.dKh, W.dVh, act, B, m.H, m.N, m.Dh, act, rm};
+  TRY(attention_bwd(ab, cx.s));
+  Gains gn{{cx.P(st[0].qg), cx.P(st[1].qg)}, {cx.P(st[0].kg), cx.P(st[1].kg)}};
+  TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.qkv, 3 * D, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
+                       A.rk, W.dbig, 3 * D, W.p2, cx.s));
+  for (int s = 0; s < 2; ++s) {
+    const DStream& L = st[s];
+    int c0, nc;
+    TRY(chunk_range(rm, r0[s], nr[s], &c0, &nc));
+    TRY(reduce_to_grad(W.p2, 2 * m.Dh, c0, nc, m.Dh, G(dth, m, L.qg), m.grad, beta, cx.s));
+    TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, c0, nc, m.Dh, G(dth, m, L.kg), m.grad, beta, cx.s));
+    TRY(colsum_partials(W.dbig, act, 3 * D, 3 * D, rm, r0[s], nr[s], W.p1, cx.s));
+    TRY(reduce_to_grad(W.p1, 3 * D, c0, nc, 3 * D, G(dth, m, L.qkv.b), m.grad, beta, cx.s));
+    void* dq = row(W.dbig, r0[s], 3 * D);
+    TRY(wgrad(cx, dq, 3 * D, act, row(A.a1, r0[s], D), D, nr[s], 3 * D, D, G(dth, m, L.qkv.w), beta));
+    TRY(dgrad(cx, dq, 3 * D, nr[s], cx.P(L.qkv.w), D, 3 * D, D, rowf(W.dA, r0[s], D), D, F32));
+    TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, r0[s], nr[s], A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, W.p1,
+                   W.p2 + (size_t)nchunk * 2 * m.Dh, cx.s));
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D, cx.s));
+    TRY(reduce_per_sample(W.p2 + (size_t)nchunk * 2 * m.Dh, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0, cx.s));
+    // adaLN modulation: mod = SiLU(vec) W_mod^T + b
+    TRY(small_linear_bwd(W.dmod[s], mvec, 0, B, D, cx.P(L.mod.w), m.act, 6 * D, G(dth, m, L.mod.w),
+                         G(dth, m, L.mod.b), m.grad, beta, W.tmp, W.slpart, cx.s));
+    TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, cx.s));
+  }
+  return 0;
+}
+
+static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int B, Ws& W, void* dth, float beta) {
+  const Model& m = cx.m;
+  const int D = m.D, F = m.F, act = m.act, LD = 3 * D + F, LC = D + F;
+  const RowMap rm{B, m.nt, m.ni};
+  const int R = rm.rows();
+  const size_t es = dsize(act);
+  const SBlock& L = m.sgl[i];
+  const int nchunk = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
+  TRY(gate_bwd(W.g, A.y, act, D, rm, 0, R, A.mod, A.mod, 3 * D, 2 * D, W.dY, D, W.p1, W.p2, cx.s));
+  TRY(reduce_per_sample(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, 2 * D, cx.s));
+  TRY(reduce_to_grad(W.p2, D, 0, nchunk, D, G(dth, m, L.out.b), m.grad, beta, cx.s));
+  TRY(wgrad(cx, W.dY, D, act, A.cat, LC, R, D, LC, G(dth, m, L.out.w), beta));
+  // d[O, gelu(u)] = dY W_out: attention part, then the MLP part through GELU'
+  TRY(dgrad(cx, W.dY, D, R, cx.P(L.out.w), LC, D, D, W.dO, D, act));
+  TRY(dgrad(cx, W.dY, D, R, (const char*)cx.P(L.out.w) + (size_t)D * es, LC, D, F, (char*)W.dbig + 3 * D * es, LD,
+            act, EPI_GELU_BWD, (char*)A.proj + 3 * D * es, LD));
+  AttnBwd ab{A.Qh, A.Kh, A.Vh, A.cat, LC, W.dO, D, A.lse, W.delta, W.dQh, W.dKh, W.dVh, act, B, m.H, m.N, m.Dh, act, rm};
+  TRY(attention_bwd(ab, cx.s));
+  Gains gn{{cx.P(L.qg), cx.P(L.qg)}, {cx.P(L.kg), cx.P(L.kg)}};
+  TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.proj, LD, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
+                       A.rk, W.dbig, LD, W.p2, cx.s));
+  TRY(reduce_to_grad(W.p2, 2 * m.Dh, 0, nchunk, m.Dh, G(dth, m, L.qg), m.grad, beta, cx.s));
+  TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, 0, nchunk, m.Dh, G(dth, m, L.kg), m.grad, beta, cx.s));
+  TRY(colsum_partials(W.dbig, act, LD, LD, rm, 0, R, W.p1, cx.s));
+  TRY(reduce_to_grad(W.p1, LD, 0, nchunk, LD, G(dth, m, L.in.b), m.grad, beta, cx.s));
+  TRY(wgrad(cx, W.dbig, LD, act, A.a, D, R, LD, D, G(dth, m, L.in.w), beta));
+  TRY(dgrad(cx, W.dbig, LD, R, cx.P(L.in.w), D, LD, D, W.dA, D, F32));
+  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m, A.r, A.mod, A.mod, 3 * D, D, W.g, W.p1, W.p2, cx.s));
+  TRY(reduce_per_sample(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, D, cx.s));
+  TRY(reduce_per_sample(W.p2, D, rm, 0, R, W.dmod[0], 3 * D, 0, cx.s));
+  TRY(small_linear_bwd(W.dmod[0], mvec, 0, B, D, cx.P(L.mod.w), m.act, 3 * D, G(dth, m, L.mod.w), G(dth, m, L.mod.b),
+                       m.grad, beta, W.tmp, W.slpart, cx.s));
+  TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, cx.s));
+  return 0;
+}
+
+static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const void* cot, void* dth, float beta) {
+  const Model& m = ctx->m;
+  Ctx cx{m, ctx->stream, (const char*)theta, dsize(m.act)};
+  const int act = m.act, D = m.D;
+  const size_t es = dsize(act);
+  const RowMap rm{B, m.nt, m.ni};
+  const int rt = rm.rows_txt(), R = rm.rows();
+  const int nchunk = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
+  Ws W;
+  plan_ws(m, B, ctx->ws, W);
+  Saved S;
+  plan_saved(m, B, (void*)saved, S);
+  const Global& gl = S.g;
+  TRY(fill_zero(W.dmvec, (size_t)B * D * 4, cx.s));
+  if (m.c.block_only) {
+    TRY(convert(cot, act, W.g, F32, (size_t)R * D, cx.s));
+  } else {
+    // final layer: v = unpatchify((LN(x_img)(1 + scale) + shift) W_f^T + b_f)
+    TRY(patchify(cot, act, B, m.C, m.c.lat_h, m.c.lat_w, m.p, W.fout, cx.s));
+    const int Mi = B * m.ni;
+    const RowMap rimg{B, 0, m.ni};  // image rows only, as their own row space
+    TRY(colsum_partials(W.fout, act, m.pd, m.pd, rimg, 0, Mi, W.p1, cx.s));
+    TRY(reduce_to_grad(W.p1, m.pd, 0, Chunks{B, 0, m.ni, RED_ROWS}.count(), m.pd, G(dth, m, m.fin.b), m.grad, beta,
+                       cx.s));
+    TRY(wgrad(cx, W.fout, m.pd, act, (char*)gl.fa + (size_t)rt * D * es, D, Mi, m.pd, D, G(dth, m, m.fin.w), beta));
+    TRY(dgrad(cx, W.fout, m.pd, Mi, cx.P(m.fin.w), D, m.pd, D, W.dfa + (size_t)rt * D, D, F32));
+    TRY(fill_zero(W.g, (size_t)R * D * 4, cx.s));
+    void* xl = m.sgl.empty() ? (m.dbl.empty() ? gl.x0 : S.d.back().x_out) : S.s.back().x_out;
+    TRY(ln_mod_bwd(W.dfa, xl, act, D, rm, rt, R - rt, gl.fm, gl.fr, gl.fmod, gl.fmod, 2 * D, D, W.g, W.p1, W.p2,
+                   cx.s));
+    TRY(reduce_per_sample(W.p1, D, rm, rt, R - rt, W.dmod[0], 2 * D, D, cx.s));
+    TRY(reduce_per_sample(W.p2, D, rm, rt, R - rt, W.dmod[0], 2 * D, 0, cx.s));
+    TRY(small_linear_bwd(W.dmod[0], gl.mvec, 0, B, D, cx.P(m.fmod.w), act, 2 * D, G(dth, m, m.fmod.w),
+                         G(dth, m, m.fmod.b), m.grad, beta, W.tmp, W.slpart, cx.s));
+    TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, cx.s));
+  }
+  for (int i = m.c.n_single - 1; i >= 0; --i) {
+    SglAct A = S.s[i];
+    if (m.c.checkpoint) {
+      SglAct R2 = W.ss;
+      R2.x_in = S.s[i].x_in;
+      R2.x_out = W.xa;
+      TRY(sgl_fwd(cx, i, R2, gl.mvec, B));
+      A = R2;
+    }
+    TRY(sgl_bwd(cx, i, A, gl.mvec, B, W, dth, beta));
+  }
+  for (int i = m.c.n_double - 1; i >= 0; --i) {
+    DblAct A = S.d[i];
+    if (m.c.checkpoint) {
+      DblAct R2 = W.sd;
+      R2.x_in = S.d[i].x_in;
+      R2.x_out = W.xa;
+      TRY(dbl_fwd(cx, i, R2, gl.mvec, B));
+      A = R2;
+    }
+    TRY(dbl_bwd(cx, i, A, gl.mvec, B, W, dth, beta));
+  }
+  if (!m.c.block_only) {
+    // input embeddings (no gradient to the inputs themselves)
+    TRY(convert(W.g, F32, W.gact, act, (size_t)R * D, cx.s));
+    int c0, nc;
+    TRY(colsum_partials(W.g, F32, D, D, rm, rt, R - rt, W.p1, cx.s));
+    TRY(chunk_range(rm, rt, R - rt, &c0, &nc));
+    TRY(reduce_to_grad(W.p1, D, c0, nc, D, G(dth, m, m.img_in.b), m.grad, beta, cx.s));
+    TRY(wgrad(cx, (char*)W.gact + (size_t)rt * D * es, D, act, gl.patches, m.pd, B * m.ni, D, m.pd,
+              G(dth, m, m.img_in.w), beta));
+    TRY(colsum_partials(W.g, F32, D, D, rm, 0, rt, W.p1, cx.s));
+    TRY(chunk_range(rm, 0, rt, &c0, &nc));
+    TRY(reduce_to_grad(W.p1, D, c0, nc, D, G(dth, m, m.txt_in.b), m.grad, beta, cx.s));
+    TRY(wgrad(cx, W.gact, D, act, gl.txt, m.dtxt, rt, D, m.dtxt, G(dth, m, m.txt_in.w), beta));
+  }
+  (void)nchunk;
+  // time MLP: vec = SiLU(temb W1^T + b1) W2^T + b2; modulations read SiLU(vec)
+  TRY(mul_silu_grad(W.dmvec, gl.vec, (size_t)B * D, cx.s));
+  TRY(small_linear_bwd(W.dmvec, gl.sh1, 0, B, D, cx.P(m.t_out.w), act, D, G(dth, m, m.t_out.w), G(dth, m, m.t_out.b),
+                       m.grad, beta, W.dsh1, W.slpart, cx.s));
+  TRY(mul_silu_grad(W.dsh1, gl.h1, (size_t)B * D, cx.s));
+  TRY(small_linear_bwd(W.dsh1, gl.temb, 0, B, m.tf, cx.P(m.t_in.w), act, D, G(dth, m, m.t_in.w), G(dth, m, m.t_in.b),
+                       m.grad, beta, nullptr, W.slpart, cx.s));
+  return 0;
+}
+
+}  // namespace jg
+
+// ====================================================================== C ABI
+namespace {
+
+constexpr int MAX_BATCH = 32;
+
+jagg_status fail(jagg_status st, const std::string& msg) {
+  jg::set_error(msg);
+  return st;
+}
+
+jagg_status to_status(int rc) {
+  if (rc == 0) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+      jg::set_error(std::string("HIP error: ") + hipGetErrorString(e));
+      return JAGG_EDEVICE;
+    }
+    return JAGG_OK;
+  }
+  return (jagg_status)rc;
+}
+
+jagg_status need_ws(const jagg_ctx* ctx, int batch) {
+  jg::Ws W;
+  const size_t need = jg::plan_ws(ctx->m, batch, nullptr, W);
+  if (!ctx->ws || ctx->ws_bytes < need)
+    return fail(JAGG_EINVAL, "workspace not bound or smaller than dit_workspace_bytes(" + std::to_string(batch) +
+                                 ") = " + std::to_string(need));
+  return JAGG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* jagg_last_error(void) { return jg::get_error(); }
+
+jagg_status dit_param_layout(const dit_config* cfg, size_t* n_tensors, size_t* n_elems, jagg_tensor_desc* out,
+                             size_t cap) {
+  if (!cfg || !n_tensors || !n_elems) return fail(JAGG_EINVAL, "dit_param_layout: null argument");
+  jg::Model m;
+  if (jg::build_model(*cfg, m)) return JAGG_EINVAL;
+  *n_tensors = m.layout.size();
+  *n_elems = m.total;
+  if (out)
+    for (size_t i = 0; i < m.layout.size() && i < cap; ++i) out[i] = m.layout[i];
+  return JAGG_OK;
+}
+
+jagg_status jagg_ctx_create(const dit_config* cfg, void* hip_stream, jagg_ctx** out) {
+  if (!cfg || !out) return fail(JAGG_EINVAL, "jagg_ctx_create: null argument");
+  jagg_ctx* c = new (std::nothrow) jagg_ctx();
+  if (!c) return fail(JAGG_ENOMEM, "jagg_ctx_create: out of host memory");
+  if (jg::build_model(*cfg, c->m)) { delete c; return JAGG_EINVAL; }
+  c->stream = (hipStream_t)hip_stream;
+  *out = c;
+  return JAGG_OK;
+}
+
+void jagg_ctx_destroy(jagg_ctx* ctx) { delete ctx; }
+
+jagg_status dit_saved_bytes(const jagg_ctx* ctx, int batch, size_t* bytes) {
+  if (!ctx || !bytes) return fail(JAGG_EINVAL, "dit_saved_bytes: null argument");
+  if (batch < 1 || batch > MAX_BATCH) return fail(JAGG_EINVAL, "dit_saved_bytes: batch must be 1..32");
+  jg::Saved S;
+  *bytes = jg::plan_saved(ctx->m, batch, nullptr, S);
+  return JAGG_OK;
+}
+
+jagg_status dit_workspace_bytes(const jagg_ctx* ctx, int batch, size_t* bytes) {
+  if (!ctx || !bytes) return fail(JAGG_EINVAL, "dit_workspace_bytes: null argument");
+  if (batch < 1 || batch > MAX_BATCH) return fail(JAGG_EINVAL, "dit_workspace_bytes: batch must be 1..32");
+  jg::Ws W;
+  *bytes = jg::plan_ws(ctx->m, batch, nullptr, W);
+  return JAGG_OK;
+}
+
+jagg_status jagg_ctx_set_workspace(jagg_ctx* ctx, void* ws, size_t bytes) {
+  if (!ctx) return fail(JAGG_EINVAL, "jagg_ctx_set_workspace: null context");
+  if ((uintptr_t)ws % 256) return fail(JAGG_EINVAL, "jagg_ctx_set_workspace: workspace must be 256-byte aligned");
+  ctx->ws = ws;
+  ctx->ws_bytes = ws ? bytes : 0;
+  return JAGG_OK;
+}
+
+jagg_status dit_forward_save(jagg_ctx* ctx, const void* theta, const void* z, const float* t, const void* txt,
+                             void* v_out, void* saved, int batch) {
+  if (!ctx || !theta || !z || !t || !v_out) return fail(JAGG_EINVAL, "dit_forward_save: null argument");
+  if (!ctx->m.c.block_only && !txt) return fail(JAGG_EINVAL, "dit_forward_save: txt is required");
+  if (batch < 1 || batch > MAX_BATCH) return fail(JAGG_EINVAL, "dit_forward_save: batch must be 1..32");
+  if (((uintptr_t)theta | (uintptr_t)z | (uintptr_t)v_out | (uintptr_t)saved | (uintptr_t)txt) % 16)
+    return fail(JAGG_EINVAL, "dit_forward_save: device pointers must be 16-byte aligned");
+  jagg_status st = need_ws(ctx, batch);
+  if (st) return st;
+  return to_status(jg::forward(ctx, theta, z, t, txt, v_out, saved, batch));
+}
+
+jagg_status dit_vjp(jagg_ctx* ctx, const void* theta, const void* saved, int batch, const void* s, void* dtheta,
+                    float beta) {
+  if (!ctx || !theta || !saved || !s || !dtheta) return fail(JAGG_EINVAL, "dit_vjp: null argument");
+  if (batch < 1 || batch > MAX_BATCH) return fail(JAGG_EINVAL, "dit_vjp: batch must be 1..32");
+  if (beta != 0.f && beta != 1.f) return fail(JAGG_EINVAL, "dit_vjp: beta must be 0 or 1");
+  if (((uintptr_t)theta | (uintptr_t)saved | (uintptr_t)s | (uintptr_t)dtheta) % 16)
+    return fail(JAGG_EINVAL, "dit_vjp: device pointers must be 16-byte aligned");
+  jagg_status st = need_ws(ctx, batch);
+  if (st) return st;
+  return to_status(jg::vjp(ctx, theta, saved, batch, s, dtheta, beta));
+}
+
+jagg_status jagg_alpha(const float* t, int W, float* alpha_out) {
+  if (!t || !alpha_out) return fail(JAGG_EINVAL, "jagg_alpha: null argument");
+  if (W < 2) return fail(JAGG_EINVAL, "jagg_alpha: W must be >= 2");
+  const double t0 = t[0], den = (double)t[0] - (double)t[W - 1];
+  if (den == 0.0) return fail(JAGG_EINVAL, "jagg_alpha: t_0 == t_{W-1}");
+  for (int j = 0; j < W; ++j) alpha_out[j] = (float)((t0 - (double)t[j]) / den);
+  return JAGG_OK;
+}
+
+static jagg_status agg_weights(const float* t, int W, jg::AggArgs& a) {
+  if (W < 2 || W > 64) return fail(JAGG_EINVAL, "aggregation: W must be 2..64");
+  const double t0 = t[0], den = (double)t[0] - (double)t[W - 1];
+  if (den == 0.0) return fail(JAGG_EINVAL, "aggregation: t_0 == t_{W-1}");
+  for (int j = 0; j < W; ++j) {
+    const double al = (t0 - (double)t[j]) / den;
+    a.wb[j] = (float)(1.0 - al);
+    a.wc[j] = (float)al;
+  }
+  a.W = W;
+  return JAGG_OK;
+}
+
+jagg_status jagg_aggregate(jagg_ctx* ctx, const void* const* s, const float* t, int W, size_t n, int dtype,
+                           void* s_base, void* s_corr) {
+  if (!ctx || !s || !t || !s_base || !s_corr) return fail(JAGG_EINVAL, "jagg_aggregate: null argument");
+  if (dtype != JAGG_F32 && dtype != JAGG_BF16) return fail(JAGG_EINVAL, "jagg_aggregate: unknown dtype");
+  jg::AggArgs a;
+  std::memset(&a, 0, sizeof(a));
+  jagg_status st = agg_weights(t, W, a);
+  if (st) return st;
+  for (int j = 0; j < W; ++j) {
+    if (!s[j]) return fail(JAGG_EINVAL, "jagg_aggregate: null s_j");
+    a.s[j] = s[j];
+  }
+  a.n = n;
+  a.split = n;
+  a.base0 = a.base1 = s_base;
+  a.corr0 = a.corr1 = s_corr;
+  a.in_dt = a.out_dt = dtype;
+  return to_status(jg::aggregate(a, ctx->stream));
+}
+
+jagg_status jagg_group_scores(jagg_ctx* ctx, const void* const* h, size_t n, int W, int dtype, double* score_out) {
+  if (!ctx || !h || !score_out) return fail(JAGG_EINVAL, "jagg_group_scores: null argument");
+  if (W < 2 || W > 8) return fail(JAGG_EINVAL, "jagg_group_scores: W must be 2..8");
+  if (n == 0) return fail(JAGG_EINVAL, "jagg_group_scores: empty vectors");
+  if (dtype != JAGG_F32 && dtype != JAGG_BF16) return fail(JAGG_EINVAL, "jagg_group_scores: unknown dtype");
+  jg::Ws W0;
+  jg::plan_ws(ctx->m, 1, ctx->ws, W0);
+  const size_t need = jg::score_part_doubles(8) * sizeof(double) + 256;
+  if (!ctx->ws || ctx->ws_bytes < need) return fail(JAGG_EINVAL, "jagg_group_scores: workspace not bound");
+  jg::ScoreArgs a;
+  std::memset(&a, 0, sizeof(a));
+  for (int j = 0; j < W; ++j) {
+    if (!h[j]) return fail(JAGG_EINVAL, "jagg_group_scores: null h_j");
+    a.h[j] = h[j];
+  }
+  a.W = W;
+  a.n = n;
+  a.dt = dtype;
+  int rc = jg::group_scores(a, W0.spart, W0.score, ctx->stream);
+  if (rc) return (jagg_status)rc;
+  if (hipMemcpyAsync(score_out, W0.score, sizeof(double), hipMemcpyDeviceToHost, ctx->stream) != hipSuccess ||
+      hipStreamSynchronize(ctx->stream) != hipSuccess)
+    return fail(JAGG_EDEVICE, "jagg_group_scores: copy of the score failed");
+  return JAGG_OK;
+}
+
+jagg_status jagg_route(const double* scores, int n_groups, double tau, double frac, unsigned char* use_jagg_out,
+                       double* frac_out) {
+  if (!use_jagg_out || n_groups <= 0) return fail(JAGG_EINVAL, "jagg_route: bad arguments");
+  int n = 0;
+  if (frac >= 0.0) {
+    if (frac > 1.0) return fail(JAGG_EINVAL, "jagg_route: frac must lie in [0, 1]");
+    n = (int)std::floor(frac * n_groups + 1e-6);
+  } else {
+    if (!scores) return fail(JAGG_EINVAL, "jagg_route: scores required when frac < 0");
+    while (n < n_groups && scores[n] >= tau) ++n;
+  }
+  for (int g = 0; g < n_groups; ++g) use_jagg_out[g] = g < n ? 1 : 0;
+  if (frac_out) *frac_out = (double)n / n_groups;
+  return JAGG_OK;
+}
+
+jagg_status jagg_group_backward(jagg_ctx* ctx, const void* theta, const void* saved_pair, int batch,
+                                const void* const* s, const float* t, int W, void* dtheta, float beta) {
+  if (!ctx || !theta || !saved_pair || !s || !t || !dtheta) return fail(JAGG_EINVAL, "jagg_group_backward: null argument");
+  if (batch < 1 || 2 * batch > MAX_BATCH) return fail(JAGG_EINVAL, "jagg_group_backward: batch must be 1..16");
+  if (beta != 0.f && beta != 1.f) return fail(JAGG_EINVAL, "jagg_group_backward: beta must be 0 or 1");
+  const int B2 = 2 * batch;
+  jagg_status st = need_ws(ctx, B2);
+  if (st) return st;
+  const jg::Model& m = ctx->m;
+  jg::AggArgs a;
+  std::memset(&a, 0, sizeof(a));
+  st = agg_weights(t, W, a);
+  if (st) return st;
+  for (int j = 0; j < W; ++j) {
+    if (!s[j] || (uintptr_t)s[j] % 16) return fail(JAGG_EINVAL, "jagg_group_backward: null or unaligned s_j");
+    a.s[j] = s[j];
+  }
+  jg::Ws Wp;
+  jg::plan_ws(m, B2, ctx->ws, Wp);
+  const size_t es = jg::dsize(m.act);
+  char* cot = (char*)Wp.cot;
+  a.n = (size_t)batch * jg::out_elems(m);
+  if (m.c.block_only) {
+    const size_t txt = (size_t)batch * m.nt * m.D, img = (size_t)batch * m.ni * m.D;
+    a.split = txt;
+    a.base0 = cot;
+    a.corr0 = cot + txt * es;
+    a.base1 = cot + 2 * txt * es;
+    a.corr1 = cot + (2 * txt + img) * es;
+  } else {
+    a.split = a.n;
+    a.base0 = a.base1 = cot;
+    a.corr0 = a.corr1 = cot + a.n * es;
+  }
+  a.in_dt = a.out_dt = m.act;
+  int rc = jg::aggregate(a, ctx->stream);
+  if (rc) return (jagg_status)rc;
+  return to_status(jg::vjp(ctx, theta, saved_pair, B2, cot, dtheta, beta));
+}
+
+jagg_status perstep_group_backward(jagg_ctx* ctx, const void* theta, const void* const* saved, int batch,
+                                   const void* const* s, int W, void* dtheta, float beta) {
+  if (!ctx || !theta || !saved || !s || !dtheta) return fail(JAGG_EINVAL, "perstep_group_backward: null argument");
+  if (W < 1 || W > 64) return fail(JAGG_EINVAL, "perstep_group_backward: W must be 1..64");
+  for (int j = 0; j < W; ++j) {
+    jagg_status st = dit_vjp(ctx, theta, saved[j], batch, s[j], dtheta, j == 0 ? beta : 1.f);
+    if (st) return st;
+  }
+  return JAGG_OK;
+}
+
+}  // extern "C"

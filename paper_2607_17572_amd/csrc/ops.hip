@@ -1,0 +1,914 @@
+// Memory-bound kernels: adaLN / LayerNorm, gated residuals, q/k RMSNorm with
+// 2-D rotary embedding, deterministic chunked column reductions, the small-M
+// (batch) linear layers of the time MLP and modulation, and the JAGG
+// aggregation and group-score kernels.  All arithmetic is fp32 (scores fp64);
+// storage follows the activation dtype.
+#include "ops.h"
+
+namespace jg {
+
+#define LAUNCH_OK(name) JG_CHECK_LAUNCH(name)
+
+__device__ inline int sample_of(const RowMap& rm, int r) {
+  const int bt = rm.B * rm.nt;
+  return r < bt ? r / rm.nt : (r - bt) / rm.ni;
+}
+__device__ inline bool is_txt(const RowMap& rm, int r) { return r < rm.B * rm.nt; }
+
+// chunk q -> (first row, row count, sample)
+__device__ inline void chunk_rows(const Chunks& c, int q, int& r0, int& n, int& b) {
+  const int ct = c.ct(), ci = c.ci();
+  if (q < c.B * ct) {
+    b = q / ct;
+    const int k = q % ct;
+    r0 = b * c.nt + k * c.R;
+    n = min(c.R, c.nt - k * c.R);
+  } else {
+    const int q2 = q - c.B * ct;
+    b = q2 / ci;
+    const int k = q2 % ci;
+    r0 = c.B * c.nt + b * c.ni + k * c.R;
+    n = min(c.R, c.ni - k * c.R);
+  }
+}
+
+int chunk_range(RowMap rm, int row0, int nrows, int* c0, int* nc) {
+  Chunks c{rm.B, rm.nt, rm.ni, RED_ROWS};
+  const int bt = rm.rows_txt();
+  if (row0 == 0 && nrows == rm.rows()) { *c0 = 0; *nc = c.count(); return 0; }
+  if (row0 == 0 && nrows == bt) { *c0 = 0; *nc = rm.B * c.ct(); return 0; }
+  if (row0 == bt && nrows == rm.rows() - bt) { *c0 = rm.B * c.ct(); *nc = rm.B * c.ci(); return 0; }
+  set_error("chunk_range: row range must be one stream or all rows");
+  return 1;
+}
+
+// ================================================================ small linear
+template <typename TW>
+__global__ __launch_bounds__(256) void small_linear_fwd_k(const float* __restrict__ in, int B, int Din,
+                                                          const TW* __restrict__ W, const TW* __restrict__ bias,
+                                                          float* __restrict__ out, int Dout) {
+  const int lane = threadIdx.x & 63;
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= Dout) return;
+  const TW* w = W + (size_t)j * Din;
+  for (int b0 = 0; b0 < B; b0 += 8) {
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int d = lane; d < Din; d += 64) {
+      const float wv = ldf(w, d);
+#pragma unroll
+      for (int bb = 0; bb < 8; ++bb)
+        if (b0 + bb < B) acc[bb] = fmaf(wv, in[(size_t)(b0 + bb) * Din + d], acc[bb]);
+    }
+#pragma unroll
+    for (int bb = 0; bb < 8; ++bb) {
+      const float s = wave_sum(acc[bb]);
+      if (lane == 0 && b0 + bb < B) out[(size_t)(b0 + bb) * Dout + j] = s + (bias ? ldf(bias, j) : 0.f);
+    }
+  }
+}
+
+int small_linear_fwd(const float* in, int act, int B, int Din, const void* W, const void* bias, int w_dt,
+                     float* out, int Dout, hipStream_t s) {
+  if (act != 0 || B <= 0 || B > 64) { set_error("small_linear_fwd: bad batch/act"); return 1; }
+  dim3 grid((Dout + 3) / 4);
+  if (w_dt == BF16)
+    hipLaunchKernelGGL(small_linear_fwd_k<uint16_t>, grid, dim3(256), 0, s, in, B, Din, (const uint16_t*)W,
+                       (const uint16_t*)bias, out, Dout);
+  else
+    hipLaunchKernelGGL(small_linear_fwd_k<float>, grid, dim3(256), 0, s, in, B, Din, (const float*)W,
+                       (const float*)bias, out, Dout);
+  LAUNCH_OK("small_linear_fwd");
+  return 0;
+}
+
+constexpr int SL_JT = 64;   // output rows per tile
+constexpr int SL_DT = 256;  // input columns per tile (one per thread)
+constexpr int SL_MAXB = 32;
+
+size_t small_linear_bwd_part_floats(int B, int Din, int Dout) {
+  return (size_t)((Dout + SL_JT - 1) / SL_JT) * B * Din;
+}
+
+template <typename TW, typename TG>
+__global__ __launch_bounds__(256) void small_linear_bwd_k(const float* __restrict__ dout, const float* __restrict__ in,
+                                                          int B, int Din, const TW* __restrict__ W, int Dout,
+                                                          TG* __restrict__ dW, TG* __restrict__ db, float beta,
+                                                          float* __restrict__ part) {
+  __shared__ float sd[SL_MAXB][SL_JT];
+  const int jt = blockIdx.y, j0 = jt * SL_JT;
+  const int d = blockIdx.x * SL_DT + threadIdx.x;
+  for (int i = threadIdx.x; i < B * SL_JT; i += 256) {
+    const int b = i / SL_JT, jj = i % SL_JT;
+    sd[b][jj] = (j0 + jj < Dout) ? dout[(size_t)b * Dout + j0 + jj] : 0.f;
+  }
+  __syncthreads();
+  if (blockIdx.x == 0 && db) {
+    for (int jj = threadIdx.x; jj < SL_JT; jj += 256) {
+      if (j0 + jj >= Dout) continue;
+      float s = 0.f;
+      for (int b = 0; b < B; ++b) s += sd[b][jj];
+      if (beta != 0.f) s += beta * ldf(db, j0 + jj);
+      stf(db, j0 + jj, s);
+    }
+  }
+  if (d >= Din) return;
+  float x[SL_MAXB], acc[SL_MAXB];
+  for (int b = 0; b < B; ++b) { x[b] = in[(size_t)b * Din + d]; acc[b] = 0.f; }
+  const int jn = min(SL_JT, Dout - j0);
+  for (int jj = 0; jj < jn; ++jj) {
+    const size_t idx = (size_t)(j0 + jj) * Din + d;
+    const float w = ldf(W, idx);
+    float g = 0.f;
+    for (int b = 0; b < B; ++b) {
+      g = fmaf(sd[b][jj], x[b], g);
+      acc[b] = fmaf(sd[b][jj], w, acc[b]);
+    }
+    if (beta != 0.f) g += beta * ldf(dW, idx);
+    stf(dW, idx, g);
+  }
+  if (part)
+    for (int b = 0; b < B; ++b) part[((size_t)jt * B + b) * Din + d] = acc[b];
+}
+
+__global__ void sum_parts_k(const float* __restrict__ part, int nparts, size_t n, float* __restrict__ out) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int p = 0; p < nparts; ++p) s += part[(size_t)p * n + i];
+  out[i] = s;
+}
+
+int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din, const void* W, int w_dt,
+                     int Dout, void* dW, void* db, int g_dt, float beta, float* din, float* part,
+                     hipStream_t s) {
+  if (act != 0 || B <= 0 || B > SL_MAXB) { set_error("small_linear_bwd: batch must be 1..32"); return 1; }
+  const int njt = (Dout + SL_JT - 1) / SL_JT;
+  dim3 grid((Din + SL_DT - 1) / SL_DT, njt);
+  float* p = din ? part : nullptr;
+#define SLB(TW, TG)                                                                                  \
+  hipLaunchKernelGGL((small_linear_bwd_k<TW, TG>), grid, dim3(256), 0, s, dout, in, B, Din, (const TW*)W, \
+                     Dout, (TG*)dW, (TG*)db, beta, p)
+  if (w_dt == BF16 && g_dt == BF16) SLB(uint16_t, uint16_t);
+  else if (w_dt == BF16) SLB(uint16_t, float);
+  else if (g_dt == BF16) SLB(float, uint16_t);
+  else SLB(float, float);
+#undef SLB
+  LAUNCH_OK("small_linear_bwd");
+  if (din) {
+    const size_t n = (size_t)B * Din;
+    hipLaunchKernelGGL(sum_parts_k, dim3((n + 255) / 256), dim3(256), 0, s, part, njt, n, din);
+    LAUNCH_OK("small_linear_bwd_sum");
+  }
+  return 0;
+}
+
+// ================================================================ time embed
+__global__ void time_embed_k(TVals tv, int B, int F, float* temb) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int half = F / 2;
+  if (i >= B * half) return;
+  const int b = i / half, k = i % half;
+  // w_k = 10000^(-k/half); argument 1000 t w_k
+  const double w = exp(-log(10000.0) * (double)k / (double)half);
+  const double arg = 1000.0 * (double)tv.t[b] * w;
+  temb[(size_t)b * F + k] = (float)cos(arg);
+  temb[(size_t)b * F + half + k] = (float)sin(arg);
+}
+
+int time_embed(const TVals& tv, int B, int F, float* temb, hipStream_t s) {
+  if (B <= 0 || B > 64 || F % 2) { set_error("time_embed: bad batch or width"); return 1; }
+  const int n = B * F / 2;
+  hipLaunchKernelGGL(time_embed_k, dim3((n + 255) / 256), dim3(256), 0, s, tv, B, F, temb);
+  LAUNCH_OK("time_embed");
+  return 0;
+}
+
+__global__ void silu_k(const float* x, float* y, size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = silu(x[i]);
+}
+__global__ void mul_silu_grad_k(float* y, const float* x, size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] *= silu_grad(x[i]);
+}
+int silu_fwd(const float* x, float* y, size_t n, hipStream_t s) {
+  hipLaunchKernelGGL(silu_k, dim3((n + 255) / 256), dim3(256), 0, s, x, y, n);
+  LAUNCH_OK("silu");
+  return 0;
+}
+int mul_silu_grad(float* y, const float* x, size_t n, hipStream_t s) {
+  hipLaunchKernelGGL(mul_silu_grad_k, dim3((n + 255) / 256), dim3(256), 0, s, y, x, n);
+  LAUNCH_OK("mul_silu_grad");
+  return 0;
+}
+
+// ================================================================ LayerNorm + modulate
+constexpr int MAXC = 16;  // columns per thread (D <= 4096 with 256 threads)
+
+template <typename T>
+__global__ __launch_bounds__(256) void ln_mod_fwd_k(const T* __restrict__ x, int D, RowMap rm, int row0,
+                                                    const float* __restrict__ mt, const float* __restrict__ mi,
+                                                    int mod_w, int sh_off, int sc_off, T* __restrict__ a,
+                                                    float* __restrict__ mean, float* __restrict__ rstd) {
+  __shared__ float sh[16];
+  const int r = row0 + blockIdx.x;
+  const T* xr = x + (size_t)r * D;
+  float v[MAXC];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = threadIdx.x + i * 256;
+    v[i] = c < D ? ldf(xr, c) : 0.f;
+    s += v[i];
+  }
+  const float mu = block_sum(s, sh) / D;
+  float s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = threadIdx.x + i * 256;
+    const float dlt = c < D ? v[i] - mu : 0.f;
+    s2 += dlt * dlt;
+  }
+  const float var = block_sum(s2, sh) / D;
+  const float rs = rsqrtf(var + 1e-6f);
+  const int b = sample_of(rm, r);
+  const float* m = (is_txt(rm, r) ? mt : mi) + (size_t)b * mod_w;
+  T* ar = a + (size_t)r * D;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = threadIdx.x + i * 256;
+    if (c < D) stf(ar, c, (v[i] - mu) * rs * (1.f + m[sc_off + c]) + m[sh_off + c]);
+  }
+  if (threadIdx.x == 0) { mean[r] = mu; rstd[r] = rs; }
+}
+
+int ln_mod_fwd(const void* x, int act_dt, int D, RowMap rm, int row0, int nrows, const float* mod_txt,
+               const float* mod_img, int mod_w, int sh_off, int sc_off, void* a, float* mean, float* rstd,
+               hipStream_t s) {
+  if (D > 256 * MAXC) { set_error("ln_mod_fwd: hidden too large"); return 1; }
+  if (nrows <= 0) return 0;
+  if (act_dt == BF16)
+    hipLaunchKernelGGL(ln_mod_fwd_k<uint16_t>, dim3(nrows), dim3(256), 0, s, (const uint16_t*)x, D, rm, row0,
+                       mod_txt, mod_img, mod_w, sh_off, sc_off, (uint16_t*)a, mean, rstd);
+  else
+    hipLaunchKernelGGL(ln_mod_fwd_k<float>, dim3(nrows), dim3(256), 0, s, (const float*)x, D, rm, row0, mod_txt,
+                       mod_img, mod_w, sh_off, sc_off, (float*)a, mean, rstd);
+  LAUNCH_OK("ln_mod_fwd");
+  return 0;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA, const T* __restrict__ x, int D,
+                                                    Chunks ch, int c0, const float* __restrict__ mean,
+                                                    const float* __restrict__ rstd, const float* __restrict__ mt,
+                                                    const float* __restrict__ mi, int mod_w, int sc_off,
+                                                    float* __restrict__ g, float* __restrict__ psc,
+                                                    float* __restrict__ psh) {
+  __shared__ float sh[16];
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  const bool txt = r0 < ch.B * ch.nt;
+  const float* m = (txt ? mt : mi) + (size_t)b * mod_w + sc_off;
+  float scl[MAXC], asc[MAXC], ash[MAXC];
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = threadIdx.x + i * 256;
+    scl[i] = c < D ? 1.f + m[c] : 0.f;
+    asc[i] = 0.f;
+    ash[i] = 0.f;
+  }
+  for (int rr = 0; rr < n; ++rr) {
+    const int r = r0 + rr;
+    const float mu = mean[r], rs = rstd[r];
+    float xh[MAXC], dxh[MAXC];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = threadIdx.x + i * 256;
+      if (c < D) {
+        const float da = dA[(size_t)r * D + c];
+        xh[i] = (ldf(x, (size_t)r * D + c) - mu) * rs;
+        dxh[i] = da * scl[i];
+        asc[i] = fmaf(da, xh[i], asc[i]);
+        ash[i] += da;
+        s1 += dxh[i];
+        s2 += dxh[i] * xh[i];
+      } else {
+        xh[i] = dxh[i] = 0.f;
+      }
+    }
+    const float m1 = block_sum(s1, sh) / D;
+    const float m2 = block_sum(s2, sh) / D;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = threadIdx.x + i * 256;
+      if (c < D) g[(size_t)r * D + c] += rs * (dxh[i] - m1 - xh[i] * m2);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = threadIdx.x + i * 256;
+    if (c < D) {
+      psc[(size_t)q * D + c] = asc[i];
+      psh[(size_t)q * D + c] = ash[i];
+    }
+  }
+}
+
+int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int row0, int nrows,
+               const float* mean, const float* rstd, const float* mod_txt, const float* mod_img, int mod_w,
+               int sc_off, float* g, float* part_scale, float* part_shift, hipStream_t s) {
+  if (D > 256 * MAXC) { set_error("ln_mod_bwd: hidden too large"); return 1; }
+  int c0, nc;
+  if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
+  if (nc == 0) return 0;
+  Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (act_dt == BF16)
+    hipLaunchKernelGGL(ln_mod_bwd_k<uint16_t>, dim3(nc), dim3(256), 0, s, dA, (const uint16_t*)x, D, ch, c0, mean,
+                       rstd, mod_txt, mod_img, mod_w, sc_off, g, part_scale, part_shift);
+  else
+    hipLaunchKernelGGL(ln_mod_bwd_k<float>, dim3(nc), dim3(256), 0, s, dA, (const float*)x, D, ch, c0, mean, rstd,
+                       mod_txt, mod_img, mod_w, sc_off, g, part_scale, part_shift);
+  LAUNCH_OK("ln_mod_bwd");
+  return 0;
+}
+
+// ================================================================ gated residual
+template <typename T>
+__global__ void gated_residual_k(const T* __restrict__ xi, const T* __restrict__ y, int D, int ld_y, RowMap rm,
+                                 int row0, size_t n, const float* __restrict__ mt, const float* __restrict__ mi,
+                                 int mod_w, int gate_off, T* __restrict__ xo) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int r = row0 + (int)(i / D), c = (int)(i % D);
+  const int b = sample_of(rm, r);
+  const float gt = ((is_txt(rm, r) ? mt : mi) + (size_t)b * mod_w)[gate_off + c];
+  const size_t xidx = (size_t)r * D + c;
+  stf(xo, xidx, ldf(xi, xidx) + gt * ldf(y, (size_t)r * ld_y + c));
+}
+
+int gated_residual(const void* xi, const void* y, int act_dt, int D, int ld_y, RowMap rm, int row0, int nrows,
+                   const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* xo,
+                   hipStream_t s) {
+  const size_t n = (size_t)nrows * D;
+  if (n == 0) return 0;
+  dim3 grid((unsigned)((n + 255) / 256));
+  if (act_dt == BF16)
+    hipLaunchKernelGGL(gated_residual_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)xi, (const uint16_t*)y,
+                       D, ld_y, rm, row0, n, mod_txt, mod_img, mod_w, gate_off, (uint16_t*)xo);
+  else
+    hipLaunchKernelGGL(gated_residual_k<float>, grid, dim3(256), 0, s, (const float*)xi, (const float*)y, D, ld_y,
+                       rm, row0, n, mod_txt, mod_img, mod_w, gate_off, (float*)xo);
+  LAUNCH_OK("gated_residual");
+  return 0;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gate_bwd_k(const float* __restrict__ g, const T* __restrict__ y, int D,
+                                                  Chunks ch, int c0, const float* __restrict__ mt,
+                                                  const float* __restrict__ mi, int mod_w, int gate_off,
+                                                  T* __restrict__ dY, int ld_dy, float* __restrict__ pg,
+                                                  float* __restrict__ pb) {
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  const float* m = ((r0 < ch.B * ch.nt) ? mt : mi) + (size_t)b * mod_w + gate_off;
+  for (int c = threadIdx.x; c < D; c += 256) {
+    const float gt = m[c];
+    float sg = 0.f, sb = 0.f;
+    for (int rr = 0; rr < n; ++rr) {
+      const int r = r0 + rr;
+      const float gv = g[(size_t)r * D + c];
+      sg = fmaf(gv, ldf(y, (size_t)r * D + c), sg);
+      const float d = gv * gt;
+      sb += d;
+      stf(dY, (size_t)r * ld_dy + c, d);
+    }
+    pg[(size_t)q * D + c] = sg;
+    pb[(size_t)q * D + c] = sb;
+  }
+}
+
+int gate_bwd(const float* g, const void* y, int act_dt, int D, RowMap rm, int row0, int nrows,
+             const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* dY, int ld_dy,
+             float* part_gate, float* part_bias, hipStream_t s) {
+  int c0, nc;
+  if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
+  if (nc == 0) return 0;
+  Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (act_dt == BF16)
+    hipLaunchKernelGGL(gate_bwd_k<uint16_t>, dim3(nc), dim3(256), 0, s, g, (const uint16_t*)y, D, ch, c0, mod_txt,
+                       mod_img, mod_w, gate_off, (uint16_t*)dY, ld_dy, part_gate, part_bias);
+  else
+    hipLaunchKernelGGL(gate_bwd_k<float>, dim3(nc), dim3(256), 0, s, g, (const float*)y, D, ch, c0, mod_txt,
+                       mod_img, mod_w, gate_off, (float*)dY, ld_dy, part_gate, part_bias);
+  LAUNCH_OK("gate_bwd");
+  return 0;
+}
+
+// ================================================================ q/k norm + rope
+__device__ inline void tok_of_row(const RowMap& rm, int r, int& b, int& j) {
+  const int bt = rm.B * rm.nt;
+  if (r < bt) { b = r / rm.nt; j = r % rm.nt; }
+  else { b = (r - bt) / rm.ni; j = rm.nt + (r - bt) % rm.ni; }
+}
+
+// angle of rotation pair p for joint token j
+__device__ inline float rope_angle(const Rope& rp, int j, int p) {
+  float pos = 0.f;
+  const int quarter = rp.Dh / 4;
+  if (j >= rp.nt) {
+    const int i = j - rp.nt;
+    pos = (p < quarter) ? (float)(i / rp.gw) : (float)(i % rp.gw);
+  }
+  const int k = p % quarter;
+  const float freq = exp2f(-(2.f * k / (rp.Dh / 2)) * 13.287712379549449f);  // log2(1e4)
+  return pos * freq;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void qk_norm_rope_fwd_k(const T* __restrict__ proj, int ld, RowMap rm, Rope rp,
+                                                          Gains gn, T* __restrict__ Qh, T* __restrict__ Kh,
+                                                          T* __restrict__ Vh, float* __restrict__ rq,
+                                                          float* __restrict__ rk, int nitems) {
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= nitems) return;
+  const int lane = threadIdx.x & 63;
+  const int r = item / rp.H, h = item % rp.H;
+  const int D = rp.H * rp.Dh;
+  const bool act = lane < rp.Dh / 2;
+  const int p = act ? lane : 0;
+  const T* pr = proj + (size_t)r * ld;
+  const int st = r < rm.B * rm.nt ? 0 : 1;
+  const T* qg = (const T*)gn.q[st];
+  const T* kg = (const T*)gn.k[st];
+  float q0 = 0, q1 = 0, k0 = 0, k1 = 0;
+  if (act) {
+    q0 = ldf(pr, h * rp.Dh + 2 * p);
+    q1 = ldf(pr, h * rp.Dh + 2 * p + 1);
+    k0 = ldf(pr, D + h * rp.Dh + 2 * p);
+    k1 = ldf(pr, D + h * rp.Dh + 2 * p + 1);
+  }
+  const float riq = rsqrtf(wave_sum(q0 * q0 + q1 * q1) / rp.Dh + 1e-6f);
+  const float rik = rsqrtf(wave_sum(k0 * k0 + k1 * k1) / rp.Dh + 1e-6f);
+  if (lane == 0) { rq[(size_t)r * rp.H + h] = riq; rk[(size_t)r * rp.H + h] = rik; }
+  if (!act) return;
+  int b, j;
+  tok_of_row(rm, r, b, j);
+  const int N = rm.nt + rm.ni;
+  float sn, cs;
+  sincosf(rope_angle(rp, j, p), &sn, &cs);
+  const float qa = q0 * riq * ldf(qg, 2 * p), qb = q1 * riq * ldf(qg, 2 * p + 1);
+  const float ka = k0 * rik * ldf(kg, 2 * p), kb = k1 * rik * ldf(kg, 2 * p + 1);
+  const size_t o = (((size_t)b * rp.H + h) * N + j) * rp.Dh + 2 * p;
+  stf(Qh, o, qa * cs - qb * sn);
+  stf(Qh, o + 1, qa * sn + qb * cs);
+  stf(Kh, o, ka * cs - kb * sn);
+  stf(Kh, o + 1, ka * sn + kb * cs);
+  stf(Vh, o, ldf(pr, 2 * D + h * rp.Dh + 2 * p));
+  stf(Vh, o + 1, ldf(pr, 2 * D + h * rp.Dh + 2 * p + 1));
+}
+
+int qk_norm_rope_fwd(const void* proj, int ld, int act_dt, RowMap rm, Rope rp, Gains gn,
+                     void* Qh, void* Kh, void* Vh, float* rinv_q, float* rinv_k, hipStream_t s) {
+  if (rp.Dh > 128 || rp.Dh % 4) { set_error("qk_norm_rope: head_dim must be <= 128 and a multiple of 4"); return 1; }
+  const int nitems = rm.rows() * rp.H;
+  dim3 grid((nitems + 3) / 4);
+  if (act_dt == BF16)
+    hipLaunchKernelGGL(qk_norm_rope_fwd_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)proj, ld, rm, rp,
+                       gn, (uint16_t*)Qh, (uint16_t*)Kh, (uint16_t*)Vh,
+                       rinv_q, rinv_k, nitems);
+  else
+    hipLaunchKernelGGL(qk_norm_rope_fwd_k<float>, grid, dim3(256), 0, s, (const float*)proj, ld, rm, rp,
+                       gn, (float*)Qh, (float*)Kh, (float*)Vh, rinv_q, rinv_k,
+                       nitems);
+  LAUNCH_OK("qk_norm_rope_fwd");
+  return 0;
+}
+
+template <typename T, typename TD>
+__global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__ dQh, const TD* __restrict__ dKh,
+                                                          const TD* __restrict__ dVh, const T* __restrict__ proj,
+                                                          int ld, RowMap rm, Rope rp, Chunks ch, int c0,
+                                                          Gains gn, const float* __restrict__ rq, const float* __restrict__ rk,
+                                                          T* __restrict__ dproj, int ld_d, float* __restrict__ pgain) {
+  __shared__ float red[4][4][64];
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int D = rp.H * rp.Dh, N = rm.nt + rm.ni;
+  const bool act = lane < rp.Dh / 2;
+  const int p = act ? lane : 0;
+  const int st = r0 < ch.B * ch.nt ? 0 : 1;
+  const T* qg = (const T*)gn.q[st];
+  const T* kg = (const T*)gn.k[st];
+  float gq0 = 0, gq1 = 0, gk0 = 0, gk1 = 0;
+  const float qga = act ? ldf(qg, 2 * p) : 0.f, qgb = act ? ldf(qg, 2 * p + 1) : 0.f;
+  const float kga = act ? ldf(kg, 2 * p) : 0.f, kgb = act ? ldf(kg, 2 * p + 1) : 0.f;
+  for (int it = wave; it < n * rp.H; it += 4) {
+    const int r = r0 + it / rp.H, h = it % rp.H;
+    int bb, j;
+    tok_of_row(rm, r, bb, j);
+    const size_t o = (((size_t)bb * rp.H + h) * N + j) * rp.Dh + 2 * p;
+    const T* pr = proj + (size_t)r * ld;
+    T* dp = dproj + (size_t)r * ld_d;
+    float sn = 0.f, cs = 1.f;
+    if (act) sincosf(rope_angle(rp, j, p), &sn, &cs);
+    // q
+    float d0 = 0, d1 = 0, x0 = 0, x1 = 0;
+    if (act) {
+      const float a = ldf(dQh, o), c = ldf(dQh, o + 1);
+      d0 = a * cs + c * sn;
+      d1 = -a * sn + c * cs;
+      x0 = ldf(pr, h * rp.Dh + 2 * p);
+      x1 = ldf(pr, h * rp.Dh + 2 * p + 1);
+    }
+    float ri = rq[(size_t)r * rp.H + h];
+    float dot = wave_sum(d0 * qga * x0 + d1 * qgb * x1);
+    if (act) {
+      stf(dp, h * rp.Dh + 2 * p, d0 * qga * ri - x0 * ri * ri * ri * dot / rp.Dh);
+      stf(dp, h * rp.Dh + 2 * p + 1, d1 * qgb * ri - x1 * ri * ri * ri * dot / rp.Dh);
+      gq0 = fmaf(d0, x0 * ri, gq0);
+      gq1 = fmaf(d1, x1 * ri, gq1);
+    }
+    // k
+    if (act) {
+      const float a = ldf(dKh, o), c = ldf(dKh, o + 1);
+      d0 = a * cs + c * sn;
+      d1 = -a * sn + c * cs;
+      x0 = ldf(pr, D + h * rp.Dh + 2 * p);
+      x1 = ldf(pr, D + h * rp.Dh + 2 * p + 1);
+    }
+    ri = rk[(size_t)r * rp.H + h];
+    dot = wave_sum(d0 * kga * x0 + d1 * kgb * x1);
+    if (act) {
+      stf(dp, D + h * rp.Dh + 2 * p, d0 * kga * ri - x0 * ri * ri * ri * dot / rp.Dh);
+      stf(dp, D + h * rp.Dh + 2 * p + 1, d1 * kgb * ri - x1 * ri * ri * ri * dot / rp.Dh);
+      gk0 = fmaf(d0, x0 * ri, gk0);
+      gk1 = fmaf(d1, x1 * ri, gk1);
+      // v
+      stf(dp, 2 * D + h * rp.Dh + 2 * p, ldf(dVh, o));
+      stf(dp, 2 * D + h * rp.Dh + 2 * p + 1, ldf(dVh, o + 1));
+    }
+  }
+  red[wave][0][lane] = gq0;
+  red[wave][1][lane] = gq1;
+  red[wave][2][lane] = gk0;
+  red[wave][3][lane] = gk1;
+  __syncthreads();
+  if (threadIdx.x < 64 && act) {
+    float a[4] = {0, 0, 0, 0};
+    for (int w = 0; w < 4; ++w)
+      for (int k = 0; k < 4; ++k) a[k] += red[w][k][lane];
+    float* out = pgain + (size_t)q * 2 * rp.Dh;
+    out[2 * p] = a[0];
+    out[2 * p + 1] = a[1];
+    out[rp.Dh + 2 * p] = a[2];
+    out[rp.Dh + 2 * p + 1] = a[3];
+  }
+}
+
+int qk_norm_rope_bwd(const void* dQh, const void* dKh, const void* dVh, int dt_d, const void* proj, int ld,
+                     int act_dt, RowMap rm, Rope rp, Gains gn, const float* rinv_q,
+                     const float* rinv_k, void* dproj, int ld_d, float* part_gain, hipStream_t s) {
+  if (rp.Dh > 128 || rp.Dh % 4) { set_error("qk_norm_rope_bwd: head_dim"); return 1; }
+  int c0, nc;
+  if (chunk_range(rm, 0, rm.rows(), &c0, &nc)) return 1;
+  Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+#define QKB(T, TD)                                                                                            \
+  hipLaunchKernelGGL((qk_norm_rope_bwd_k<T, TD>), dim3(nc), dim3(256), 0, s, (const TD*)dQh, (const TD*)dKh,     \
+                     (const TD*)dVh, (const T*)proj, ld, rm, rp, ch, c0, gn, rinv_q, rinv_k, \
+                     (T*)dproj, ld_d, part_gain)
+  if (act_dt == BF16 && dt_d == BF16) QKB(uint16_t, uint16_t);
+  else if (act_dt == BF16) QKB(uint16_t, float);
+  else if (dt_d == BF16) QKB(float, uint16_t);
+  else QKB(float, float);
+#undef QKB
+  LAUNCH_OK("qk_norm_rope_bwd");
+  return 0;
+}
+
+// ================================================================ reductions
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_k(const T* __restrict__ X, int ld, int N, Chunks ch, int c0,
+                                                float* __restrict__ part) {
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  for (int c = threadIdx.x; c < N; c += 256) {
+    float s = 0.f;
+    for (int rr = 0; rr < n; ++rr) s += ldf(X, (size_t)(r0 + rr) * ld + c);
+    part[(size_t)q * N + c] = s;
+  }
+}
+
+int colsum_partials(const void* X, int dt, int ld, int N, RowMap rm, int row0, int nrows, float* part,
+                    hipStream_t s) {
+  int c0, nc;
+  if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
+  if (nc == 0) return 0;
+  Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (dt == BF16)
+    hipLaunchKernelGGL(colsum_k<uint16_t>, dim3(nc), dim3(256), 0, s, (const uint16_t*)X, ld, N, ch, c0, part);
+  else
+    hipLaunchKernelGGL(colsum_k<float>, dim3(nc), dim3(256), 0, s, (const float*)X, ld, N, ch, c0, part);
+  LAUNCH_OK("colsum");
+  return 0;
+}
+
+__global__ void reduce_per_sample_k(const float* __restrict__ part, int N, Chunks ch, int c0, int nc,
+                                    float* __restrict__ out, int out_stride, int out_off) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= ch.B * N) return;
+  const int b = i / N, c = i % N;
+  float s = 0.f;
+  for (int q = c0; q < c0 + nc; ++q) {
+    int r0, n, bq;
+    chunk_rows(ch, q, r0, n, bq);
+    if (bq == b) s += part[(size_t)q * N + c];
+  }
+  out[(size_t)b * out_stride + out_off + c] = s;
+}
+
+int reduce_per_sample(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
+                      int out_off, hipStream_t s) {
+  int c0, nc;
+  if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
+  Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  const int n = rm.B * N;
+  hipLaunchKernelGGL(reduce_per_sample_k, dim3((n + 255) / 256), dim3(256), 0, s, part, N, ch, c0, nc, out,
+                     out_stride, out_off);
+  LAUNCH_OK("reduce_per_sample");
+  return 0;
+}
+
+template <typename TG>
+__global__ void reduce_to_grad_k(const float* __restrict__ part, int ld, int chunk0, int nchunk, int N,
+                                 TG* __restrict__ g, float beta) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= N) return;
+  float s = 0.f;
+  for (int q = chunk0; q < chunk0 + nchunk; ++q) s += part[(size_t)q * ld + c];
+  if (beta != 0.f) s += beta * ldf(g, c);
+  stf(g, c, s);
+}
+
+int reduce_to_grad(const float* part, int ld, int chunk0, int nchunk, int N, void* g, int g_dt,
+                   float beta, hipStream_t s) {
+  dim3 grid((N + 255) / 256);
+  if (g_dt == BF16)
+    hipLaunchKernelGGL(reduce_to_grad_k<uint16_t>, grid, dim3(256), 0, s, part, ld, chunk0, nchunk, N, (uint16_t*)g,
+                       beta);
+  else
+    hipLaunchKernelGGL(reduce_to_grad_k<float>, grid, dim3(256), 0, s, part, ld, chunk0, nchunk, N, (float*)g, beta);
+  LAUNCH_OK("reduce_to_grad");
+  return 0;
+}
+
+// ================================================================ misc
+template <typename T>
+__global__ void patchify_k(const T* __restrict__ z, int B, int C, int Hh, int Ww, int p, T* __restrict__ out,
+                           bool inverse) {
+  const size_t n = (size_t)B * C * Hh * Ww;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int gw = Ww / p, gh = Hh / p, pd = C * p * p;
+  // i indexes the token-major tensor [B][gh*gw][pd]
+  const int f = (int)(i % pd);
+  const size_t tok = i / pd;
+  const int b = (int)(tok / ((size_t)gh * gw));
+  const int t = (int)(tok % ((size_t)gh * gw));
+  const int r = t / gw, c = t % gw;
+  const int ch = f / (p * p), py = (f / p) % p, px = f % p;
+  const size_t zi = (((size_t)b * C + ch) * Hh + r * p + py) * Ww + c * p + px;
+  if (!inverse) out[i] = z[zi];
+  else out[zi] = z[i];
+}
+
+int patchify(const void* z, int dt, int B, int C, int Hh, int Ww, int p, void* out, hipStream_t s) {
+  const size_t n = (size_t)B * C * Hh * Ww;
+  dim3 grid((unsigned)((n + 255) / 256));
+  if (dt == BF16)
+    hipLaunchKernelGGL(patchify_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)z, B, C, Hh, Ww, p,
+                       (uint16_t*)out, false);
+  else
+    hipLaunchKernelGGL(patchify_k<float>, grid, dim3(256), 0, s, (const float*)z, B, C, Hh, Ww, p, (float*)out,
+                       false);
+  LAUNCH_OK("patchify");
+  return 0;
+}
+
+int unpatchify(const void* x, int dt, int B, int C, int Hh, int Ww, int p, void* z, hipStream_t s) {
+  const size_t n = (size_t)B * C * Hh * Ww;
+  dim3 grid((unsigned)((n + 255) / 256));
+  if (dt == BF16)
+    hipLaunchKernelGGL(patchify_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)x, B, C, Hh, Ww, p,
+                       (uint16_t*)z, true);
+  else
+    hipLaunchKernelGGL(patchify_k<float>, grid, dim3(256), 0, s, (const float*)x, B, C, Hh, Ww, p, (float*)z, true);
+  LAUNCH_OK("unpatchify");
+  return 0;
+}
+
+__global__ void convert_k(const void* x, int dti, void* y, int dto, size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) st_any(y, dto, i, ld_any(x, dti, i));
+}
+int convert(const void* x, int dt_in, void* y, int dt_out, size_t n, hipStream_t s) {
+  if (!n) return 0;
+  hipLaunchKernelGGL(convert_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, dt_in, y, dt_out, n);
+  LAUNCH_OK("convert");
+  return 0;
+}
+
+__global__ void fill_zero_k(uint32_t* p, size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+int fill_zero(void* x, size_t bytes, hipStream_t s) {
+  if (bytes % 4) { set_error("fill_zero: size must be a multiple of 4 bytes"); return 1; }
+  const size_t n = bytes / 4;
+  if (!n) return 0;
+  hipLaunchKernelGGL(fill_zero_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (uint32_t*)x, n);
+  LAUNCH_OK("fill_zero");
+  return 0;
+}
+
+__global__ void add_into_k(float* y, const float* x, size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] += x[i];
+}
+int add_into(float* y, const float* x, size_t n, hipStream_t s) {
+  if (!n) return 0;
+  hipLaunchKernelGGL(add_into_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, x, n);
+  LAUNCH_OK("add_into");
+  return 0;
+}
+
+// ================================================================ aggregation
+// Each thread owns 8 consecutive elements per grid-stride step: W 16-byte (bf16)
+// or 32-byte (fp32) loads, fp32 FMA accumulation in j order, one rounding on
+// store.  HBM traffic per element: W reads + 2 writes.
+template <typename TI, typename TO>
+__global__ __launch_bounds__(256) void aggregate_k(AggArgs a) {
+  const size_t nv = a.n / 8;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < nv; v += stride) {
+    float sb[8], sc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sb[e] = sc[e] = 0.f;
+    for (int j = 0; j < a.W; ++j) {
+      float x[8];
+      const TI* p = (const TI*)a.s[j] + v * 8;
+      if constexpr (sizeof(TI) == 2) {
+        const uint4 u = *(const uint4*)p;
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { x[2 * e] = bf2f(w[e] & 0xffff); x[2 * e + 1] = bf2f(w[e] >> 16); }
+      } else {
+        const float4 u0 = *(const float4*)p, u1 = *(const float4*)(p + 4);
+        x[0] = u0.x; x[1] = u0.y; x[2] = u0.z; x[3] = u0.w;
+        x[4] = u1.x; x[5] = u1.y; x[6] = u1.z; x[7] = u1.w;
+      }
+      const float wb = a.wb[j], wc = a.wc[j];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { sb[e] = fmaf(wb, x[e], sb[e]); sc[e] = fmaf(wc, x[e], sc[e]); }
+    }
+    const size_t e0 = v * 8;
+    TO* db;
+    TO* dc;
+    if (e0 < a.split) { db = (TO*)a.base0 + e0; dc = (TO*)a.corr0 + e0; }
+    else { db = (TO*)a.base1 + (e0 - a.split); dc = (TO*)a.corr1 + (e0 - a.split); }
+    if constexpr (sizeof(TO) == 2) {
+      uint4 ub, uc;
+      ub.x = f2bf(sb[0]) | ((uint32_t)f2bf(sb[1]) << 16); ub.y = f2bf(sb[2]) | ((uint32_t)f2bf(sb[3]) << 16);
+      ub.z = f2bf(sb[4]) | ((uint32_t)f2bf(sb[5]) << 16); ub.w = f2bf(sb[6]) | ((uint32_t)f2bf(sb[7]) << 16);
+      uc.x = f2bf(sc[0]) | ((uint32_t)f2bf(sc[1]) << 16); uc.y = f2bf(sc[2]) | ((uint32_t)f2bf(sc[3]) << 16);
+      uc.z = f2bf(sc[4]) | ((uint32_t)f2bf(sc[5]) << 16); uc.w = f2bf(sc[6]) | ((uint32_t)f2bf(sc[7]) << 16);
+      *(uint4*)db = ub;
+      *(uint4*)dc = uc;
+    } else {
+      *(float4*)db = make_float4(sb[0], sb[1], sb[2], sb[3]);
+      *(float4*)(db + 4) = make_float4(sb[4], sb[5], sb[6], sb[7]);
+      *(float4*)dc = make_float4(sc[0], sc[1], sc[2], sc[3]);
+      *(float4*)(dc + 4) = make_float4(sc[4], sc[5], sc[6], sc[7]);
+    }
+  }
+}
+
+// scalar tail / unaligned path
+__global__ void aggregate_scalar_k(AggArgs a, size_t e_begin) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t e = e_begin + (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < a.n; e += stride) {
+    float sb = 0.f, sc = 0.f;
+    for (int j = 0; j < a.W; ++j) {
+      const float x = ld_any(a.s[j], a.in_dt, e);
+      sb = fmaf(a.wb[j], x, sb);
+      sc = fmaf(a.wc[j], x, sc);
+    }
+    if (e < a.split) { st_any(a.base0, a.out_dt, e, sb); st_any(a.corr0, a.out_dt, e, sc); }
+    else { st_any(a.base1, a.out_dt, e - a.split, sb); st_any(a.corr1, a.out_dt, e - a.split, sc); }
+  }
+}
+
+int aggregate(const AggArgs& a, hipStream_t s) {
+  if (a.W < 1 || a.W > 64) { set_error("aggregate: W must be 1..64"); return 1; }
+  if (a.n == 0) return 0;
+  bool vec = (a.n % 8 == 0) && (a.split % 8 == 0);
+  const uintptr_t al = (uintptr_t)a.base0 | (uintptr_t)a.base1 | (uintptr_t)a.corr0 | (uintptr_t)a.corr1;
+  vec = vec && (al % 16 == 0);
+  for (int j = 0; j < a.W; ++j) vec = vec && ((uintptr_t)a.s[j] % 16 == 0);
+  if (vec) {
+    const size_t nv = a.n / 8;
+    const unsigned grid = (unsigned)std::min<size_t>((nv + 255) / 256, 256 * 16);
+#define AGG(TI, TO) hipLaunchKernelGGL((aggregate_k<TI, TO>), dim3(grid), dim3(256), 0, s, a)
+    if (a.in_dt == BF16 && a.out_dt == BF16) AGG(uint16_t, uint16_t);
+    else if (a.in_dt == BF16) AGG(uint16_t, float);
+    else if (a.out_dt == BF16) AGG(float, uint16_t);
+    else AGG(float, float);
+#undef AGG
+  } else {
+    const unsigned grid = (unsigned)std::min<size_t>((a.n + 255) / 256, 256 * 16);
+    hipLaunchKernelGGL(aggregate_scalar_k, dim3(grid), dim3(256), 0, s, a, (size_t)0);
+  }
+  LAUNCH_OK("aggregate");
+  return 0;
+}
+
+// ================================================================ group scores
+// Pair products (i <= j) accumulated in fp64; one partial row per block, then a
+// single block sums partials in block order (deterministic).
+constexpr int SC_BLOCKS = 512;
+size_t score_part_doubles(int W) { return (size_t)SC_BLOCKS * (W * (W + 1) / 2); }
+
+template <int W>
+__global__ __launch_bounds__(256) void scores_pass1_k(ScoreArgs a, double* part) {
+  constexpr int P = W * (W + 1) / 2;
+  __shared__ double sh[4][P];
+  double acc[P];
+#pragma unroll
+  for (int k = 0; k < P; ++k) acc[k] = 0.0;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < a.n; e += stride) {
+    double x[W];
+#pragma unroll
+    for (int i = 0; i < W; ++i) x[i] = (double)ld_any(a.h[i], a.dt, e);
+    int k = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i)
+#pragma unroll
+      for (int j = i; j < W; ++j) acc[k++] += x[i] * x[j];
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int k = 0; k < P; ++k) {
+    double v = acc[k];
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0) sh[wv][k] = v;
+  }
+  __syncthreads();
+  for (int k = threadIdx.x; k < P; k += 256)
+    part[(size_t)blockIdx.x * P + k] = sh[0][k] + sh[1][k] + sh[2][k] + sh[3][k];
+}
+
+__global__ void scores_pass2_k(const double* part, int nblk, int W, double* score) {
+  __shared__ double tot[64];
+  const int P = W * (W + 1) / 2;
+  for (int k = threadIdx.x; k < P; k += blockDim.x) {
+    double s = 0.0;
+    for (int b = 0; b < nblk; ++b) s += part[(size_t)b * P + k];
+    tot[k] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    // index of (i, j), i <= j, in the row-major upper triangle
+    auto idx = [W](int i, int j) { return i * W - i * (i - 1) / 2 + (j - i); };
+    double s = 0.0;
+    int cnt = 0;
+    for (int i = 0; i < W; ++i)
+      for (int j = i + 1; j < W; ++j) {
+        s += tot[idx(i, j)] / (sqrt(tot[idx(i, i)]) * sqrt(tot[idx(j, j)]));
+        ++cnt;
+      }
+    *score = s / cnt;
+  }
+}
+
+int group_scores(const ScoreArgs& a, double* part, double* score_dev, hipStream_t s) {
+  if (a.W < 2 || a.W > 8) { set_error("group_scores: W must be 2..8"); return 1; }
+  if (a.n == 0) { set_error("group_scores: empty vectors"); return 1; }
+  const unsigned grid = SC_BLOCKS;
+  switch (a.W) {
+#define SCW(w) case w: hipLaunchKernelGGL(scores_pass1_k<w>, dim3(grid), dim3(256), 0, s, a, part); break;
+    SCW(2) SCW(3) SCW(4) SCW(5) SCW(6) SCW(7) SCW(8)
+#undef SCW
+  }
+  LAUNCH_OK("group_scores_pass1");
+  hipLaunchKernelGGL(scores_pass2_k, dim3(1), dim3(64), 0, s, part, (int)grid, a.W, score_dev);
+  LAUNCH_OK("group_scores_pass2");
+  return 0;
+}
+
+}  // namespace jg

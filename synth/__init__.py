@@ -91,3 +91,15 @@ def hidden_profile(W: int, n: int, rho: float, seed: int) -> np.ndarray:
     basis = orthonormal_rows(W + 1, n, seed)
     u, e = basis[0], basis[1:]
     return np.sqrt(rho) * u[None, :] + np.sqrt(1.0 - rho) * e
+
+
+def device_normal(shape, seed: int, std: float = 1.0, dtype=None, device="cuda"):
+    """N(0, std^2) drawn on the device with a seeded torch generator (for
+    full-size workloads, where host generation would dominate set-up time)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    if std != 1.0:
+        x.mul_(std)
+    return x if dtype is None else x.to(dtype)

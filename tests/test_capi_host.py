@@ -1,0 +1,109 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function declared in include/jagg.h, its parameter layout equals the
+oracle's, and the host-only routing and interpolation-weight calls agree with
+the oracle bit for bit."""
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2607_17572_amd as pk
+from oracle import jagg, mmdit
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib_or_skip():
+    if not os.path.exists(pk.api.LIB_PATH):
+        pytest.skip("libjagg.so not built")
+    return pk.lib()
+
+
+def test_library_exports_every_declared_function():
+    L = _lib_or_skip()
+    hdr = open(os.path.join(ROOT, "include", "jagg.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    names = set(re.findall(r"\b(\w+)\s*\([^;{]*\)\s*;", hdr))
+    names -= {"if", "while", "for", "return"}
+    assert {"dit_forward_save", "dit_vjp", "jagg_aggregate", "jagg_route", "jagg_group_backward"} <= names
+    for n in sorted(names):
+        assert hasattr(L, n), n
+
+
+def _oracle_cfg(c: pk.Config) -> mmdit.Config:
+    return mmdit.Config(n_double=c.n_double, n_single=c.n_single, hidden=c.hidden, heads=c.heads,
+                        head_dim=c.head_dim, mlp_hidden=c.mlp_hidden, in_ch=c.in_ch, patch=c.patch, lat_h=c.lat_h,
+                        lat_w=c.lat_w, n_txt=c.n_txt, txt_dim=c.txt_dim, t_freq_dim=c.t_freq_dim,
+                        block_only=bool(c.block_only))
+
+
+@pytest.mark.parametrize("name", ["tiny", "block", "slice", "flux", "qwen"])
+def test_param_layout_matches_oracle(name):
+    _lib_or_skip()
+    c = pk.config(name)
+    lay, total = pk.param_layout(c)
+    olay, ototal = mmdit.param_layout(_oracle_cfg(c))
+    assert total == ototal
+    assert len(lay) == len(olay)
+    for (n, off, numel, r, cc), (on, oshape, ooff) in zip(lay, olay):
+        assert n == on and off == ooff and numel == int(np.prod(oshape))
+        assert (r, cc) == (oshape if len(oshape) == 2 else (oshape[0], 1))
+
+
+def test_flux_like_parameter_count():
+    _lib_or_skip()
+    lay, _ = pk.param_layout(pk.config("flux"))
+    n = sum(x[2] for x in lay)
+    assert 11.5e9 < n < 12.2e9  # "~12B" full-depth Flux-like MMDiT
+
+
+def test_alpha_host_matches_oracle():
+    _lib_or_skip()
+    for t in ([1.0, 0.875, 0.75, 0.625], [0.5, 0.375, 0.25, 0.125], [0.9, 0.4],
+              list(np.float32(3 * np.array([1, .9, .8, .7, .6]) / (1 + 2 * np.array([1, .9, .8, .7, .6]))))):
+        a = pk.alpha(t)
+        want = jagg.alpha(np.asarray(t, dtype=np.float32).astype(np.float64)).astype(np.float32)
+        assert list(np.asarray(a, dtype=np.float32)) == list(want)
+        assert a[0] == 0.0 and a[-1] == 1.0
+    with pytest.raises(pk.JaggError):
+        pk.alpha([0.5])
+    with pytest.raises(pk.JaggError):
+        pk.alpha([0.5, 0.2, 0.5])
+
+
+def test_route_host_bit_exact_against_oracle():
+    _lib_or_skip()
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "jagg_quality.json")))
+    for m in g["models"].values():
+        mask, frac = pk.route(5, scores=m["cos"], tau=g["tau"])
+        omask, ofrac = jagg.route(5, scores=m["cos"], tau=g["tau"])
+        assert mask == list(omask) and frac == ofrac
+    rs = np.random.default_rng(0)
+    for _ in range(200):
+        n = int(rs.integers(1, 12))
+        sc = list(np.round(rs.uniform(0.3, 0.7, n), 3))
+        tau = float(rs.choice([0.4, 0.5, 0.6]))
+        mask, frac = pk.route(n, scores=sc, tau=tau)
+        omask, ofrac = jagg.route(n, scores=sc, tau=tau)
+        assert mask == list(omask) and frac == ofrac
+        fr = float(rs.choice([0.0, 0.2, 0.4, 0.5, 0.6, 0.75, 1.0]))
+        mask, frac = pk.route(n, frac=fr)
+        omask, ofrac = jagg.route(n, frac=fr)
+        assert mask == list(omask) and frac == ofrac
+
+
+def test_invalid_arguments_are_rejected_before_any_launch():
+    L = _lib_or_skip()
+    bad = pk.Config(n_double=1, n_single=0, hidden=64, heads=3, head_dim=16, mlp_hidden=64)  # 3*16 != 64
+    with pytest.raises(pk.JaggError) as e:
+        pk.param_layout(bad)
+    assert e.value.status == 1
+    with pytest.raises(pk.JaggError):
+        pk.route(0, frac=0.5)
+    with pytest.raises(pk.JaggError):
+        pk.route(3, frac=1.5)
+    import ctypes
+    assert L.dit_vjp(None, None, None, 1, None, None, 0.0) == 1
+    assert L.jagg_group_backward(None, None, None, 1, None, None, 4, None, 0.0) == 1

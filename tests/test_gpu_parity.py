@@ -1,0 +1,165 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle on the same
+seeded inputs.  fp32 path: relative L2 <= 1e-4; bf16 path: <= 2e-2 (the
+oracle is fed the same bf16-rounded parameters, inputs and upstream
+gradients); routing decisions bit-exact."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_17572_amd as pk
+import synth
+from harness import Case, compare_grads, rel_l2, rounded, to_dev
+from oracle import jagg, mmdit
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+TINY = pk.config("tiny")
+# multi-tile bf16 shapes with ragged row counts: 2*(40 + 64) = 208 rows per stream pair
+BLOCK_SMALL = pk.Config(n_double=1, n_single=0, hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_ch=16, patch=2,
+                        lat_h=16, lat_w=16, n_txt=40, txt_dim=256, t_freq_dim=256, block_only=1, act_dtype=pk.BF16,
+                        grad_dtype=pk.F32)
+FULL_SMALL = pk.Config(n_double=1, n_single=1, hidden=256, heads=2, head_dim=128, mlp_hidden=512, in_ch=16, patch=2,
+                       lat_h=16, lat_w=20, n_txt=24, txt_dim=128, t_freq_dim=256, act_dtype=pk.BF16, grad_dtype=pk.F32)
+
+
+# ------------------------------------------------------------------ fp32
+def test_tiny_fp32_forward_matches_oracle():
+    say("case: tiny fp32 forward")
+    cs = Case(TINY, B=1, W=4)
+    v, _ = cs.forward(0, saved=False)
+    want, _ = mmdit.forward(cs.oc, cs.P(), cs.inputs[0])
+    assert rel_l2(v.double().cpu().numpy(), want) < 1e-5
+
+
+def test_tiny_fp32_vjp_matches_oracle():
+    say("case: tiny fp32 vjp")
+    cs = Case(TINY, B=2, W=1, t=[0.7])
+    v, sv = cs.forward(0)
+    d = cs.new_grad()
+    cs.ctx.vjp(cs.theta_dev, sv, 2, cs.s_dev[0], d)
+    want = cs.oracle_exact()
+    eg, worst = compare_grads(cs, d, want, 1e-4)
+    say(f"tiny vjp rel L2 {eg:.2e}, worst tensor {worst}")
+
+
+def test_tiny_fp32_jagg_and_perstep_match_oracle():
+    say("case: tiny fp32 jagg/perstep W=4")
+    cs = Case(TINY, B=1, W=4)
+    compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 1e-4)
+    compare_grads(cs, cs.gpu_perstep(), cs.oracle_exact(), 1e-4)
+
+
+def test_tiny_fp32_second_window_and_accumulate():
+    """Gradient accumulation over windows: beta = 1 adds the second window."""
+    say("case: tiny fp32 two windows, accumulate")
+    w0 = Case(TINY, B=1, W=4, t=synth.uniform_grid(8)[:4])
+    w1 = Case(TINY, B=1, W=4, t=synth.uniform_grid(8)[4:], seed=0)
+    w1.theta_dev = w0.theta_dev
+    d = w0.gpu_jagg()
+    w1.gpu_perstep(dtheta=d, beta=1.0)
+    want = w0.oracle_jagg() + w1.oracle_exact()
+    compare_grads(w0, d, want, 1e-4)
+
+
+def test_w2_jagg_equals_perstep_on_gpu():
+    """W = 2: alpha = (0, 1), so the composites are s_0, s_1 and JAGG is exact."""
+    say("case: tiny fp32 W=2")
+    cs = Case(TINY, B=2, W=2)
+    a = cs.gpu_jagg().double().cpu().numpy()
+    b = cs.gpu_perstep().double().cpu().numpy()
+    assert rel_l2(a, b) < 1e-6
+
+
+# ------------------------------------------------------------------ bf16
+def test_bf16_block_jagg_matches_oracle():
+    say("case: bf16 block (D=256, ragged rows) jagg W=4 B=1")
+    cs = Case(BLOCK_SMALL, B=1, W=4)
+    eg, worst = compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 2e-2)
+    say(f"bf16 block jagg rel L2 {eg:.2e}, worst {worst}")
+
+
+def test_bf16_block_perstep_batch2_matches_oracle():
+    say("case: bf16 block perstep W=3 B=2")
+    cs = Case(BLOCK_SMALL, B=2, W=3)
+    compare_grads(cs, cs.gpu_perstep(), cs.oracle_exact(), 2e-2)
+
+
+def test_bf16_full_model_with_single_block_matches_oracle():
+    say("case: bf16 full model 1 double + 1 single")
+    cs = Case(FULL_SMALL, B=1, W=4)
+    eg, worst = compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 2e-2)
+    say(f"bf16 full jagg rel L2 {eg:.2e}, worst {worst}")
+    compare_grads(cs, cs.gpu_perstep(), cs.oracle_exact(), 2e-2)
+
+
+def test_checkpoint_recompute_is_bitwise_identical():
+    """Per-block activation checkpointing recomputes the block forward with the
+    same kernels, so the gradient is bitwise the one from saved activations."""
+    say("case: checkpoint vs saved")
+    a = Case(FULL_SMALL, B=1, W=4).gpu_jagg()
+    cfg = pk.Config(**{**FULL_SMALL.__dict__, "checkpoint": 1})
+    b = Case(cfg, B=1, W=4).gpu_jagg()
+    assert torch.equal(a, b)
+
+
+def test_determinism_bitwise():
+    say("case: determinism")
+    cs = Case(BLOCK_SMALL, B=1, W=4)
+    a = cs.gpu_jagg()
+    b = cs.gpu_jagg()
+    assert torch.equal(a, b)
+
+
+# ------------------------------------------------------------ aggregation
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("n,W", [(1, 4), (77, 4), (4096, 2), (100003, 5), (262144, 8)])
+def test_aggregate_matches_oracle(dt, n, W):
+    say(f"case: aggregate n={n} W={W} {dt}")
+    ctx = pk.Context(TINY)
+    t = np.asarray(synth.uniform_grid(2 * W)[:W], dtype=np.float32)
+    s_np = [rounded(synth.normal(n, 50 + j), dt) for j in range(W)]
+    s = [to_dev(x, dt) for x in s_np]
+    sb, sc = torch.empty_like(s[0]), torch.empty_like(s[0])
+    ctx.aggregate(s, t, sb, sc)
+    wb, wc = jagg.aggregate(s_np, t.astype(np.float64))
+    gb, gc = sb.double().cpu().numpy(), sc.double().cpu().numpy()
+    if dt == torch.float32:
+        # fp32 accumulation of W terms vs the fp64 definition
+        assert np.max(np.abs(gb - wb) / (np.abs(wb) + 1e-6)) < 1e-5
+        assert np.max(np.abs(gc - wc) / (np.abs(wc) + 1e-6)) < 1e-5
+    else:
+        # one rounding to bf16 of an fp32 sum: within one bf16 ulp
+        ulp = lambda x: np.maximum(np.abs(x), 1e-30) * 2.0 ** -7
+        assert np.all(np.abs(gb - wb) <= ulp(wb) + 1e-6)
+        assert np.all(np.abs(gc - wc) <= ulp(wc) + 1e-6)
+    if W == 2:
+        assert torch.equal(sb, s[0]) and torch.equal(sc, s[1])
+
+
+# ---------------------------------------------------------- routing scores
+def test_group_scores_and_routing_bit_exact():
+    say("case: group scores + routing")
+    ctx = pk.Context(TINY)
+    rhos = [0.97, 0.9, 0.81, 0.62, 0.4]
+    W, n = 4, 262144
+    scores, oscores = [], []
+    for g, rho in enumerate(rhos):
+        h = synth.hidden_profile(W, n, rho, seed=900 + g)
+        hd = [to_dev(x, torch.float32) for x in h]
+        hf = [x.double().cpu().numpy() for x in hd]
+        scores.append(ctx.group_score(hd))
+        oscores.append(jagg.group_score(hf))
+    for s, o, r in zip(scores, oscores, rhos):
+        assert abs(s - o) < 1e-9 and abs(s - r) < 1e-5
+    for tau in (0.5, 0.7, 0.85):
+        m, f = pk.route(len(rhos), scores=scores, tau=tau)
+        om, of = jagg.route(len(rhos), scores=oscores, tau=tau)
+        assert m == list(om) and f == of
