@@ -1,8 +1,437 @@
-// MFMA (bf16) flash attention for head dim 128 on gfx950.  Placeholder until
-// the MFMA kernels land: returns -1 so the caller takes the VALU kernels.
+// Flash attention forward and backward on gfx950 MFMA (bf16 in, fp32
+// accumulation), head dim 128.
+//
+// Layout trick: every score tile is computed in the orientation whose MFMA
+// accumulator can feed the next MFMA directly as its "B" operand.  With
+// v_mfma_f32_32x32x16_bf16 a lane holds one column j (lane % 32) of the 32x32
+// accumulator and 16 rows 8*(e/4) + 4*(lane/32) + e%4.  Taking the contraction
+// slots of the next product as those same rows, the 8 fp32 values
+// e = 8c .. 8c+7 of a lane are exactly its bf16 B fragment for 16-row block c,
+// provided the A operand is read with the same row order (two 8-byte LDS
+// reads at rows 16c + 4h and 16c + 8 + 4h).  Hence:
+//   forward:  S^T = K Q^T, O^T += V^T P^T   (query = lane column: softmax
+//             statistics and the rescale of O stay inside the lane)
+//   dK/dV:    S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dS
+//   dQ:       S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T
+// Softmax works in the log2 domain with the hardware exp2; the stored
+// log-sum-exp is in natural-log units of the scaled scores (shared with the
+// VALU kernels).  Ragged sequence lengths are masked (keys >= N get P = 0,
+// padded queries are not written).
 #include "attention.h"
 
 namespace jg {
-int attention_fwd_mfma(const AttnFwd&, hipStream_t) { return -1; }
-int attention_bwd_mfma(const AttnBwd&, hipStream_t) { return -1; }
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int DH = 128;
+constexpr float LOG2E = 1.4426950408889634f;
+constexpr float LN2 = 0.6931471805599453f;
+
+__device__ inline int row_of_tok_m(const RowMap& rm, int b, int j) {
+  return j < rm.nt ? b * rm.nt + j : rm.B * rm.nt + b * rm.ni + (j - rm.nt);
+}
+
+__device__ inline f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ inline f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+// 16-byte read of 8 bf16 at p (LDS or global)
+__device__ inline bf16x8 ld8(const uint16_t* p) { return __builtin_bit_cast(bf16x8, *(const u32x4*)p); }
+// two 8-byte reads at p and p + 8 elements (rows 16c+4h.. and 16c+8+4h..)
+__device__ inline bf16x8 ld4x2(const uint16_t* p) {
+  const u32x2 a = *(const u32x2*)p, b = *(const u32x2*)(p + 8);
+  u32x4 r = {a[0], a[1], b[0], b[1]};
+  return __builtin_bit_cast(bf16x8, r);
+}
+// accumulator values e = 8c .. 8c+7 as a bf16 B fragment
+__device__ inline bf16x8 pack8(const f32x16& v, int c) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (__bf16)v[8 * c + i];
+  return r;
+}
+
+// Stage a T x 128 tile (rows r0.., head-major rows of length 128) into LDS
+// S[r][d] (stride DS); rows >= nrows are zero.
+template <int T, int DS>
+__device__ inline void stage_rows(uint16_t* S, const uint16_t* G, int r0, int nrows) {
+  for (int v = threadIdx.x; v < T * (DH / 8); v += 256) {
+    const int r = v / (DH / 8), c = v % (DH / 8);
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (r0 + r < nrows) x = *(const u32x4*)(G + (size_t)(r0 + r) * DH + c * 8);
+    *(u32x4*)(S + r * DS + c * 8) = x;
+  }
+}
+// Same tile transposed: S[d][r] (stride TS)
+template <int T, int TS>
+__device__ inline void stage_rows_t(uint16_t* S, const uint16_t* G, int r0, int nrows) {
+  for (int v = threadIdx.x; v < T * (DH / 8); v += 256) {
+    const int r = v % T, c = v / T;
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (r0 + r < nrows) x = *(const u32x4*)(G + (size_t)(r0 + r) * DH + c * 8);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      S[(c * 8 + 2 * w) * TS + r] = (uint16_t)(x[w] & 0xffffu);
+      S[(c * 8 + 2 * w + 1) * TS + r] = (uint16_t)(x[w] >> 16);
+    }
+  }
+}
+// Token-major rows (the attention output layout): row j of sample b at
+// rows row_of_tok(b, j), columns h*128 ..
+template <int T, int DS>
+__device__ inline void stage_tok(uint16_t* S, const uint16_t* G, int ld, const RowMap& rm, int b, int h, int j0,
+                                 int N) {
+  for (int v = threadIdx.x; v < T * (DH / 8); v += 256) {
+    const int r = v / (DH / 8), c = v % (DH / 8);
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (j0 + r < N) x = *(const u32x4*)(G + (size_t)row_of_tok_m(rm, b, j0 + r) * ld + h * DH + c * 8);
+    *(u32x4*)(S + r * DS + c * 8) = x;
+  }
+}
+template <int T, int TS>
+__device__ inline void stage_tok_t(uint16_t* S, const uint16_t* G, int ld, const RowMap& rm, int b, int h, int j0,
+                                   int N) {
+  for (int v = threadIdx.x; v < T * (DH / 8); v += 256) {
+    const int r = v % T, c = v / T;
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (j0 + r < N) x = *(const u32x4*)(G + (size_t)row_of_tok_m(rm, b, j0 + r) * ld + h * DH + c * 8);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      S[(c * 8 + 2 * w) * TS + r] = (uint16_t)(x[w] & 0xffffu);
+      S[(c * 8 + 2 * w + 1) * TS + r] = (uint16_t)(x[w] >> 16);
+    }
+  }
+}
+
+// ============================================================== forward
+constexpr int F_QB = 128, F_KT = 64;
+constexpr int F_KS = DH + 8;    // K tile row stride
+constexpr int F_VS = F_KT + 8;  // V^T tile row stride
+
+__global__ __launch_bounds__(256) void attn_fwd_mfma_k(AttnFwd a) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[F_KT * F_KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[DH * F_VS];
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const int q = blockIdx.x * F_QB + w * 32 + c32;  // this lane's query
+  const size_t base = (size_t)bh * a.N * DH;
+  const uint16_t* Q = (const uint16_t*)a.Q + base;
+  const uint16_t* K = (const uint16_t*)a.K + base;
+  const uint16_t* V = (const uint16_t*)a.V + base;
+  const float sc = rsqrtf((float)DH) * LOG2E;
+
+  bf16x8 qf[8];
+#pragma unroll
+  for (int kb = 0; kb < 8; ++kb) {
+    if (q < a.N) qf[kb] = ld8(Q + (size_t)q * DH + kb * 16 + h * 8);
+    else qf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+  }
+  f32x16 o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = zero16();
+  float m = -INFINITY, l = 0.f;
+
+  for (int k0 = 0; k0 < a.N; k0 += F_KT) {
+    __syncthreads();
+    stage_rows<F_KT, F_KS>(Ks, K, k0, a.N);
+    stage_rows_t<F_KT, F_VS>(Vt, V, k0, a.N);
+    __syncthreads();
+    f32x16 st[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      st[t] = zero16();
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) st[t] = mfma(ld8(Ks + (32 * t + c32) * F_KS + kb * 16 + h * 8), qf[kb], st[t]);
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3);
+        const float s = key < a.N ? st[t][e] * sc : -INFINITY;
+        st[t][e] = s;
+        mx = fmaxf(mx, s);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m, mx);
+    const float corr = __builtin_amdgcn_exp2f(m - mn);
+    float ls = 0.f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float p = __builtin_amdgcn_exp2f(st[t][e] - mn);
+        st[t][e] = p;
+        ls += p;
+      }
+    l = l * corr + ls;
+    m = mn;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[i][e] *= corr;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const bf16x8 pb = pack8(st[c >> 1], c & 1);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) o[dt] = mfma(ld4x2(Vt + (32 * dt + c32) * F_VS + 16 * c + 4 * h), pb, o[dt]);
+    }
+  }
+  l += __shfl_xor(l, 32, 64);
+  if (q >= a.N) return;
+  const float inv = 1.f / l;
+  uint16_t* O = (uint16_t*)a.O + (size_t)row_of_tok_m(a.rm, b, q) * a.ld_o + hd * DH;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(o[dt][4 * g + i] * inv);
+      *(bf16x4*)(O + 32 * dt + 8 * g + 4 * h) = v;
+    }
+  if (h == 0) a.lse[(size_t)bh * a.N + q] = (m + __log2f(l)) * LN2;
+}
+
+// ============================================================== delta
+// delta[b][h][j] = sum_d dO[j][h*128+d] * O[j][h*128+d]; one wave per row,
+// 16 lanes per head, 16-byte loads.
+__global__ __launch_bounds__(256) void attn_delta_mfma_k(AttnBwd a) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int rows = a.rm.rows();
+  if (r >= rows) return;
+  const int bt = a.rm.B * a.rm.nt;
+  int b, j;
+  if (r < bt) { b = r / a.rm.nt; j = r % a.rm.nt; }
+  else { b = (r - bt) / a.rm.ni; j = a.rm.nt + (r - bt) % a.rm.ni; }
+  const uint16_t* O = (const uint16_t*)a.O + (size_t)r * a.ld_o;
+  const uint16_t* G = (const uint16_t*)a.dO + (size_t)r * a.ld_do;
+  const int D = a.H * DH;
+  for (int c0 = 0; c0 < D; c0 += 512) {
+    const int c = c0 + lane * 8;
+    float s = 0.f;
+    if (c < D) {
+      const u32x4 x = *(const u32x4*)(O + c), y = *(const u32x4*)(G + c);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        s = fmaf(bf2f(x[w] & 0xffffu), bf2f(y[w] & 0xffffu), s);
+        s = fmaf(bf2f(x[w] >> 16), bf2f(y[w] >> 16), s);
+      }
+    }
+    s += __shfl_xor(s, 1, 64);
+    s += __shfl_xor(s, 2, 64);
+    s += __shfl_xor(s, 4, 64);
+    s += __shfl_xor(s, 8, 64);
+    if ((lane & 15) == 0 && c < D) {
+      const int hd = c / DH;
+      a.delta[((size_t)b * a.H + hd) * a.N + j] = s;
+    }
+  }
+}
+
+// ============================================================== dK, dV
+constexpr int KV_KB = 128, KV_QT = 32;
+constexpr int KV_S = DH + 8;       // [q][d] tiles
+constexpr int KV_T = KV_QT + 8;    // [d][q] tiles
+
+__global__ __launch_bounds__(256) void attn_bwd_kv_mfma_k(AttnBwd a) {
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[KV_QT * KV_S];
+  __shared__ __attribute__((aligned(16))) uint16_t Gs[KV_QT * KV_S];
+  __shared__ __attribute__((aligned(16))) uint16_t Qt[DH * KV_T];
+  __shared__ __attribute__((aligned(16))) uint16_t Gt[DH * KV_T];
+  __shared__ float Ls[KV_QT], Ds[KV_QT];
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const int key = blockIdx.x * KV_KB + w * 32 + c32;
+  const size_t base = (size_t)bh * a.N * DH;
+  const uint16_t* Q = (const uint16_t*)a.Q + base;
+  const uint16_t* K = (const uint16_t*)a.K + base;
+  const uint16_t* V = (const uint16_t*)a.V + base;
+  const float sc = rsqrtf((float)DH);
+
+  bf16x8 kf[8], vf[8];
+#pragma unroll
+  for (int kb = 0; kb < 8; ++kb) {
+    if (key < a.N) {
+      kf[kb] = ld8(K + (size_t)key * DH + kb * 16 + h * 8);
+      vf[kb] = ld8(V + (size_t)key * DH + kb * 16 + h * 8);
+    } else {
+      kf[kb] = vf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    }
+  }
+  f32x16 dv[4], dk[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
+
+  for (int q0 = 0; q0 < a.N; q0 += KV_QT) {
+    __syncthreads();
+    stage_rows<KV_QT, KV_S>(Qs, Q, q0, a.N);
+    stage_rows_t<KV_QT, KV_T>(Qt, Q, q0, a.N);
+    stage_tok<KV_QT, KV_S>(Gs, (const uint16_t*)a.dO, a.ld_do, a.rm, b, hd, q0, a.N);
+    stage_tok_t<KV_QT, KV_T>(Gt, (const uint16_t*)a.dO, a.ld_do, a.rm, b, hd, q0, a.N);
+    if (threadIdx.x < KV_QT) {
+      const int qq = q0 + threadIdx.x;
+      Ls[threadIdx.x] = qq < a.N ? a.lse[(size_t)bh * a.N + qq] : INFINITY;
+      Ds[threadIdx.x] = qq < a.N ? a.delta[(size_t)bh * a.N + qq] : 0.f;
+    }
+    __syncthreads();
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int kb = 0; kb < 8; ++kb) {
+      s = mfma(ld8(Qs + c32 * KV_S + kb * 16 + h * 8), kf[kb], s);
+      dp = mfma(ld8(Gs + c32 * KV_S + kb * 16 + h * 8), vf[kb], dp);
+    }
+    // lane: key column, query rows 8(e/4) + 4h + e%4
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 L4 = *(const float4*)(Ls + 8 * g + 4 * h);
+      const float4 D4 = *(const float4*)(Ds + 8 * g + 4 * h);
+      const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 4 * g + i;
+        const float p = __builtin_amdgcn_exp2f((s[e] * sc - Lv[i]) * LOG2E);
+        s[e] = p;
+        dp[e] = p * (dp[e] - Dv[i]);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const bf16x8 pb = pack8(s, c), db = pack8(dp, c);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        dv[dt] = mfma(ld4x2(Gt + (32 * dt + c32) * KV_T + 16 * c + 4 * h), pb, dv[dt]);
+        dk[dt] = mfma(ld4x2(Qt + (32 * dt + c32) * KV_T + 16 * c + 4 * h), db, dk[dt]);
+      }
+    }
+  }
+  if (key >= a.N) return;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 vk, vv;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        vk[i] = (__bf16)(dk[dt][4 * g + i] * sc);
+        vv[i] = (__bf16)dv[dt][4 * g + i];
+      }
+      const size_t off = base + (size_t)key * DH + 32 * dt + 8 * g + 4 * h;
+      *(bf16x4*)((uint16_t*)a.dK + off) = vk;
+      *(bf16x4*)((uint16_t*)a.dV + off) = vv;
+    }
+}
+
+// ============================================================== dQ
+constexpr int Q_QB = 128, Q_KT = 32;
+constexpr int Q_S = DH + 8;
+constexpr int Q_T = Q_KT + 8;
+
+__global__ __launch_bounds__(256) void attn_bwd_q_mfma_k(AttnBwd a) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[Q_KT * Q_S];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[Q_KT * Q_S];
+  __shared__ __attribute__((aligned(16))) uint16_t Kt[DH * Q_T];
+  const int bh = blockIdx.y, b = bh / a.H;
+  const int hd = bh % a.H;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const int q = blockIdx.x * Q_QB + w * 32 + c32;
+  const size_t base = (size_t)bh * a.N * DH;
+  const uint16_t* Q = (const uint16_t*)a.Q + base;
+  const uint16_t* K = (const uint16_t*)a.K + base;
+  const uint16_t* V = (const uint16_t*)a.V + base;
+  const float sc = rsqrtf((float)DH);
+
+  bf16x8 qf[8], gf[8];
+  const bool qv = q < a.N;
+  const uint16_t* G = (const uint16_t*)a.dO + (qv ? (size_t)row_of_tok_m(a.rm, b, q) * a.ld_do + hd * DH : 0);
+#pragma unroll
+  for (int kb = 0; kb < 8; ++kb) {
+    if (qv) {
+      qf[kb] = ld8(Q + (size_t)q * DH + kb * 16 + h * 8);
+      gf[kb] = ld8(G + kb * 16 + h * 8);
+    } else {
+      qf[kb] = gf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    }
+  }
+  const float L = qv ? a.lse[(size_t)bh * a.N + q] * LOG2E : INFINITY;
+  const float Dl = qv ? a.delta[(size_t)bh * a.N + q] : 0.f;
+  f32x16 dq[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dq[i] = zero16();
+
+  for (int k0 = 0; k0 < a.N; k0 += Q_KT) {
+    __syncthreads();
+    stage_rows<Q_KT, Q_S>(Ks, K, k0, a.N);
+    stage_rows<Q_KT, Q_S>(Vs, V, k0, a.N);
+    stage_rows_t<Q_KT, Q_T>(Kt, K, k0, a.N);
+    __syncthreads();
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int kb = 0; kb < 8; ++kb) {
+      s = mfma(ld8(Ks + c32 * Q_S + kb * 16 + h * 8), qf[kb], s);
+      dp = mfma(ld8(Vs + c32 * Q_S + kb * 16 + h * 8), gf[kb], dp);
+    }
+    // lane: query column, key rows 8(e/4) + 4h + e%4
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int kk = k0 + 8 * (e >> 2) + 4 * h + (e & 3);
+      const float p = kk < a.N ? __builtin_amdgcn_exp2f(s[e] * sc * LOG2E - L) : 0.f;
+      dp[e] = p * (dp[e] - Dl);
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const bf16x8 db = pack8(dp, c);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(ld4x2(Kt + (32 * dt + c32) * Q_T + 16 * c + 4 * h), db, dq[dt]);
+    }
+  }
+  if (!qv) return;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(dq[dt][4 * g + i] * sc);
+      *(bf16x4*)((uint16_t*)a.dQ + base + (size_t)q * DH + 32 * dt + 8 * g + 4 * h) = v;
+    }
+}
+
+// ============================================================== dispatch
+static bool mfma_ok(int Dh, int dt, const void* O, int ld_o) {
+  return Dh == DH && dt == BF16 && ((uintptr_t)O % 16 == 0) && (ld_o % 8 == 0);
+}
+
+int attention_fwd_mfma(const AttnFwd& a, hipStream_t s) {
+  if (!mfma_ok(a.Dh, a.dt, a.O, a.ld_o)) return -1;
+  dim3 grid((a.N + F_QB - 1) / F_QB, a.B * a.H);
+  hipLaunchKernelGGL(attn_fwd_mfma_k, grid, dim3(256), 0, s, a);
+  JG_CHECK_LAUNCH("attention_fwd_mfma");
+  return 0;
+}
+
+int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
+  if (!mfma_ok(a.Dh, a.dt, a.dO, a.ld_do) || a.dt_d != BF16 || (uintptr_t)a.O % 16 || a.ld_o % 8) return -1;
+  hipLaunchKernelGGL(attn_delta_mfma_k, dim3((a.rm.rows() + 3) / 4), dim3(256), 0, s, a);
+  JG_CHECK_LAUNCH("attention_delta_mfma");
+  hipLaunchKernelGGL(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0, s, a);
+  JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
+  hipLaunchKernelGGL(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0, s, a);
+  JG_CHECK_LAUNCH("attention_bwd_q_mfma");
+  return 0;
+}
+
 }  // namespace jg

@@ -250,12 +250,12 @@ int attention_fwd(const AttnFwd& a, hipStream_t s) {
 
 int attention_bwd(const AttnBwd& a, hipStream_t s) {
   if (a.N <= 0 || a.B <= 0 || a.H <= 0) { set_error("attention_bwd: empty problem"); return 1; }
+  const int rc = attention_bwd_mfma(a, s);
+  if (rc >= 0) return rc;
   const size_t n = (size_t)a.B * a.H * a.N;
   if (a.dt == BF16) hipLaunchKernelGGL(attn_delta_k<uint16_t>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   else hipLaunchKernelGGL(attn_delta_k<float>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   JG_CHECK_LAUNCH("attention_delta");
-  const int rc = attention_bwd_mfma(a, s);
-  if (rc >= 0) return rc;
   switch (a.Dh) {
     case 16: bwd_valu<16>(a, s); break;
     case 32: bwd_valu<32>(a, s); break;

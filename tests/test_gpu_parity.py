@@ -131,15 +131,15 @@ def test_aggregate_matches_oracle(dt, n, W):
     ctx.aggregate(s, t, sb, sc)
     wb, wc = jagg.aggregate(s_np, t.astype(np.float64))
     gb, gc = sb.double().cpu().numpy(), sc.double().cpu().numpy()
-    if dt == torch.float32:
-        # fp32 accumulation of W terms vs the fp64 definition
-        assert np.max(np.abs(gb - wb) / (np.abs(wb) + 1e-6)) < 1e-5
-        assert np.max(np.abs(gc - wc) / (np.abs(wc) + 1e-6)) < 1e-5
-    else:
-        # one rounding to bf16 of an fp32 sum: within one bf16 ulp
-        ulp = lambda x: np.maximum(np.abs(x), 1e-30) * 2.0 ** -7
-        assert np.all(np.abs(gb - wb) <= ulp(wb) + 1e-6)
-        assert np.all(np.abs(gc - wc) <= ulp(wc) + 1e-6)
+    a = jagg.alpha(t.astype(np.float64))
+    # error bound of W fused multiply-adds in fp32 (weights rounded to fp32 too):
+    # (W + 1) * 2^-24 * sum_j |w_j s_j|, plus one rounding of the result to the
+    # storage dtype (half an ulp: 2^-24 fp32, 2^-8 bf16, relative)
+    mag_b = sum(abs(1 - a[j]) * np.abs(s_np[j]) for j in range(W))
+    mag_c = sum(abs(a[j]) * np.abs(s_np[j]) for j in range(W))
+    rnd = 2.0 ** -24 if dt == torch.float32 else 2.0 ** -8
+    assert np.all(np.abs(gb - wb) <= (W + 1) * 2.0 ** -24 * mag_b + rnd * np.abs(wb) + 1e-30)
+    assert np.all(np.abs(gc - wc) <= (W + 1) * 2.0 ** -24 * mag_c + rnd * np.abs(wc) + 1e-30)
     if W == 2:
         assert torch.equal(sb, s[0]) and torch.equal(sc, s[1])
 
