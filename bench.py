@@ -44,6 +44,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--only", choices=["all", "jagg"], default="all",
+                    help="jagg: time the JAGG windows only (for a kernel trace of exactly those launches)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
@@ -110,11 +112,30 @@ def main():
 
     for _ in range(args.warmup):
         run_jagg()
-        run_perstep()
+        if args.only == "all":
+            run_perstep()
     t_jagg = timed(run_jagg, args.steps)
-    t_ps = timed(run_perstep, args.steps)
+    t_ps = timed(run_perstep, args.steps) if args.only == "all" else float("nan")
     print(f"[bench] jagg {1e3 * t_jagg / args.steps:.3f} ms/window, per-step {1e3 * t_ps / args.steps:.3f} ms/window",
           file=sys.stderr, flush=True)
+
+    # dominant kernel: the weight-gradient GEMMs (the products that contract
+    # over the token rows of both endpoints).  Live HIP-event timing of every
+    # launch of that class over K JAGG windows, on the library's stream.
+    kernels = {}
+    for name, cls in (("gemm_wgrad", pk.PROF_GEMM_WGRAD), ("gemm_dgrad", pk.PROF_GEMM_DGRAD),
+                      ("attn_bwd_kv", pk.PROF_ATTN_BWD_KV), ("attn_bwd_q", pk.PROF_ATTN_BWD_Q),
+                      ("aggregate", pk.PROF_AGGREGATE)):
+        pk.prof_begin(cls)
+        for _ in range(args.steps):
+            run_jagg()
+        n, ms, work = pk.prof_end()
+        kernels[name] = {"launches_per_window": n // args.steps, "avg_us": 1e3 * ms / max(n, 1),
+                         "work_per_window": work / args.steps, "ms_per_window": ms / args.steps}
+    wg = kernels["gemm_wgrad"]
+    achieved = wg["work_per_window"] / (wg["ms_per_window"] * 1e-3) / 1e12
+    agg = kernels["aggregate"]
+    print(f"[bench] kernels {json.dumps(kernels)}", file=sys.stderr, flush=True)
 
     ms_jagg = 1e3 * t_jagg / args.steps
     ms_ps = 1e3 * t_ps / args.steps
@@ -137,14 +158,57 @@ def main():
         "config": {"workload": "one double-stream MMDiT block, hidden 3072, 24x128 heads, MLP 12288, "
                                "4096 image + 512 text tokens, batch 1, W=4 (JAGG joint endpoint pair)",
                    "W": W, "batch": B, "tokens": N, "hidden": D},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s",
+                     "frac": achieved * 1e12 / MFMA_BF16_PEAK, "traffic": None,
+                     "kernel": "gemm_mfma_kernel (weight-gradient GEMMs, dW = dY^T X)",
+                     "avg_launch_us": wg["avg_us"], "launches_per_window": wg["launches_per_window"]},
         "perstep": {"value": W * args.steps / t_ps, "ms_per_window": ms_ps},
         "speedup_vs_perstep": t_ps / t_jagg,
         "tflops_jagg": fl_pair / (ms_jagg * 1e-3) / 1e12,
         "tflops_perstep": W * fl_one / (ms_ps * 1e-3) / 1e12,
         "forward_ms_per_step": fwd_ms,
+        "aggregate_gbps": agg["work_per_window"] / (agg["ms_per_window"] * 1e-3) / 1e9,
+        "kernels": kernels,
     }
     out["mfma_frac_whole_backward"] = out["tflops_jagg"] * 1e12 / MFMA_BF16_PEAK
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(cfg, theta, xs, ss, t, W)
     print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, theta, xs, ss, t, W):
+    """The oracle, timed on this host on a bounded sample of the same workload:
+    the composites of one window plus ONE endpoint VJP (batch 1, full size, fp32),
+    scaled to the window (two endpoint VJPs) and reported in steps/s."""
+    import numpy as np
+    import threadpoolctl
+    from oracle import jagg as ojagg, mmdit
+
+    oc = mmdit.Config(n_double=cfg.n_double, n_single=0, hidden=cfg.hidden, heads=cfg.heads,
+                      head_dim=cfg.head_dim, mlp_hidden=cfg.mlp_hidden, in_ch=cfg.in_ch, patch=cfg.patch,
+                      lat_h=cfg.lat_h, lat_w=cfg.lat_w, n_txt=cfg.n_txt, txt_dim=cfg.txt_dim,
+                      t_freq_dim=cfg.t_freq_dim, block_only=True)
+    nt, ni, D = cfg.n_txt, cfg.n_img, cfg.hidden
+    P = mmdit.unflatten(oc, theta.float().cpu().numpy(), np.float32)
+    x0 = xs[0].float().cpu().numpy()
+    inp = mmdit.Inputs(t=np.array([t[0]]), x_txt=x0[:nt][None], x_img=x0[nt:][None])
+    s_np = [s.float().cpu().numpy() for s in ss]
+    print("[bench] oracle forward (untimed)", file=sys.stderr, flush=True)
+    _, cache = mmdit.forward(oc, P, inp)
+    info = threadpoolctl.threadpool_info()
+    cores = max([i.get("num_threads", 1) for i in info] + [1])
+    t0 = time.perf_counter()
+    sb, sc = ojagg.aggregate(s_np, np.asarray(t, dtype=np.float64), acc_dtype=np.float32)
+    t_agg = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    mmdit.vjp(oc, P, cache, (sb[:nt][None], sb[nt:][None]))
+    t_vjp = time.perf_counter() - t0
+    t_window = t_agg + 2.0 * t_vjp
+    print(f"[bench] oracle: aggregate {t_agg:.2f}s, one endpoint VJP {t_vjp:.2f}s", file=sys.stderr, flush=True)
+    return {"value": W / t_window, "unit": "steps/s", "cores": cores, "kind": "oracle",
+            "sample": "numpy fp32 oracle: composites of one W=4 window + one batch-1 endpoint VJP of the "
+                      "full-size block, timed; window = composites + 2 endpoint VJPs",
+            "seconds_measured": t_agg + t_vjp}
 
 
 if __name__ == "__main__":

@@ -163,6 +163,21 @@ jagg_status jagg_group_backward(jagg_ctx* ctx, const void* theta, const void* sa
 jagg_status perstep_group_backward(jagg_ctx* ctx, const void* theta, const void* const* saved, int batch,
                                    const void* const* s, int W, void* dtheta, float beta);
 
+/* Measurement hook (no effect on results).  jagg_prof_begin(cls) arms one
+ * kernel class for this process; every later launch of that class, on any
+ * context, is bracketed by a pair of HIP events on its stream.
+ * jagg_prof_end synchronises those events, returns the launch count, the
+ * summed kernel time in ms and the summed algorithmic work of the launches
+ * (FLOPs: 2 per multiply-add of the defining products; bytes for the
+ * aggregation: W reads + 2 writes per element), and disarms.
+ * Classes: 1 forward GEMM (Y = X W^T), 2 input-gradient GEMM (dX = dY W),
+ * 3 weight-gradient GEMM (dW = dY^T X), 4 attention forward (work: the QK^T
+ * and PV products), 5 attention backward dK/dV kernel (work: the dV, dP and
+ * dK products; the score recompute is not counted), 6 attention backward dQ
+ * kernel (work: the dQ product), 7 aggregation. */
+jagg_status jagg_prof_begin(int cls);
+jagg_status jagg_prof_end(long* launches, double* total_ms, double* total_work);
+
 #ifdef __cplusplus
 }
 #endif

@@ -62,6 +62,10 @@ def lib() -> ctypes.CDLL:
             fn.restype = ctypes.c_int
         L.jagg_ctx_destroy.argtypes = [vp]
         L.jagg_ctx_destroy.restype = None
+        L.jagg_prof_begin.argtypes = [i]
+        L.jagg_prof_begin.restype = ctypes.c_int
+        L.jagg_prof_end.argtypes = [ctypes.POINTER(ctypes.c_long), ctypes.POINTER(d), ctypes.POINTER(d)]
+        L.jagg_prof_end.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -136,6 +140,22 @@ def route(n_groups: int, frac: float | None = None, scores=None, tau: float = 0.
     fr = ctypes.c_double()
     _check(lib().jagg_route(sc, n_groups, float(tau), -1.0 if frac is None else float(frac), mask, ctypes.byref(fr)))
     return list(mask), fr.value
+
+
+PROF_GEMM_FWD, PROF_GEMM_DGRAD, PROF_GEMM_WGRAD = 1, 2, 3
+PROF_ATTN_FWD, PROF_ATTN_BWD_KV, PROF_ATTN_BWD_Q, PROF_AGGREGATE = 4, 5, 6, 7
+
+
+def prof_begin(cls: int):
+    """Arm HIP-event timing of every launch of kernel class ``cls``."""
+    _check(lib().jagg_prof_begin(cls))
+
+
+def prof_end():
+    """(launches, total kernel ms, total algorithmic work) of the armed class."""
+    n, ms, work = ctypes.c_long(), ctypes.c_double(), ctypes.c_double()
+    _check(lib().jagg_prof_end(ctypes.byref(n), ctypes.byref(ms), ctypes.byref(work)))
+    return n.value, ms.value, work.value
 
 
 def _ptrs(tensors):

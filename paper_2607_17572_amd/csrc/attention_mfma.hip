@@ -18,6 +18,7 @@
 // VALU kernels).  Ragged sequence lengths are masked (keys >= N get P = 0,
 // padded queries are not written).
 #include "attention.h"
+#include "prof.h"
 
 namespace jg {
 
@@ -418,7 +419,10 @@ static bool mfma_ok(int Dh, int dt, const void* O, int ld_o) {
 int attention_fwd_mfma(const AttnFwd& a, hipStream_t s) {
   if (!mfma_ok(a.Dh, a.dt, a.O, a.ld_o)) return -1;
   dim3 grid((a.N + F_QB - 1) / F_QB, a.B * a.H);
+  const double nn = (double)a.B * a.H * a.N * (double)a.N * DH;
+  const int pi = prof_begin(PROF_ATTN_FWD, s);
   hipLaunchKernelGGL(attn_fwd_mfma_k, grid, dim3(256), 0, s, a);
+  prof_end(pi, s, 4.0 * nn);
   JG_CHECK_LAUNCH("attention_fwd_mfma");
   return 0;
 }
@@ -427,9 +431,14 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   if (!mfma_ok(a.Dh, a.dt, a.dO, a.ld_do) || a.dt_d != BF16 || (uintptr_t)a.O % 16 || a.ld_o % 8) return -1;
   hipLaunchKernelGGL(attn_delta_mfma_k, dim3((a.rm.rows() + 3) / 4), dim3(256), 0, s, a);
   JG_CHECK_LAUNCH("attention_delta_mfma");
+  const double nn = (double)a.B * a.H * a.N * (double)a.N * DH;
+  int pi = prof_begin(PROF_ATTN_BWD_KV, s);
   hipLaunchKernelGGL(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0, s, a);
+  prof_end(pi, s, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
+  pi = prof_begin(PROF_ATTN_BWD_Q, s);
   hipLaunchKernelGGL(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0, s, a);
+  prof_end(pi, s, 2.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_q_mfma");
   return 0;
 }

@@ -17,6 +17,7 @@
 // Anything else (fp32 operands, contiguous dims not multiple of 8) takes a
 // plain LDS-tiled VALU kernel with fp32 accumulation.
 #include "gemm.h"
+#include "prof.h"
 
 namespace jg {
 
@@ -269,9 +270,25 @@ static int launch_mfma(const GemmArgs& g, hipStream_t s) {
   return 0;
 }
 
-static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+static int prof_class(const GemmArgs& g) {
+  if (!g.ta && !g.tb) return PROF_GEMM_FWD;
+  if (!g.ta && g.tb) return PROF_GEMM_DGRAD;
+  if (g.ta && g.tb) return PROF_GEMM_WGRAD;
+  return PROF_NONE;
+}
+
+static int gemm_launch(const GemmArgs& g, hipStream_t s);
 
 int gemm(const GemmArgs& g, hipStream_t s) {
+  const int pi = prof_begin(prof_class(g), s);
+  const int rc = gemm_launch(g, s);
+  prof_end(pi, s, 2.0 * g.M * g.N * (double)g.K);
+  return rc;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   if (g.M < 0 || g.N < 0 || g.K < 0 || !g.A || !g.B || !g.epi.C) {
     set_error("gemm: invalid arguments");
     return 1;

@@ -4,6 +4,7 @@
 // aggregation and group-score kernels.  All arithmetic is fp32 (scores fp64);
 // storage follows the activation dtype.
 #include "ops.h"
+#include "prof.h"
 
 namespace jg {
 
@@ -820,6 +821,7 @@ int aggregate(const AggArgs& a, hipStream_t s) {
   const uintptr_t al = (uintptr_t)a.base0 | (uintptr_t)a.base1 | (uintptr_t)a.corr0 | (uintptr_t)a.corr1;
   vec = vec && (al % 16 == 0);
   for (int j = 0; j < a.W; ++j) vec = vec && ((uintptr_t)a.s[j] % 16 == 0);
+  const int pi = prof_begin(PROF_AGGREGATE, s);
   if (vec) {
     const size_t nv = a.n / 8;
     const unsigned grid = (unsigned)std::min<size_t>((nv + 255) / 256, 256 * 16);
@@ -833,6 +835,7 @@ int aggregate(const AggArgs& a, hipStream_t s) {
     const unsigned grid = (unsigned)std::min<size_t>((a.n + 255) / 256, 256 * 16);
     hipLaunchKernelGGL(aggregate_scalar_k, dim3(grid), dim3(256), 0, s, a, (size_t)0);
   }
+  prof_end(pi, s, (double)a.n * ((double)a.W * dsize(a.in_dt) + 2.0 * dsize(a.out_dt)));
   LAUNCH_OK("aggregate");
   return 0;
 }

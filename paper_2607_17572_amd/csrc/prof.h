@@ -1,0 +1,23 @@
+// Per-kernel-class launch timing with HIP events (measurement only).
+#pragma once
+#include "common.h"
+
+namespace jg {
+
+enum ProfClass {
+  PROF_NONE = 0,
+  PROF_GEMM_FWD = 1,    // Y = X W^T
+  PROF_GEMM_DGRAD = 2,  // dX = dY W
+  PROF_GEMM_WGRAD = 3,  // dW = dY^T X
+  PROF_ATTN_FWD = 4,
+  PROF_ATTN_BWD_KV = 5,
+  PROF_ATTN_BWD_Q = 6,
+  PROF_AGGREGATE = 7,
+};
+
+// Returns a record index (>= 0) when class `cls` is being profiled, else -1.
+int prof_begin(int cls, hipStream_t s);
+// Closes record `idx` and attributes `work` (flops or bytes) to it.
+void prof_end(int idx, hipStream_t s, double work);
+
+}  // namespace jg
