@@ -40,5 +40,7 @@ struct GemmArgs {
 
 // Returns 0 on success, 1 on invalid arguments, 3 on a launch error.
 int gemm(const GemmArgs& g, hipStream_t s);
+// Tile configuration used by the MFMA kernel (tuning hook; 0 = default).
+void gemm_set_tile_cfg(int c);
 
 }  // namespace jg

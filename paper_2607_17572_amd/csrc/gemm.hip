@@ -56,6 +56,17 @@ __device__ inline void tile_coords(int id, int tiles_m, int tiles_n, int& tm, in
 }
 
 // ------------------------------------------------------------ tile loaders
+// Operands are read through buffer resources: an out-of-range offset returns
+// zero, so ragged edges cost a select per load instead of a branch.
+constexpr int OOB = 0x7ffffff0;
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, (int)bytes, 0x00020000);
+}
+__device__ inline u32x4 bload(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
 // Loads a ROWS x BK tile of an operand into registers and stores it into LDS
 // as S[row * LDSK + k].
 template <int ROWS, int BK, int NT, bool T>
@@ -66,16 +77,14 @@ struct Loader<ROWS, BK, NT, false> {  // P[row * ld + k], vectors along k
   static constexpr int NVEC = ROWS * BK / 8;
   static constexpr int NV = (NVEC + NT - 1) / NT;
   u32x4 r[NV];
-  __device__ inline void load(const uint16_t* P, int ld, int row0, int nrows, int k0, int K) {
+  __device__ inline void load(__amdgpu_buffer_rsrc_t P, int ld, int row0, int nrows, int k0, int K) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int v = threadIdx.x + i * NT;
       const int row = v / (BK / 8), kv = v % (BK / 8);
       const int gr = row0 + row, gk = k0 + kv * 8;
-      if (v < NVEC && gr < nrows && gk < K)
-        r[i] = *(const u32x4*)(P + (size_t)gr * ld + gk);
-      else
-        r[i] = u32x4{0u, 0u, 0u, 0u};
+      const bool ok = (NVEC % NT == 0 || v < NVEC) && gr < nrows && gk < K;
+      r[i] = bload(P, ok ? (gr * ld + gk) * 2 : OOB);
     }
   }
   template <int LDSK>
@@ -83,7 +92,7 @@ struct Loader<ROWS, BK, NT, false> {  // P[row * ld + k], vectors along k
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int v = threadIdx.x + i * NT;
-      if (v < NVEC) {
+      if (NVEC % NT == 0 || v < NVEC) {
         const int row = v / (BK / 8), kv = v % (BK / 8);
         *(u32x4*)(S + row * LDSK + kv * 8) = r[i];
       }
@@ -96,19 +105,19 @@ struct Loader<ROWS, BK, NT, true> {  // P[k * ld + row], 8x8 blocks transposed i
   static constexpr int NBLK = (ROWS / 8) * (BK / 8);
   static constexpr int NB = (NBLK + NT - 1) / NT;
   u32x4 r[NB * 8];
-  __device__ inline void load(const uint16_t* P, int ld, int row0, int nrows, int k0, int K) {
+  __device__ inline void load(__amdgpu_buffer_rsrc_t P, int ld, int row0, int nrows, int k0, int K) {
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int b = threadIdx.x + i * NT;
-      const int kb = b / (ROWS / 8), rb = b % (ROWS / 8);
+      // lanes vary the k block fastest: the 16 lanes of a 16-byte LDS store
+      // group then cover 8 k blocks x 2 row parities = 16 distinct bank groups
+      const int kb = b % (BK / 8), rb = b / (BK / 8);
       const int gr = row0 + rb * 8;
+      const bool okb = (NBLK % NT == 0 || b < NBLK) && gr < nrows;
 #pragma unroll
       for (int kk = 0; kk < 8; ++kk) {
         const int gk = k0 + kb * 8 + kk;
-        if (b < NBLK && gr < nrows && gk < K)
-          r[i * 8 + kk] = *(const u32x4*)(P + (size_t)gk * ld + gr);
-        else
-          r[i * 8 + kk] = u32x4{0u, 0u, 0u, 0u};
+        r[i * 8 + kk] = bload(P, (okb && gk < K) ? (gk * ld + gr) * 2 : OOB);
       }
     }
   }
@@ -117,8 +126,8 @@ struct Loader<ROWS, BK, NT, true> {  // P[k * ld + row], 8x8 blocks transposed i
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int b = threadIdx.x + i * NT;
-      if (b >= NBLK) continue;
-      const int kb = b / (ROWS / 8), rb = b % (ROWS / 8);
+      if (NBLK % NT != 0 && b >= NBLK) continue;
+      const int kb = b % (BK / 8), rb = b / (BK / 8);
       const u32x4* in = r + i * 8;
       // out[m] word w = element (k=2w, m) | element (k=2w+1, m) << 16
 #pragma unroll
@@ -137,15 +146,108 @@ struct Loader<ROWS, BK, NT, true> {  // P[k * ld + row], 8x8 blocks transposed i
   }
 };
 
+// ------------------------------------------------------------ epilogues
+// Output kinds (the host picks one per launch):
+enum EpiKind {
+  EK_F32 = 0,       // C fp32 = acc
+  EK_F32_ACC = 1,   // C fp32 += acc
+  EK_BF16 = 2,      // C bf16 = acc
+  EK_BF16_ACC = 3,  // C bf16 += acc
+  EK_BIAS = 4,      // C bf16 = acc + bias
+  EK_GELU = 5,      // aux bf16 = acc + bias, C bf16 = gelu(aux)
+  EK_DGELU = 6,     // C bf16 = acc * gelu'(aux)
+};
+
+__device__ inline void unpack8(const u32x4& u, float* f) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) { f[2 * w] = bf2f(u[w] & 0xffffu); f[2 * w + 1] = bf2f(u[w] >> 16); }
+}
+__device__ inline u32x4 pack8(const float* f) {
+  u32x4 u;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) u[w] = (uint32_t)f2bf(f[2 * w]) | ((uint32_t)f2bf(f[2 * w + 1]) << 16);
+  return u;
+}
+
+// 8 consecutive outputs of one row, all inside C (vector path)
+template <int EK>
+__device__ inline void epi8(const Epi& e, int row, int col, float* v) {
+  if (EK == EK_BIAS || EK == EK_GELU) {
+    float bb[8];
+    unpack8(*(const u32x4*)((const uint16_t*)e.bias + col), bb);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] += bb[q];
+  }
+  if (EK == EK_GELU) {
+    *(u32x4*)((uint16_t*)e.aux + (size_t)row * e.ldaux + col) = pack8(v);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = gelu_tanh(v[q]);
+  }
+  if (EK == EK_DGELU) {
+    float pa[8];
+    unpack8(*(const u32x4*)((const uint16_t*)e.aux + (size_t)row * e.ldaux + col), pa);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] *= gelu_tanh_grad(pa[q]);
+  }
+  if (EK == EK_F32 || EK == EK_F32_ACC) {
+    float4* cp = (float4*)((float*)e.C + (size_t)row * e.ldc + col);
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+      float4 x = make_float4(v[4 * w], v[4 * w + 1], v[4 * w + 2], v[4 * w + 3]);
+      if (EK == EK_F32_ACC) {
+        const float4 o = cp[w];
+        x.x += o.x; x.y += o.y; x.z += o.z; x.w += o.w;
+      }
+      cp[w] = x;
+    }
+  } else {
+    uint16_t* cp = (uint16_t*)e.C + (size_t)row * e.ldc + col;
+    if (EK == EK_BF16_ACC) {
+      float o[8];
+      unpack8(*(const u32x4*)cp, o);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += o[q];
+    }
+    *(u32x4*)cp = pack8(v);
+  }
+}
+
+// one output element (edge path)
+template <int EK>
+__device__ inline void epi1(const Epi& e, int row, int col, float v) {
+  if (EK == EK_BIAS || EK == EK_GELU) v += bf2f(((const uint16_t*)e.bias)[col]);
+  if (EK == EK_GELU) {
+    ((uint16_t*)e.aux)[(size_t)row * e.ldaux + col] = f2bf(v);
+    v = gelu_tanh(v);
+  }
+  if (EK == EK_DGELU) v *= gelu_tanh_grad(bf2f(((const uint16_t*)e.aux)[(size_t)row * e.ldaux + col]));
+  const size_t idx = (size_t)row * e.ldc + col;
+  if (EK == EK_F32 || EK == EK_F32_ACC) {
+    float* cp = (float*)e.C;
+    cp[idx] = (EK == EK_F32_ACC ? cp[idx] : 0.f) + v;
+  } else {
+    uint16_t* cp = (uint16_t*)e.C;
+    cp[idx] = f2bf((EK == EK_BF16_ACC ? bf2f(cp[idx]) : 0.f) + v);
+  }
+}
+
 // --------------------------------------------------------------- MFMA GEMM
-template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB>
+// BM x BN workgroup tile, WM x WN waves (each (BM/WM) x (BN/WN), made of 32x32
+// MFMA tiles), BK-deep k steps through two LDS stages: the global loads of
+// step k+1 are in flight while step k's MFMAs run, and one barrier per step
+// separates the LDS write of the next stage from the reads of the current one.
+// The epilogue stages each 32x32 accumulator tile through LDS (transposed) so
+// that every lane then owns 16 consecutive outputs of one row: 16-byte
+// global stores and vector reads of bias / GELU input / the accumulated C.
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_mfma_kernel(GemmArgs g) {
   constexpr int NT = WM * WN * 64;
   constexpr int LDSK = BK + 8;
   constexpr int TMW = BM / WM, TNW = BN / WN;
   constexpr int FM = TMW / 32, FN = TNW / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t As[BM * LDSK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * LDSK];
+  constexpr int STAGE = (BM + BN) * LDSK;
+  constexpr int ES = 36;  // epilogue staging row stride (floats)
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
 
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
   int tm, tn;
@@ -157,8 +259,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_mfma_kernel(GemmArgs g) {
 
   Loader<BM, BK, NT, TA> la;
   Loader<BN, BK, NT, TB> lb;
-  const uint16_t* A = (const uint16_t*)g.A;
-  const uint16_t* B = (const uint16_t*)g.B;
+  const long ext_a = TA ? ((long)(g.K - 1) * g.lda + g.M) * 2 : ((long)(g.M - 1) * g.lda + g.K) * 2;
+  const long ext_b = TB ? ((long)(g.K - 1) * g.ldb + g.N) * 2 : ((long)(g.N - 1) * g.ldb + g.K) * 2;
+  const __amdgpu_buffer_rsrc_t RA = make_rsrc(g.A, ext_a), RB = make_rsrc(g.B, ext_b);
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -168,49 +271,94 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_mfma_kernel(GemmArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+  // Pipeline: LDS holds tiles kt (being read) and kt+1 (written at the top of
+  // iteration kt from registers); the registers receive tile kt+2, so every
+  // global load has a full iteration of MFMA work to land.
   const int nk = (g.K + BK - 1) / BK;
-  la.load(A, g.lda, m0, g.M, 0, g.K);
-  lb.load(B, g.ldb, n0, g.N, 0, g.K);
+  la.load(RA, g.lda, m0, g.M, 0, g.K);
+  lb.load(RB, g.ldb, n0, g.N, 0, g.K);
+  la.template store<LDSK>(lds);
+  lb.template store<LDSK>(lds + BM * LDSK);
+  if (nk > 1) {
+    la.load(RA, g.lda, m0, g.M, BK, g.K);
+    lb.load(RB, g.ldb, n0, g.N, BK, g.K);
+  }
+  __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    __syncthreads();
-    la.template store<LDSK>(As);
-    lb.template store<LDSK>(Bs);
-    __syncthreads();
+    const uint16_t* As = lds + (kt & 1) * STAGE;
+    const uint16_t* Bs = As + BM * LDSK;
     if (kt + 1 < nk) {
-      la.load(A, g.lda, m0, g.M, (kt + 1) * BK, g.K);
-      lb.load(B, g.ldb, n0, g.N, (kt + 1) * BK, g.K);
+      uint16_t* An = lds + ((kt + 1) & 1) * STAGE;
+      la.template store<LDSK>(An);
+      lb.template store<LDSK>(An + BM * LDSK);
     }
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 a[FM], b[FN];
+    if (kt + 2 < nk) {
+      la.load(RA, g.lda, m0, g.M, (kt + 2) * BK, g.K);
+      lb.load(RB, g.ldb, n0, g.N, (kt + 2) * BK, g.K);
+    }
+    // fragments of step kk+1 are read from LDS while the MFMAs of step kk run
+    constexpr int KS = BK / 16;
+    bf16x8 fa[2][FM], fb[2][FN];
+    auto ldfrag = [&](int kk, int buf) {
       const int ko = kk * 16 + (lane >> 5) * 8;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        a[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(As + (wm * TMW + i * 32 + (lane & 31)) * LDSK + ko));
+        fa[buf][i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(As + (wm * TMW + i * 32 + (lane & 31)) * LDSK + ko));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(Bs + (wn * TNW + j * 32 + (lane & 31)) * LDSK + ko));
+        fb[buf][j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(Bs + (wn * TNW + j * 32 + (lane & 31)) * LDSK + ko));
+    };
+    ldfrag(0, 0);
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int cb = kk & 1;
+      if (kk + 1 < KS) ldfrag(kk + 1, cb ^ 1);
+      // keep the reads of step kk+1 ahead of the MFMAs of step kk
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cb][i], fb[cb][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    __syncthreads();
   }
 
-  // 32x32 accumulator layout: lane holds column (lane % 32); register e holds
-  // row 8*(e/4) + 4*(lane/32) + e%4.
+  // epilogue.  Accumulator layout: lane holds column (lane % 32), register e
+  // holds row 8*(e/4) + 4*(lane/32) + e%4.  Staged transposed: T[col][row].
+  float* T = (float*)lds + wave * 32 * ES;
+  const int h = lane >> 5, c32 = lane & 31;
+  const int rr = lane >> 1, cc = (lane & 1) * 16;
+  const bool vec_ok = (g.N % 8 == 0) && (g.epi.ldc % 8 == 0);
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int col = n0 + wn * TNW + j * 32 + (lane & 31);
-      if (col >= g.N) continue;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * TMW + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-        if (row < g.M) epi_apply(g.epi, row, col, acc[i][j][e]);
+      for (int gq = 0; gq < 4; ++gq) {
+        float4 x = make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]);
+        *(float4*)(T + c32 * ES + 8 * gq + 4 * h) = x;
       }
+      __syncthreads();
+      const int row = m0 + wm * TMW + i * 32 + rr;
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = T[(cc + 8 * half + q) * ES + rr];
+        const int col = n0 + wn * TNW + j * 32 + cc + 8 * half;
+        if (row < g.M) {
+          if (vec_ok && col + 8 <= g.N) {
+            epi8<EK>(g.epi, row, col, v);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+              if (col + q < g.N) epi1<EK>(g.epi, row, col + q, v[q]);
+          }
+        }
+      }
+      __syncthreads();
     }
 }
 
@@ -262,12 +410,64 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(GemmArgs g) {
 }
 
 // ------------------------------------------------------------------ launch
-template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB>
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK>
 static int launch_mfma(const GemmArgs& g, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_mfma_kernel<BM, BN, BK, WM, WN, TA, TB>), dim3(tiles), dim3(WM * WN * 64), 0, s, g);
+  const size_t lds = 2 * (size_t)(BM + BN) * (BK + 8) * sizeof(uint16_t);
+  auto kern = gemm_mfma_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
+  static bool attr = false;
+  if (!attr) {
+    hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    attr = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(WM * WN * 64), lds, s, g);
   JG_CHECK_LAUNCH("gemm_mfma");
   return 0;
+}
+
+// Tile configuration override for tuning: 0 = default choice.
+static int g_tile_cfg = 0;
+void gemm_set_tile_cfg(int c) { g_tile_cfg = c; }
+
+template <bool TA, bool TB, int EK>
+static int launch_cfg(const GemmArgs& g, hipStream_t s, int cfg) {
+  switch (cfg) {
+    case 1: return launch_mfma<128, 128, 64, 2, 2, TA, TB, EK>(g, s);
+    case 2: return launch_mfma<256, 128, 64, 2, 2, TA, TB, EK>(g, s);
+    case 4: return launch_mfma<256, 256, 64, 2, 2, TA, TB, EK>(g, s);
+    case 6: return launch_mfma<256, 256, 64, 2, 4, TA, TB, EK>(g, s);
+    case 7: return launch_mfma<256, 256, 32, 2, 4, TA, TB, EK>(g, s);
+    default: return launch_mfma<256, 256, 64, 2, 2, TA, TB, EK>(g, s);
+  }
+}
+
+template <bool TA, bool TB>
+static int launch_kind(const GemmArgs& g, hipStream_t s, int cfg, int ek) {
+  switch (ek) {
+    case EK_F32: return launch_cfg<TA, TB, EK_F32>(g, s, cfg);
+    case EK_F32_ACC: return launch_cfg<TA, TB, EK_F32_ACC>(g, s, cfg);
+    case EK_BF16: return launch_cfg<TA, TB, EK_BF16>(g, s, cfg);
+    case EK_BF16_ACC: return launch_cfg<TA, TB, EK_BF16_ACC>(g, s, cfg);
+    case EK_BIAS: return launch_cfg<TA, TB, EK_BIAS>(g, s, cfg);
+    case EK_GELU: return launch_cfg<TA, TB, EK_GELU>(g, s, cfg);
+    default: return launch_cfg<TA, TB, EK_DGELU>(g, s, cfg);
+  }
+}
+
+// The output kind of an epilogue, or -1 if the MFMA epilogues do not cover it.
+static int epi_kind(const Epi& e) {
+  const bool bias = e.bias != nullptr;
+  if (bias && e.bias_dt != BF16) return -1;
+  if ((e.mode == EPI_GELU_FWD || e.mode == EPI_GELU_BWD) && e.aux_dt != BF16) return -1;
+  if (e.mode == EPI_STORE && !bias) {
+    if (e.beta != 0.f && e.beta != 1.f) return -1;
+    if (e.c_dt == F32) return e.beta != 0.f ? EK_F32_ACC : EK_F32;
+    return e.beta != 0.f ? EK_BF16_ACC : EK_BF16;
+  }
+  if (e.beta != 0.f || e.c_dt != BF16) return -1;
+  if (e.mode == EPI_STORE) return EK_BIAS;
+  if (e.mode == EPI_GELU_FWD) return bias ? EK_GELU : -1;
+  return bias ? -1 : EK_DGELU;
 }
 
 static int prof_class(const GemmArgs& g) {
@@ -297,11 +497,30 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   bool mfma = g.a_dt == BF16 && g.b_dt == BF16 && g.K > 0 && aligned16(g.A) && aligned16(g.B) &&
               g.lda % 8 == 0 && g.ldb % 8 == 0;
   if (mfma) mfma = (g.ta ? g.M % 8 == 0 : g.K % 8 == 0) && (g.tb ? g.N % 8 == 0 : g.K % 8 == 0);
-  if (mfma) {
-    if (!g.ta && !g.tb) return launch_mfma<128, 128, 64, 2, 2, false, false>(g, s);
-    if (!g.ta && g.tb) return launch_mfma<128, 128, 64, 2, 2, false, true>(g, s);
-    if (g.ta && g.tb) return launch_mfma<128, 128, 64, 2, 2, true, true>(g, s);
-    return launch_mfma<128, 128, 64, 2, 2, true, false>(g, s);
+  const int ek = mfma ? epi_kind(g.epi) : -1;
+  if (ek >= 0 && (g.epi.ldc % 8 != 0 || !aligned16(g.epi.C) || (g.epi.aux && (g.epi.ldaux % 8 || !aligned16(g.epi.aux)))))
+    mfma = false;
+  // operand extents must fit a 32-bit buffer offset
+  const double ea = 2.0 * (g.ta ? (double)g.K * g.lda : (double)g.M * g.lda);
+  const double eb = 2.0 * (g.tb ? (double)g.K * g.ldb : (double)g.N * g.ldb);
+  if (ea >= 2147483000.0 || eb >= 2147483000.0) mfma = false;
+  if (mfma && ek >= 0) {
+    // default tiles: 256x256 whenever that grid still covers the 256 CUs
+    // (4 waves for the products with a transposed operand, 8 waves for the
+    // forward product), else 128x128
+    // (the GELU epilogues keep too many values live for the 4-wave 256x256
+    // tile: the backward one takes the 8-wave tile, the forward one 128x128)
+    int cfg = g_tile_cfg;
+    if (cfg == 0) {
+      const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
+      if (t256 < 256 || ek == EK_GELU) cfg = 1;
+      else if (ek == EK_DGELU || (!g.ta && !g.tb)) cfg = 6;
+      else cfg = 4;
+    }
+    if (!g.ta && !g.tb) return launch_kind<false, false>(g, s, cfg, ek);
+    if (!g.ta && g.tb) return launch_kind<false, true>(g, s, cfg, ek);
+    if (g.ta && g.tb) return launch_kind<true, true>(g, s, cfg, ek);
+    return launch_kind<true, false>(g, s, cfg, ek);
   }
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
   if (g.K == 0) {
