@@ -278,7 +278,7 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   W.dKh = a.take(hn * m.Dh * es);
   W.dVh = a.take(hn * m.Dh * es);
   W.delta = a.f32(hn);
-  W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, 2 * m.Dh, m.pd});
+  W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, QK_PARTS * 2 * m.Dh + m.D, m.pd});
   const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   W.p1 = a.f32((size_t)nch * W.maxcols);
   W.p2 = a.f32((size_t)nch * W.maxcols);
@@ -540,17 +540,19 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
     const DStream& L = st[s];
     int c0, nc;
     TRY(chunk_range(rm, r0[s], nr[s], &c0, &nc));
-    TRY(reduce_to_grad(W.p2, 2 * m.Dh, c0, nc, m.Dh, G(dth, m, L.qg), m.grad, beta, cx.s));
-    TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, c0, nc, m.Dh, G(dth, m, L.kg), m.grad, beta, cx.s));
+    TRY(reduce_to_grad(W.p2, 2 * m.Dh, c0 * QK_PARTS, nc * QK_PARTS, m.Dh, G(dth, m, L.qg), m.grad, beta, cx.s));
+    TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, c0 * QK_PARTS, nc * QK_PARTS, m.Dh, G(dth, m, L.kg), m.grad, beta,
+                       cx.s));
     TRY(colsum_partials(W.dbig, act, 3 * D, 3 * D, rm, r0[s], nr[s], W.p1, cx.s));
     TRY(reduce_to_grad(W.p1, 3 * D, c0, nc, 3 * D, G(dth, m, L.qkv.b), m.grad, beta, cx.s));
     void* dq = row(W.dbig, r0[s], 3 * D);
     TRY(wgrad(cx, dq, 3 * D, act, row(A.a1, r0[s], D), D, nr[s], 3 * D, D, G(dth, m, L.qkv.w), beta));
     TRY(dgrad(cx, dq, 3 * D, nr[s], cx.P(L.qkv.w), D, 3 * D, D, rowf(W.dA, r0[s], D), D, F32));
     TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, r0[s], nr[s], A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, W.p1,
-                   W.p2 + (size_t)nchunk * 2 * m.Dh, cx.s));
+                   W.p2 + (size_t)nchunk * QK_PARTS * 2 * m.Dh, cx.s));
     TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D, cx.s));
-    TRY(reduce_per_sample(W.p2 + (size_t)nchunk * 2 * m.Dh, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0, cx.s));
+    TRY(reduce_per_sample(W.p2 + (size_t)nchunk * QK_PARTS * 2 * m.Dh, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0,
+                          cx.s));
     // adaLN modulation: mod = SiLU(vec) W_mod^T + b
     TRY(small_linear_bwd(W.dmod[s], mvec, 0, B, D, cx.P(L.mod.w), m.act, 6 * D, G(dth, m, L.mod.w),
                          G(dth, m, L.mod.b), m.grad, beta, W.tmp, W.slpart, cx.s));
@@ -580,8 +582,8 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   Gains gn{{cx.P(L.qg), cx.P(L.qg)}, {cx.P(L.kg), cx.P(L.kg)}};
   TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.proj, LD, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
                        A.rk, W.dbig, LD, W.p2, cx.s));
-  TRY(reduce_to_grad(W.p2, 2 * m.Dh, 0, nchunk, m.Dh, G(dth, m, L.qg), m.grad, beta, cx.s));
-  TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, 0, nchunk, m.Dh, G(dth, m, L.kg), m.grad, beta, cx.s));
+  TRY(reduce_to_grad(W.p2, 2 * m.Dh, 0, nchunk * QK_PARTS, m.Dh, G(dth, m, L.qg), m.grad, beta, cx.s));
+  TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, 0, nchunk * QK_PARTS, m.Dh, G(dth, m, L.kg), m.grad, beta, cx.s));
   TRY(colsum_partials(W.dbig, act, LD, LD, rm, 0, R, W.p1, cx.s));
   TRY(reduce_to_grad(W.p1, LD, 0, nchunk, LD, G(dth, m, L.in.b), m.grad, beta, cx.s));
   TRY(wgrad(cx, W.dbig, LD, act, A.a, D, R, LD, D, G(dth, m, L.in.w), beta));

@@ -78,7 +78,9 @@ struct Rope {
 struct Gains { const void* q[2]; const void* k[2]; };
 int qk_norm_rope_fwd(const void* proj, int ld, int act_dt, RowMap rm, Rope rp, Gains gn,
                      void* Qh, void* Kh, void* Vh, float* rinv_q, float* rinv_k, hipStream_t s);
-// dQh/dKh/dVh head-major (dt_d) -> dproj[row][0..3D) (act dtype, ld), dgain partials [chunk][2*Dh].
+// dQh/dKh/dVh head-major (dt_d) -> dproj[row][0..3D) (act dtype, ld), dgain partials
+// [chunk * QK_PARTS + sub][2*Dh] (QK_PARTS sub-chunks per reduction chunk).
+constexpr int QK_PARTS = 4;
 int qk_norm_rope_bwd(const void* dQh, const void* dKh, const void* dVh, int dt_d, const void* proj, int ld,
                      int act_dt, RowMap rm, Rope rp, Gains gn, const float* rinv_q,
                      const float* rinv_k, void* dproj, int ld_d, float* part_gain, hipStream_t s);

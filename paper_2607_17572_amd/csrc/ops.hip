@@ -43,6 +43,32 @@ int chunk_range(RowMap rm, int row0, int nrows, int* c0, int* nc) {
   return 1;
 }
 
+
+// ---- vector helpers: 8 consecutive elements of a row ----
+__device__ inline void ld8f(const uint16_t* p, float* f) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) { f[2 * e] = bf2f(w[e] & 0xffffu); f[2 * e + 1] = bf2f(w[e] >> 16); }
+}
+__device__ inline void ld8f(const float* p, float* f) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+}
+__device__ inline void st8f(uint16_t* p, const float* f) {
+  uint4 u;
+  u.x = f2bf(f[0]) | ((uint32_t)f2bf(f[1]) << 16);
+  u.y = f2bf(f[2]) | ((uint32_t)f2bf(f[3]) << 16);
+  u.z = f2bf(f[4]) | ((uint32_t)f2bf(f[5]) << 16);
+  u.w = f2bf(f[6]) | ((uint32_t)f2bf(f[7]) << 16);
+  *(uint4*)p = u;
+}
+__device__ inline void st8f(float* p, const float* f) {
+  *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
+  *(float4*)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
+}
+static inline bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
 // ================================================================ small linear
 template <typename TW>
 __global__ __launch_bounds__(256) void small_linear_fwd_k(const float* __restrict__ in, int B, int Din,
@@ -139,11 +165,96 @@ __global__ void sum_parts_k(const float* __restrict__ part, int nparts, size_t n
   out[i] = s;
 }
 
+// Small batches: 8 consecutive input columns per thread (16-byte loads and
+// stores of W and dW), all samples' rows kept in registers.
+template <typename TW, typename TG, int BM>
+__global__ __launch_bounds__(128) void small_linear_bwd_vec_k(const float* __restrict__ dout,
+                                                              const float* __restrict__ in, int B, int Din,
+                                                              const TW* __restrict__ W, int Dout, TG* __restrict__ dW,
+                                                              TG* __restrict__ db, float beta,
+                                                              float* __restrict__ part) {
+  __shared__ float sd[BM][SL_JT];
+  const int jt = blockIdx.y, j0 = jt * SL_JT;
+  for (int i = threadIdx.x; i < BM * SL_JT; i += 128) {
+    const int b = i / SL_JT, jj = i % SL_JT;
+    sd[b][jj] = (b < B && j0 + jj < Dout) ? dout[(size_t)b * Dout + j0 + jj] : 0.f;
+  }
+  __syncthreads();
+  if (blockIdx.x == 0 && db) {
+    for (int jj = threadIdx.x; jj < SL_JT; jj += 128) {
+      if (j0 + jj >= Dout) continue;
+      float sacc = 0.f;
+      for (int b = 0; b < B; ++b) sacc += sd[b][jj];
+      if (beta != 0.f) sacc += beta * ldf(db, j0 + jj);
+      stf(db, j0 + jj, sacc);
+    }
+  }
+  const int d = (blockIdx.x * 128 + threadIdx.x) * 8;
+  if (d >= Din) return;
+  float x[BM][8], acc[BM][8];
+#pragma unroll
+  for (int b = 0; b < BM; ++b) {
+    if (b < B) ld8f(in + (size_t)b * Din + d, x[b]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (b >= B) x[b][e] = 0.f;
+      acc[b][e] = 0.f;
+    }
+  }
+  const int jn = min(SL_JT, Dout - j0);
+  for (int jj = 0; jj < jn; ++jj) {
+    const size_t idx = (size_t)(j0 + jj) * Din + d;
+    float w[8], gw[8];
+    ld8f(W + idx, w);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) gw[e] = 0.f;
+#pragma unroll
+    for (int b = 0; b < BM; ++b) {
+      const float sv = sd[b][jj];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        gw[e] = fmaf(sv, x[b][e], gw[e]);
+        acc[b][e] = fmaf(sv, w[e], acc[b][e]);
+      }
+    }
+    if (beta != 0.f) {
+      float o[8];
+      ld8f(dW + idx, o);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) gw[e] += beta * o[e];
+    }
+    st8f(dW + idx, gw);
+  }
+  if (part)
+#pragma unroll
+    for (int b = 0; b < BM; ++b)
+      if (b < B) st8f(part + ((size_t)jt * B + b) * Din + d, acc[b]);
+}
+
 int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din, const void* W, int w_dt,
                      int Dout, void* dW, void* db, int g_dt, float beta, float* din, float* part,
                      hipStream_t s) {
   if (act != 0 || B <= 0 || B > SL_MAXB) { set_error("small_linear_bwd: batch must be 1..32"); return 1; }
   const int njt = (Dout + SL_JT - 1) / SL_JT;
+  if (B <= 4 && Din % 8 == 0 && al16(in) && al16(W) && al16(dW) && (!din || al16(part))) {
+    dim3 grid((Din + 1023) / 1024, njt);
+    float* p = din ? part : nullptr;
+#define SLV(TW, TG) \
+  hipLaunchKernelGGL((small_linear_bwd_vec_k<TW, TG, 4>), grid, dim3(128), 0, s, dout, in, B, Din, (const TW*)W, Dout, \
+                     (TG*)dW, (TG*)db, beta, p)
+    if (w_dt == BF16 && g_dt == BF16) SLV(uint16_t, uint16_t);
+    else if (w_dt == BF16) SLV(uint16_t, float);
+    else if (g_dt == BF16) SLV(float, uint16_t);
+    else SLV(float, float);
+#undef SLV
+    LAUNCH_OK("small_linear_bwd_vec");
+    if (din) {
+      const size_t n = (size_t)B * Din;
+      hipLaunchKernelGGL(sum_parts_k, dim3((n + 255) / 256), dim3(256), 0, s, part, njt, n, din);
+      LAUNCH_OK("small_linear_bwd_sum");
+    }
+    return 0;
+  }
   dim3 grid((Din + SL_DT - 1) / SL_DT, njt);
   float* p = din ? part : nullptr;
 #define SLB(TW, TG)                                                                                  \
@@ -317,6 +428,79 @@ __global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA
   }
 }
 
+// One wave per row (rows of the chunk dealt round-robin to the 4 waves), each
+// lane owning NV runs of 8 consecutive columns (16-byte loads); the per-column
+// partial sums of the 4 waves are combined through LDS in wave order.
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void ln_mod_bwd_vec_k(const float* __restrict__ dA, const T* __restrict__ x,
+                                                        Chunks ch, int c0, const float* __restrict__ mean,
+                                                        const float* __restrict__ rstd, const float* __restrict__ mt,
+                                                        const float* __restrict__ mi, int mod_w, int sc_off,
+                                                        float* __restrict__ g, float* __restrict__ psc,
+                                                        float* __restrict__ psh) {
+  constexpr int D = NV * 512;
+  extern __shared__ float red[];  // [4][D] reduction space, then [D] of (1 + scale)
+  float* m = red + 4 * D;
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const float* mg = ((r0 < ch.B * ch.nt) ? mt : mi) + (size_t)b * mod_w + sc_off;
+  for (int c = threadIdx.x; c < D; c += 256) m[c] = 1.f + mg[c];
+  __syncthreads();
+  float asc[NV * 8], ash[NV * 8];
+#pragma unroll
+  for (int i = 0; i < NV * 8; ++i) asc[i] = ash[i] = 0.f;
+  for (int rr = w; rr < n; rr += 4) {
+    const int r = r0 + rr;
+    const float mu = mean[r], rs = rstd[r];
+    // pass 1: row sums and the column partials; pass 2 re-reads the (cached)
+    // row and updates g, so no per-row arrays stay live
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = 8 * lane + 512 * i;
+      float xv[8], da[8];
+      ld8f(x + (size_t)r * D + c, xv);
+      ld8f(dA + (size_t)r * D + c, da);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xhat = (xv[e] - mu) * rs;
+        const float d = da[e] * m[c + e];
+        asc[8 * i + e] = fmaf(da[e], xhat, asc[8 * i + e]);
+        ash[8 * i + e] += da[e];
+        s1 += d;
+        s2 += d * xhat;
+      }
+    }
+    const float m1 = wave_sum(s1) / D, m2 = wave_sum(s2) / D;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = 8 * lane + 512 * i;
+      float xv[8], da[8], gv[8];
+      ld8f(x + (size_t)r * D + c, xv);
+      ld8f(dA + (size_t)r * D + c, da);
+      ld8f(g + (size_t)r * D + c, gv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xhat = (xv[e] - mu) * rs;
+        gv[e] += rs * (da[e] * m[c + e] - m1 - xhat * m2);
+      }
+      st8f(g + (size_t)r * D + c, gv);
+    }
+  }
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const float* a = pass == 0 ? asc : ash;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) st8f(red + w * D + 8 * lane + 512 * i, a + 8 * i);
+    __syncthreads();
+    float* out = (pass == 0 ? psc : psh) + (size_t)q * D;
+    for (int c = threadIdx.x; c < D; c += 256) out[c] = red[c] + red[D + c] + red[2 * D + c] + red[3 * D + c];
+    __syncthreads();
+  }
+}
+
 int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int row0, int nrows,
                const float* mean, const float* rstd, const float* mod_txt, const float* mod_img, int mod_w,
                int sc_off, float* g, float* part_scale, float* part_shift, hipStream_t s) {
@@ -325,6 +509,26 @@ int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   if (nc == 0) return 0;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (D % 512 == 0 && D <= 4096 && al16(dA) && al16(x) && al16(g)) {
+    const size_t lds = 5 * (size_t)D * sizeof(float);
+#define LNB(T, NV)                                                                                             \
+  case NV: {                                                                                                   \
+    auto k = ln_mod_bwd_vec_k<T, NV>;                                                                          \
+    if (lds > 65536) hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds); \
+    hipLaunchKernelGGL(k, dim3(nc), dim3(256), lds, s, dA, (const T*)x, ch, c0, mean, rstd, mod_txt, mod_img, \
+                       mod_w, sc_off, g, part_scale, part_shift);                                              \
+  } break;
+    if (act_dt == BF16) {
+      switch (D / 512) { LNB(uint16_t, 1) LNB(uint16_t, 2) LNB(uint16_t, 3) LNB(uint16_t, 4) LNB(uint16_t, 5)
+                         LNB(uint16_t, 6) LNB(uint16_t, 7) LNB(uint16_t, 8) }
+    } else {
+      switch (D / 512) { LNB(float, 1) LNB(float, 2) LNB(float, 3) LNB(float, 4) LNB(float, 5) LNB(float, 6)
+                         LNB(float, 7) LNB(float, 8) }
+    }
+#undef LNB
+    LAUNCH_OK("ln_mod_bwd_vec");
+    return 0;
+  }
   if (act_dt == BF16)
     hipLaunchKernelGGL(ln_mod_bwd_k<uint16_t>, dim3(nc), dim3(256), 0, s, dA, (const uint16_t*)x, D, ch, c0, mean,
                        rstd, mod_txt, mod_img, mod_w, sc_off, g, part_scale, part_shift);
@@ -391,6 +595,39 @@ __global__ __launch_bounds__(256) void gate_bwd_k(const float* __restrict__ g, c
   }
 }
 
+template <typename T>
+__global__ __launch_bounds__(256) void gate_bwd_vec_k(const float* __restrict__ g, const T* __restrict__ y, int D,
+                                                      Chunks ch, int c0, const float* __restrict__ mt,
+                                                      const float* __restrict__ mi, int mod_w, int gate_off,
+                                                      T* __restrict__ dY, int ld_dy, float* __restrict__ pg,
+                                                      float* __restrict__ pb) {
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 8;
+  if (c >= D) return;
+  const float* m = ((r0 < ch.B * ch.nt) ? mt : mi) + (size_t)b * mod_w + gate_off + c;
+  float gt[8], sg[8], sb[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) { gt[e] = m[e]; sg[e] = 0.f; sb[e] = 0.f; }
+#pragma unroll 2
+  for (int rr = 0; rr < n; ++rr) {
+    const int r = r0 + rr;
+    float gv[8], yv[8], d[8];
+    ld8f(g + (size_t)r * D + c, gv);
+    ld8f(y + (size_t)r * D + c, yv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      sg[e] = fmaf(gv[e], yv[e], sg[e]);
+      d[e] = gv[e] * gt[e];
+      sb[e] += d[e];
+    }
+    st8f(dY + (size_t)r * ld_dy + c, d);
+  }
+  st8f(pg + (size_t)q * D + c, sg);
+  st8f(pb + (size_t)q * D + c, sb);
+}
+
 int gate_bwd(const float* g, const void* y, int act_dt, int D, RowMap rm, int row0, int nrows,
              const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* dY, int ld_dy,
              float* part_gate, float* part_bias, hipStream_t s) {
@@ -398,6 +635,18 @@ int gate_bwd(const float* g, const void* y, int act_dt, int D, RowMap rm, int ro
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   if (nc == 0) return 0;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (D % 8 == 0 && ld_dy % 8 == 0 && mod_w % 4 == 0 && gate_off % 4 == 0 && al16(g) && al16(y) && al16(dY) &&
+      al16(mod_txt) && al16(mod_img) && al16(part_gate) && al16(part_bias)) {
+    dim3 grid(nc, (D + 2047) / 2048);
+    if (act_dt == BF16)
+      hipLaunchKernelGGL(gate_bwd_vec_k<uint16_t>, grid, dim3(256), 0, s, g, (const uint16_t*)y, D, ch, c0, mod_txt,
+                         mod_img, mod_w, gate_off, (uint16_t*)dY, ld_dy, part_gate, part_bias);
+    else
+      hipLaunchKernelGGL(gate_bwd_vec_k<float>, grid, dim3(256), 0, s, g, (const float*)y, D, ch, c0, mod_txt,
+                         mod_img, mod_w, gate_off, (float*)dY, ld_dy, part_gate, part_bias);
+    LAUNCH_OK("gate_bwd_vec");
+    return 0;
+  }
   if (act_dt == BF16)
     hipLaunchKernelGGL(gate_bwd_k<uint16_t>, dim3(nc), dim3(256), 0, s, g, (const uint16_t*)y, D, ch, c0, mod_txt,
                        mod_img, mod_w, gate_off, (uint16_t*)dY, ld_dy, part_gate, part_bias);
@@ -488,6 +737,8 @@ int qk_norm_rope_fwd(const void* proj, int ld, int act_dt, RowMap rm, Rope rp, G
   return 0;
 }
 
+constexpr int QK_SUB = RED_ROWS / QK_PARTS;  // rows per block of the q/k norm backward
+
 template <typename T, typename TD>
 __global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__ dQh, const TD* __restrict__ dKh,
                                                           const TD* __restrict__ dVh, const T* __restrict__ proj,
@@ -495,20 +746,24 @@ __global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__
                                                           Gains gn, const float* __restrict__ rq, const float* __restrict__ rk,
                                                           T* __restrict__ dproj, int ld_d, float* __restrict__ pgain) {
   __shared__ float red[4][4][64];
+  // block = (chunk, sub-chunk of QK_SUB rows); gain partials per sub-chunk
   const int q = c0 + blockIdx.x;
   int r0, n, b;
   chunk_rows(ch, q, r0, n, b);
+  const int st = r0 < ch.B * ch.nt ? 0 : 1;
+  const int sub = (int)blockIdx.y;  // signed: an empty sub-chunk must get n <= 0
+  r0 += sub * QK_SUB;
+  n = min(QK_SUB, n - sub * QK_SUB);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int D = rp.H * rp.Dh, N = rm.nt + rm.ni;
   const bool act = lane < rp.Dh / 2;
   const int p = act ? lane : 0;
-  const int st = r0 < ch.B * ch.nt ? 0 : 1;
   const T* qg = (const T*)gn.q[st];
   const T* kg = (const T*)gn.k[st];
   float gq0 = 0, gq1 = 0, gk0 = 0, gk1 = 0;
   const float qga = act ? ldf(qg, 2 * p) : 0.f, qgb = act ? ldf(qg, 2 * p + 1) : 0.f;
   const float kga = act ? ldf(kg, 2 * p) : 0.f, kgb = act ? ldf(kg, 2 * p + 1) : 0.f;
-  for (int it = wave; it < n * rp.H; it += 4) {
+  for (int it = wave; it < max(n, 0) * rp.H; it += 4) {
     const int r = r0 + it / rp.H, h = it % rp.H;
     int bb, j;
     tok_of_row(rm, r, bb, j);
@@ -563,7 +818,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__
     float a[4] = {0, 0, 0, 0};
     for (int w = 0; w < 4; ++w)
       for (int k = 0; k < 4; ++k) a[k] += red[w][k][lane];
-    float* out = pgain + (size_t)q * 2 * rp.Dh;
+    float* out = pgain + ((size_t)q * QK_PARTS + sub) * 2 * rp.Dh;
     out[2 * p] = a[0];
     out[2 * p + 1] = a[1];
     out[rp.Dh + 2 * p] = a[2];
@@ -579,7 +834,7 @@ int qk_norm_rope_bwd(const void* dQh, const void* dKh, const void* dVh, int dt_d
   if (chunk_range(rm, 0, rm.rows(), &c0, &nc)) return 1;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
 #define QKB(T, TD)                                                                                            \
-  hipLaunchKernelGGL((qk_norm_rope_bwd_k<T, TD>), dim3(nc), dim3(256), 0, s, (const TD*)dQh, (const TD*)dKh,     \
+  hipLaunchKernelGGL((qk_norm_rope_bwd_k<T, TD>), dim3(nc, QK_PARTS), dim3(256), 0, s, (const TD*)dQh, (const TD*)dKh,     \
                      (const TD*)dVh, (const T*)proj, ld, rm, rp, ch, c0, gn, rinv_q, rinv_k, \
                      (T*)dproj, ld_d, part_gain)
   if (act_dt == BF16 && dt_d == BF16) QKB(uint16_t, uint16_t);
@@ -605,12 +860,41 @@ __global__ __launch_bounds__(256) void colsum_k(const T* __restrict__ X, int ld,
   }
 }
 
+// 8 consecutive columns per thread, 16-byte loads down the chunk's rows
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_vec_k(const T* __restrict__ X, int ld, int N, Chunks ch, int c0,
+                                                    float* __restrict__ part) {
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 8;
+  if (c >= N) return;
+  float sacc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll 4
+  for (int rr = 0; rr < n; ++rr) {
+    float v[8];
+    ld8f(X + (size_t)(r0 + rr) * ld + c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sacc[e] += v[e];
+  }
+  st8f(part + (size_t)q * N + c, sacc);
+}
+
 int colsum_partials(const void* X, int dt, int ld, int N, RowMap rm, int row0, int nrows, float* part,
                     hipStream_t s) {
   int c0, nc;
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   if (nc == 0) return 0;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (N % 8 == 0 && ld % 8 == 0 && al16(X) && al16(part)) {
+    dim3 grid(nc, (N + 2047) / 2048);
+    if (dt == BF16)
+      hipLaunchKernelGGL(colsum_vec_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)X, ld, N, ch, c0, part);
+    else
+      hipLaunchKernelGGL(colsum_vec_k<float>, grid, dim3(256), 0, s, (const float*)X, ld, N, ch, c0, part);
+    LAUNCH_OK("colsum_vec");
+    return 0;
+  }
   if (dt == BF16)
     hipLaunchKernelGGL(colsum_k<uint16_t>, dim3(nc), dim3(256), 0, s, (const uint16_t*)X, ld, N, ch, c0, part);
   else
@@ -619,18 +903,31 @@ int colsum_partials(const void* X, int dt, int ld, int N, RowMap rm, int row0, i
   return 0;
 }
 
-__global__ void reduce_per_sample_k(const float* __restrict__ part, int N, Chunks ch, int c0, int nc,
-                                    float* __restrict__ out, int out_stride, int out_off) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= ch.B * N) return;
-  const int b = i / N, c = i % N;
-  float s = 0.f;
-  for (int q = c0; q < c0 + nc; ++q) {
-    int r0, n, bq;
-    chunk_rows(ch, q, r0, n, bq);
-    if (bq == b) s += part[(size_t)q * N + c];
+// Per sample: the sample's chunks inside [c0, c0 + nc) form at most two runs
+// (its text chunks, its image chunks); 32 columns x 8 slices per block.
+__global__ __launch_bounds__(256) void reduce_per_sample_k(const float* __restrict__ part, int N, Chunks ch, int c0,
+                                                           int nc, float* __restrict__ out, int out_stride,
+                                                           int out_off) {
+  __shared__ float sh[8][33];
+  const int b = blockIdx.y;
+  const int cl = threadIdx.x & 31, sl = threadIdx.x >> 5;
+  const int c = blockIdx.x * 32 + cl;
+  const int ct = ch.ct(), ci = ch.ci();
+  const int runs[2][2] = {{b * ct, b * ct + ct}, {ch.B * ct + b * ci, ch.B * ct + b * ci + ci}};
+  float acc = 0.f;
+  if (c < N)
+    for (int r = 0; r < 2; ++r) {
+      const int lo = max(runs[r][0], c0), hi = min(runs[r][1], c0 + nc);
+      for (int q = lo + sl; q < hi; q += 8) acc += part[(size_t)q * N + c];
+    }
+  sh[sl][cl] = acc;
+  __syncthreads();
+  if (sl == 0 && c < N) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) t += sh[k][cl];
+    out[(size_t)b * out_stride + out_off + c] = t;
   }
-  out[(size_t)b * out_stride + out_off + c] = s;
 }
 
 int reduce_per_sample(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
@@ -638,27 +935,37 @@ int reduce_per_sample(const float* part, int N, RowMap rm, int row0, int nrows, 
   int c0, nc;
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
-  const int n = rm.B * N;
-  hipLaunchKernelGGL(reduce_per_sample_k, dim3((n + 255) / 256), dim3(256), 0, s, part, N, ch, c0, nc, out,
+  hipLaunchKernelGGL(reduce_per_sample_k, dim3((N + 31) / 32, rm.B), dim3(256), 0, s, part, N, ch, c0, nc, out,
                      out_stride, out_off);
   LAUNCH_OK("reduce_per_sample");
   return 0;
 }
 
+// 32 columns x 8 chunk slices per block; the 8 slice sums are added in slice
+// order (deterministic), then beta * g is added once.
 template <typename TG>
-__global__ void reduce_to_grad_k(const float* __restrict__ part, int ld, int chunk0, int nchunk, int N,
-                                 TG* __restrict__ g, float beta) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= N) return;
-  float s = 0.f;
-  for (int q = chunk0; q < chunk0 + nchunk; ++q) s += part[(size_t)q * ld + c];
-  if (beta != 0.f) s += beta * ldf(g, c);
-  stf(g, c, s);
+__global__ __launch_bounds__(256) void reduce_to_grad_k(const float* __restrict__ part, int ld, int chunk0, int nchunk,
+                                                        int N, TG* __restrict__ g, float beta) {
+  __shared__ float sh[8][33];
+  const int cl = threadIdx.x & 31, sl = threadIdx.x >> 5;
+  const int c = blockIdx.x * 32 + cl;
+  float acc = 0.f;
+  if (c < N)
+    for (int q = chunk0 + sl; q < chunk0 + nchunk; q += 8) acc += part[(size_t)q * ld + c];
+  sh[sl][cl] = acc;
+  __syncthreads();
+  if (sl == 0 && c < N) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) t += sh[k][cl];
+    if (beta != 0.f) t += beta * ldf(g, c);
+    stf(g, c, t);
+  }
 }
 
 int reduce_to_grad(const float* part, int ld, int chunk0, int nchunk, int N, void* g, int g_dt,
                    float beta, hipStream_t s) {
-  dim3 grid((N + 255) / 256);
+  dim3 grid((N + 31) / 32);
   if (g_dt == BF16)
     hipLaunchKernelGGL(reduce_to_grad_k<uint16_t>, grid, dim3(256), 0, s, part, ld, chunk0, nchunk, N, (uint16_t*)g,
                        beta);

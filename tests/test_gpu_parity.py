@@ -26,6 +26,10 @@ TINY = pk.config("tiny")
 BLOCK_SMALL = pk.Config(n_double=1, n_single=0, hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_ch=16, patch=2,
                         lat_h=16, lat_w=16, n_txt=40, txt_dim=256, t_freq_dim=256, block_only=1, act_dtype=pk.BF16,
                         grad_dtype=pk.F32)
+# hidden 512: the wave-per-row LayerNorm backward and 8-column vector kernels
+BLOCK_MID = pk.Config(n_double=1, n_single=0, hidden=512, heads=4, head_dim=128, mlp_hidden=2048, in_ch=16, patch=2,
+                      lat_h=16, lat_w=18, n_txt=37, txt_dim=512, t_freq_dim=256, block_only=1, act_dtype=pk.BF16,
+                      grad_dtype=pk.F32)
 FULL_SMALL = pk.Config(n_double=1, n_single=1, hidden=256, heads=2, head_dim=128, mlp_hidden=512, in_ch=16, patch=2,
                        lat_h=16, lat_w=20, n_txt=24, txt_dim=128, t_freq_dim=256, act_dtype=pk.BF16, grad_dtype=pk.F32)
 
@@ -84,6 +88,13 @@ def test_bf16_block_jagg_matches_oracle():
     cs = Case(BLOCK_SMALL, B=1, W=4)
     eg, worst = compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 2e-2)
     say(f"bf16 block jagg rel L2 {eg:.2e}, worst {worst}")
+
+
+def test_bf16_block_hidden512_matches_oracle():
+    say("case: bf16 block hidden 512 (vector row kernels) jagg W=4 B=2")
+    cs = Case(BLOCK_MID, B=2, W=4)
+    eg, worst = compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 2e-2)
+    say(f"bf16 block512 jagg rel L2 {eg:.2e}, worst {worst}")
 
 
 def test_bf16_block_perstep_batch2_matches_oracle():
