@@ -115,6 +115,57 @@ __device__ inline void stage_tok_t(uint16_t* S, const uint16_t* G, int ld, const
   }
 }
 
+// Register-staged tile: T rows x 128 columns, fetched as 8x8 element blocks
+// (one block per participating thread: 8 x 16-byte loads, one per row) so
+// that the same registers can be written to LDS both as rows (S[r][d]) and,
+// after an in-register 8x8 transpose, as columns (S^T[d][r]).  `load` is
+// issued one tile ahead of its use; `commit` writes the LDS copies.
+template <int T>
+struct Tile8 {
+  static constexpr int NBLK = (T / 8) * (DH / 8);  // blocks per tile
+  u32x4 r[8];
+  int rb, db;
+  bool on;
+  __device__ inline void init(int slot) {  // slot in [0, NBLK) or -1
+    on = slot >= 0 && slot < NBLK;
+    db = on ? slot % (DH / 8) : 0;
+    rb = on ? slot / (DH / 8) : 0;
+  }
+  // rowptr(i) = pointer to row i (or nullptr when the row is out of range)
+  template <class RowPtr>
+  __device__ inline void load(RowPtr rowptr, int r0) {
+    if (!on) return;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint16_t* p = rowptr(r0 + rb * 8 + k);
+      r[k] = p ? *(const u32x4*)(p + db * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  template <int DS>
+  __device__ inline void commit_rows(uint16_t* S) const {
+    if (!on) return;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) *(u32x4*)(S + (rb * 8 + k) * DS + db * 8) = r[k];
+  }
+  template <int TS>
+  __device__ inline void commit_cols(uint16_t* S) const {
+    if (!on) return;
+    // word w of row m of the transposed block = element (r = 2w, m) | (r = 2w+1, m) << 16
+#pragma unroll
+    for (int mw = 0; mw < 4; ++mw) {
+      u32x4 lo, hi;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const unsigned a = r[2 * w][mw], c = r[2 * w + 1][mw];
+        lo[w] = (a & 0xffffu) | (c << 16);
+        hi[w] = (a >> 16) | (c & 0xffff0000u);
+      }
+      *(u32x4*)(S + (db * 8 + 2 * mw) * TS + rb * 8) = lo;
+      *(u32x4*)(S + (db * 8 + 2 * mw + 1) * TS + rb * 8) = hi;
+    }
+  }
+};
+
 // ============================================================== forward
 constexpr int F_QB = 128, F_KT = 64;
 constexpr int F_KS = DH + 8;    // K tile row stride
@@ -131,11 +182,19 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma_k(AttnFwd a) {
   const uint16_t* K = (const uint16_t*)a.K + base;
   const uint16_t* V = (const uint16_t*)a.V + base;
   const float sc = rsqrtf((float)DH) * LOG2E;
+  const int N = a.N;
+
+  // threads [0, 128) stage K blocks, [128, 256) V blocks (64 keys x 128 = 128 blocks each)
+  Tile8<F_KT> tk;
+  const bool isk = threadIdx.x < 128;
+  tk.init(isk ? (int)threadIdx.x : (int)threadIdx.x - 128);
+  const uint16_t* src = isk ? K : V;
+  auto rows = [&](int i) -> const uint16_t* { return i < N ? src + (size_t)i * DH : nullptr; };
 
   bf16x8 qf[8];
 #pragma unroll
   for (int kb = 0; kb < 8; ++kb) {
-    if (q < a.N) qf[kb] = ld8(Q + (size_t)q * DH + kb * 16 + h * 8);
+    if (q < N) qf[kb] = ld8(Q + (size_t)q * DH + kb * 16 + h * 8);
     else qf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
   }
   f32x16 o[4];
@@ -143,11 +202,13 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma_k(AttnFwd a) {
   for (int i = 0; i < 4; ++i) o[i] = zero16();
   float m = -INFINITY, l = 0.f;
 
-  for (int k0 = 0; k0 < a.N; k0 += F_KT) {
+  tk.load(rows, 0);
+  for (int k0 = 0; k0 < N; k0 += F_KT) {
+    __syncthreads();  // everyone is done reading the previous tile
+    if (isk) tk.commit_rows<F_KS>(Ks);
+    else tk.commit_cols<F_VS>(Vt);
     __syncthreads();
-    stage_rows<F_KT, F_KS>(Ks, K, k0, a.N);
-    stage_rows_t<F_KT, F_VS>(Vt, V, k0, a.N);
-    __syncthreads();
+    if (k0 + F_KT < N) tk.load(rows, k0 + F_KT);  // lands during this tile's MFMAs
     f32x16 st[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -161,9 +222,9 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma_k(AttnFwd a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int key = k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3);
-        const float s = key < a.N ? st[t][e] * sc : -INFINITY;
-        st[t][e] = s;
-        mx = fmaxf(mx, s);
+        const float sv = key < N ? st[t][e] * sc : -INFINITY;
+        st[t][e] = sv;
+        mx = fmaxf(mx, sv);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mn = fmaxf(m, mx);
@@ -191,7 +252,7 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma_k(AttnFwd a) {
     }
   }
   l += __shfl_xor(l, 32, 64);
-  if (q >= a.N) return;
+  if (q >= N) return;
   const float inv = 1.f / l;
   uint16_t* O = (uint16_t*)a.O + (size_t)row_of_tok_m(a.rm, b, q) * a.ld_o + hd * DH;
 #pragma unroll
@@ -203,7 +264,7 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma_k(AttnFwd a) {
       for (int i = 0; i < 4; ++i) v[i] = (__bf16)(o[dt][4 * g + i] * inv);
       *(bf16x4*)(O + 32 * dt + 8 * g + 4 * h) = v;
     }
-  if (h == 0) a.lse[(size_t)bh * a.N + q] = (m + __log2f(l)) * LN2;
+  if (h == 0) a.lse[(size_t)bh * N + q] = (m + __log2f(l)) * LN2;
 }
 
 // ============================================================== delta
@@ -244,7 +305,7 @@ __global__ __launch_bounds__(256) void attn_delta_mfma_k(AttnBwd a) {
 }
 
 // ============================================================== dK, dV
-constexpr int KV_KB = 128, KV_QT = 32;
+constexpr int KV_KB = 128, KV_QT = 64;
 constexpr int KV_S = DH + 8;       // [q][d] tiles
 constexpr int KV_T = KV_QT + 8;    // [d][q] tiles
 
@@ -261,12 +322,38 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_mfma_k(AttnBwd a) {
   const uint16_t* Q = (const uint16_t*)a.Q + base;
   const uint16_t* K = (const uint16_t*)a.K + base;
   const uint16_t* V = (const uint16_t*)a.V + base;
+  const uint16_t* G = (const uint16_t*)a.dO;
   const float sc = rsqrtf((float)DH);
+  const int N = a.N;
+
+  // threads [0, NB) stage Q blocks, [NB, 2 NB) dO blocks; lse and delta of
+  // the tile are loaded by threads [0, KV_QT) and [KV_QT, 2 KV_QT)
+  constexpr int NB = Tile8<KV_QT>::NBLK;
+  constexpr int NT = KV_QT / 32;  // 32x32 score tiles per wave per query tile
+  static_assert(2 * NB <= 256 && 2 * KV_QT <= 256, "tile too large for one block");
+  Tile8<KV_QT> tq;
+  const int tid = threadIdx.x;
+  const bool isq = tid < NB;
+  tq.init(tid < 2 * NB ? (isq ? tid : tid - NB) : -1);
+  auto rows = [&](int i) -> const uint16_t* {
+    if (i >= N) return nullptr;
+    return isq ? Q + (size_t)i * DH : G + (size_t)row_of_tok_m(a.rm, b, i) * a.ld_do + hd * DH;
+  };
+  float lsv = 0.f;
+  auto load_ld = [&](int q0) {
+    if (tid < KV_QT) {
+      const int qq = q0 + tid;
+      lsv = qq < N ? a.lse[(size_t)bh * N + qq] : INFINITY;
+    } else if (tid < 2 * KV_QT) {
+      const int qq = q0 + tid - KV_QT;
+      lsv = qq < N ? a.delta[(size_t)bh * N + qq] : 0.f;
+    }
+  };
 
   bf16x8 kf[8], vf[8];
 #pragma unroll
   for (int kb = 0; kb < 8; ++kb) {
-    if (key < a.N) {
+    if (key < N) {
       kf[kb] = ld8(K + (size_t)key * DH + kb * 16 + h * 8);
       vf[kb] = ld8(V + (size_t)key * DH + kb * 16 + h * 8);
     } else {
@@ -277,41 +364,46 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_mfma_k(AttnBwd a) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
 
-  for (int q0 = 0; q0 < a.N; q0 += KV_QT) {
+  tq.load(rows, 0);
+  load_ld(0);
+  for (int q0 = 0; q0 < N; q0 += KV_QT) {
     __syncthreads();
-    stage_rows<KV_QT, KV_S>(Qs, Q, q0, a.N);
-    stage_rows_t<KV_QT, KV_T>(Qt, Q, q0, a.N);
-    stage_tok<KV_QT, KV_S>(Gs, (const uint16_t*)a.dO, a.ld_do, a.rm, b, hd, q0, a.N);
-    stage_tok_t<KV_QT, KV_T>(Gt, (const uint16_t*)a.dO, a.ld_do, a.rm, b, hd, q0, a.N);
-    if (threadIdx.x < KV_QT) {
-      const int qq = q0 + threadIdx.x;
-      Ls[threadIdx.x] = qq < a.N ? a.lse[(size_t)bh * a.N + qq] : INFINITY;
-      Ds[threadIdx.x] = qq < a.N ? a.delta[(size_t)bh * a.N + qq] : 0.f;
-    }
+    if (isq) { tq.commit_rows<KV_S>(Qs); tq.commit_cols<KV_T>(Qt); }
+    else { tq.commit_rows<KV_S>(Gs); tq.commit_cols<KV_T>(Gt); }
+    if (tid < KV_QT) Ls[tid] = lsv;
+    else if (tid < 2 * KV_QT) Ds[tid - KV_QT] = lsv;
     __syncthreads();
-    f32x16 s = zero16(), dp = zero16();
+    if (q0 + KV_QT < N) { tq.load(rows, q0 + KV_QT); load_ld(q0 + KV_QT); }
+    f32x16 s[NT], dp[NT];
 #pragma unroll
-    for (int kb = 0; kb < 8; ++kb) {
-      s = mfma(ld8(Qs + c32 * KV_S + kb * 16 + h * 8), kf[kb], s);
-      dp = mfma(ld8(Gs + c32 * KV_S + kb * 16 + h * 8), vf[kb], dp);
-    }
-    // lane: key column, query rows 8(e/4) + 4h + e%4
+    for (int t = 0; t < NT; ++t) {
+      s[t] = zero16();
+      dp[t] = zero16();
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const float4 L4 = *(const float4*)(Ls + 8 * g + 4 * h);
-      const float4 D4 = *(const float4*)(Ds + 8 * g + 4 * h);
-      const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = 4 * g + i;
-        const float p = __builtin_amdgcn_exp2f((s[e] * sc - Lv[i]) * LOG2E);
-        s[e] = p;
-        dp[e] = p * (dp[e] - Dv[i]);
+      for (int kb = 0; kb < 8; ++kb) {
+        s[t] = mfma(ld8(Qs + (32 * t + c32) * KV_S + kb * 16 + h * 8), kf[kb], s[t]);
+        dp[t] = mfma(ld8(Gs + (32 * t + c32) * KV_S + kb * 16 + h * 8), vf[kb], dp[t]);
       }
     }
+    // lane: key column, query rows 32t + 8(e/4) + 4h + e%4
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const bf16x8 pb = pack8(s, c), db = pack8(dp, c);
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 L4 = *(const float4*)(Ls + 32 * t + 8 * g + 4 * h);
+        const float4 D4 = *(const float4*)(Ds + 32 * t + 8 * g + 4 * h);
+        const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * g + i;
+          const float p = __builtin_amdgcn_exp2f((s[t][e] * sc - Lv[i]) * LOG2E);
+          s[t][e] = p;
+          dp[t][e] = p * (dp[t][e] - Dv[i]);
+        }
+      }
+#pragma unroll
+    for (int c = 0; c < 2 * NT; ++c) {
+      const bf16x8 pb = pack8(s[c >> 1], c & 1), db = pack8(dp[c >> 1], c & 1);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
         dv[dt] = mfma(ld4x2(Gt + (32 * dt + c32) * KV_T + 16 * c + 4 * h), pb, dv[dt]);
@@ -319,7 +411,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_mfma_k(AttnBwd a) {
       }
     }
   }
-  if (key >= a.N) return;
+  if (key >= N) return;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -337,7 +429,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_mfma_k(AttnBwd a) {
 }
 
 // ============================================================== dQ
-constexpr int Q_QB = 128, Q_KT = 32;
+constexpr int Q_QB = 128, Q_KT = 64;
 constexpr int Q_S = DH + 8;
 constexpr int Q_T = Q_KT + 8;
 
@@ -354,9 +446,21 @@ __global__ __launch_bounds__(256) void attn_bwd_q_mfma_k(AttnBwd a) {
   const uint16_t* K = (const uint16_t*)a.K + base;
   const uint16_t* V = (const uint16_t*)a.V + base;
   const float sc = rsqrtf((float)DH);
+  const int N = a.N;
+
+  // threads [0, NB) stage K blocks (rows and columns), [NB, 2 NB) V blocks (rows)
+  constexpr int NB = Tile8<Q_KT>::NBLK;
+  constexpr int NT = Q_KT / 32;
+  static_assert(2 * NB <= 256, "tile too large for one block");
+  Tile8<Q_KT> tkv;
+  const int tid = threadIdx.x;
+  const bool isk = tid < NB;
+  tkv.init(tid < 2 * NB ? (isk ? tid : tid - NB) : -1);
+  const uint16_t* src = isk ? K : V;
+  auto rows = [&](int i) -> const uint16_t* { return i < N ? src + (size_t)i * DH : nullptr; };
 
   bf16x8 qf[8], gf[8];
-  const bool qv = q < a.N;
+  const bool qv = q < N;
   const uint16_t* G = (const uint16_t*)a.dO + (qv ? (size_t)row_of_tok_m(a.rm, b, q) * a.ld_do + hd * DH : 0);
 #pragma unroll
   for (int kb = 0; kb < 8; ++kb) {
@@ -367,34 +471,42 @@ __global__ __launch_bounds__(256) void attn_bwd_q_mfma_k(AttnBwd a) {
       qf[kb] = gf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
     }
   }
-  const float L = qv ? a.lse[(size_t)bh * a.N + q] * LOG2E : INFINITY;
-  const float Dl = qv ? a.delta[(size_t)bh * a.N + q] : 0.f;
+  const float L = qv ? a.lse[(size_t)bh * N + q] * LOG2E : INFINITY;
+  const float Dl = qv ? a.delta[(size_t)bh * N + q] : 0.f;
   f32x16 dq[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) dq[i] = zero16();
 
-  for (int k0 = 0; k0 < a.N; k0 += Q_KT) {
+  tkv.load(rows, 0);
+  for (int k0 = 0; k0 < N; k0 += Q_KT) {
     __syncthreads();
-    stage_rows<Q_KT, Q_S>(Ks, K, k0, a.N);
-    stage_rows<Q_KT, Q_S>(Vs, V, k0, a.N);
-    stage_rows_t<Q_KT, Q_T>(Kt, K, k0, a.N);
+    if (isk) { tkv.commit_rows<Q_S>(Ks); tkv.commit_cols<Q_T>(Kt); }
+    else tkv.commit_rows<Q_S>(Vs);
     __syncthreads();
-    f32x16 s = zero16(), dp = zero16();
+    if (k0 + Q_KT < N) tkv.load(rows, k0 + Q_KT);
+    f32x16 s[NT], dp[NT];
 #pragma unroll
-    for (int kb = 0; kb < 8; ++kb) {
-      s = mfma(ld8(Ks + c32 * Q_S + kb * 16 + h * 8), qf[kb], s);
-      dp = mfma(ld8(Vs + c32 * Q_S + kb * 16 + h * 8), gf[kb], dp);
+    for (int t = 0; t < NT; ++t) {
+      s[t] = zero16();
+      dp[t] = zero16();
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) {
+        s[t] = mfma(ld8(Ks + (32 * t + c32) * Q_S + kb * 16 + h * 8), qf[kb], s[t]);
+        dp[t] = mfma(ld8(Vs + (32 * t + c32) * Q_S + kb * 16 + h * 8), gf[kb], dp[t]);
+      }
     }
-    // lane: query column, key rows 8(e/4) + 4h + e%4
+    // lane: query column, key rows 32t + 8(e/4) + 4h + e%4
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int kk = k0 + 8 * (e >> 2) + 4 * h + (e & 3);
-      const float p = kk < a.N ? __builtin_amdgcn_exp2f(s[e] * sc * LOG2E - L) : 0.f;
-      dp[e] = p * (dp[e] - Dl);
-    }
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const bf16x8 db = pack8(dp, c);
+      for (int e = 0; e < 16; ++e) {
+        const int kk = k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3);
+        const float p = kk < N ? __builtin_amdgcn_exp2f(s[t][e] * sc * LOG2E - L) : 0.f;
+        dp[t][e] = p * (dp[t][e] - Dl);
+      }
+#pragma unroll
+    for (int c = 0; c < 2 * NT; ++c) {
+      const bf16x8 db = pack8(dp[c >> 1], c & 1);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(ld4x2(Kt + (32 * dt + c32) * Q_T + 16 * c + 4 * h), db, dq[dt]);
     }
