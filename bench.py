@@ -28,13 +28,14 @@ HBM_PEAK = 8.0e12
 def block_flops(D, F, N, nt, ni, B):
     """Algorithmic FLOPs of one double-block parameter VJP for a batch of B.
 
-    GEMMs: per token 18 D^2 weights (qkv 3, out 1, fc1 4, fc2 4 ... per stream,
-    6 D^2 modulation excluded as it is per sample), forward 2 flops/MAC; the
-    backward does the input-gradient and weight-gradient products (2x forward).
-    Attention backward: 4 N^2 Dh per head (dV, dP, dQ, dK), backward-cost appendix."""
+    GEMMs: per token 4 D^2 + 2 D F weights per stream (qkv, out, fc1, fc2; the
+    per-sample modulation is excluded), 2 flops per multiply-add; the backward
+    does the input-gradient and the weight-gradient products (2x forward).
+    Attention backward: four N x N x Dh products per head (dV, dP, dQ, dK),
+    8 N^2 Dh flops, twice the forward's (backward-cost appendix)."""
     tok = B * N
     gemm_fwd = 2.0 * tok * (3 * D * D + D * D + 2 * D * F)
-    attn_bwd = 4.0 * B * N * N * D
+    attn_bwd = 8.0 * B * N * N * D
     return 2.0 * gemm_fwd + attn_bwd
 
 

@@ -73,13 +73,13 @@ __device__ inline float block_sum(float v, float* sh) {
 
 // tanh(u) = 1 - 2 / (exp(2u) + 1): one exp and one reciprocal, exact limits at
 // +-inf, relative error ~1e-7 (far cheaper in registers than the libm tanhf)
-__device__ inline float tanh_exp(float u) { return 1.f - 2.f / (__expf(2.f * u) + 1.f); }
-__device__ inline float gelu_tanh(float x) {
+__device__ __forceinline__ float tanh_exp(float u) { return 1.f - 2.f / (__expf(2.f * u) + 1.f); }
+__device__ __forceinline__ float gelu_tanh(float x) {
   const float c = 0.7978845608028654f;
   const float th = tanh_exp(c * (x + 0.044715f * x * x * x));
   return 0.5f * x * (1.f + th);
 }
-__device__ inline float gelu_tanh_grad(float x) {
+__device__ __forceinline__ float gelu_tanh_grad(float x) {
   const float c = 0.7978845608028654f;
   const float th = tanh_exp(c * (x + 0.044715f * x * x * x));
   return 0.5f * (1.f + th) + 0.5f * x * (1.f - th * th) * c * (1.f + 3.f * 0.044715f * x * x);

@@ -17,6 +17,7 @@
 // Anything else (fp32 operands, contiguous dims not multiple of 8) takes a
 // plain LDS-tiled VALU kernel with fp32 accumulation.
 #include "gemm.h"
+#include <type_traits>
 #include "prof.h"
 
 namespace jg {
@@ -158,11 +159,11 @@ enum EpiKind {
   EK_DGELU = 6,     // C bf16 = acc * gelu'(aux)
 };
 
-__device__ inline void unpack8(const u32x4& u, float* f) {
+__device__ __forceinline__ void unpack8(const u32x4& u, float* f) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) { f[2 * w] = bf2f(u[w] & 0xffffu); f[2 * w + 1] = bf2f(u[w] >> 16); }
 }
-__device__ inline u32x4 pack8(const float* f) {
+__device__ __forceinline__ u32x4 pack8(const float* f) {
   u32x4 u;
 #pragma unroll
   for (int w = 0; w < 4; ++w) u[w] = (uint32_t)f2bf(f[2 * w]) | ((uint32_t)f2bf(f[2 * w + 1]) << 16);
@@ -171,7 +172,7 @@ __device__ inline u32x4 pack8(const float* f) {
 
 // 8 consecutive outputs of one row, all inside C (vector path)
 template <int EK>
-__device__ inline void epi8(const Epi& e, int row, int col, float* v) {
+__device__ __forceinline__ void epi8(const Epi& e, int row, int col, float* v) {
   if (EK == EK_BIAS || EK == EK_GELU) {
     float bb[8];
     unpack8(*(const u32x4*)((const uint16_t*)e.bias + col), bb);
@@ -214,7 +215,7 @@ __device__ inline void epi8(const Epi& e, int row, int col, float* v) {
 
 // one output element (edge path)
 template <int EK>
-__device__ inline void epi1(const Epi& e, int row, int col, float v) {
+__device__ __forceinline__ void epi1(const Epi& e, int row, int col, float v) {
   if (EK == EK_BIAS || EK == EK_GELU) v += bf2f(((const uint16_t*)e.bias)[col]);
   if (EK == EK_GELU) {
     ((uint16_t*)e.aux)[(size_t)row * e.ldaux + col] = f2bf(v);
@@ -229,6 +230,56 @@ __device__ inline void epi1(const Epi& e, int row, int col, float v) {
     uint16_t* cp = (uint16_t*)e.C;
     cp[idx] = f2bf((EK == EK_BF16_ACC ? bf2f(cp[idx]) : 0.f) + v);
   }
+}
+
+// Epilogue of the MFMA kernels.  Accumulator layout: lane holds column
+// (lane % 32), register e holds row 8*(e/4) + 4*(lane/32) + e%4.  Each 32x32
+// tile is staged transposed through LDS (T[col][row], stride 36 floats) so that
+// every lane then owns 16 consecutive outputs of one row.
+template <int BM, int BN, int WM, int WN, int EK>
+__device__ __forceinline__ void mfma_epilogue(const GemmArgs& g, f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0, int n0,
+                                     uint16_t* lds) {
+  constexpr int TMW = BM / WM, TNW = BN / WN;
+  constexpr int FM = TMW / 32, FN = TNW / 32;
+  constexpr int ES = 36;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  float* T = (float*)lds + wave * 32 * ES;
+  const int h = lane >> 5, c32 = lane & 31;
+  const int rr = lane >> 1, cc = (lane & 1) * 16;
+  const bool vec_ok = (g.N % 8 == 0) && (g.epi.ldc % 8 == 0);
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        float4 x = make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]);
+        *(float4*)(T + c32 * ES + 8 * gq + 4 * h) = x;
+      }
+      __syncthreads();
+      const int row = m0 + wm * TMW + i * 32 + rr;
+      // kept rolled: the accumulator tiles above must stay fully unrolled
+      // (static register indices), and the whole epilogue has to fit the
+      // unroller's budget for that
+#pragma unroll 1
+      for (int half = 0; half < 2; ++half) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = T[(cc + 8 * half + q) * ES + rr];
+        const int col = n0 + wn * TNW + j * 32 + cc + 8 * half;
+        if (row < g.M) {
+          if (vec_ok && col + 8 <= g.N) {
+            epi8<EK>(g.epi, row, col, v);
+          } else {
+#pragma unroll 1
+            for (int q = 0; q < 8; ++q)
+              if (col + q < g.N) epi1<EK>(g.epi, row, col + q, T[(cc + 8 * half + q) * ES + rr]);
+          }
+        }
+      }
+      __syncthreads();
+    }
 }
 
 // --------------------------------------------------------------- MFMA GEMM
@@ -246,7 +297,6 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_mfma_kernel(GemmArgs g) {
   constexpr int TMW = BM / WM, TNW = BN / WN;
   constexpr int FM = TMW / 32, FN = TNW / 32;
   constexpr int STAGE = (BM + BN) * LDSK;
-  constexpr int ES = 36;  // epilogue staging row stride (floats)
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
 
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -325,41 +375,265 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_mfma_kernel(GemmArgs g) {
     __syncthreads();
   }
 
-  // epilogue.  Accumulator layout: lane holds column (lane % 32), register e
-  // holds row 8*(e/4) + 4*(lane/32) + e%4.  Staged transposed: T[col][row].
-  float* T = (float*)lds + wave * 32 * ES;
-  const int h = lane >> 5, c32 = lane & 31;
-  const int rr = lane >> 1, cc = (lane & 1) * 16;
-  const bool vec_ok = (g.N % 8 == 0) && (g.epi.ldc % 8 == 0);
+  __syncthreads();
+  mfma_epilogue<BM, BN, WM, WN, EK>(g, acc, m0, n0, lds);
+}
+
+// ------------------------------------------------- pipelined MFMA GEMM
+// For K a multiple of 64.  Same tiles, LDS layout and epilogue as above, but
+// the k loop is software-pipelined at the instruction level: every 16-deep
+// MFMA step issues, between its MFMAs, the LDS fragment reads of the next step,
+// a share of the LDS writes of the next k tile and the global loads of the one
+// after (sched_group_barrier fixes that interleave), and the workgroup barrier
+// sits before the last MFMA step of a tile so that step hides the first
+// fragment reads of the next tile.
+//
+// All global offsets go through the per-lane voffset of a buffer resource, so
+// the hardware range check covers them: loads past the end of an operand (the
+// two tiles fetched beyond K at the end of the loop, rows past M or N in the
+// last row of an operand) return zero or in-buffer data that only reaches
+// outputs that are never stored.
+__device__ inline u32x4 bload_v(__amdgpu_buffer_rsrc_t r, int voff) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
+
+// k-contiguous operand, P[row * ld + k]: NV 16-byte vectors per thread, RSTEP
+// rows apart, in NSET register sets (a set is refilled right after its
+// contents went to LDS, so NSET sets give the loads NSET k tiles to land);
+// load / store a part [LO, HI) of the vectors per call.
+template <int ROWS, int BK, int NT, int LDSK, int NSET>
+struct PipeN {
+  static constexpr int VPR = BK / 8;
+  static constexpr int NV = ROWS * VPR / NT;
+  static constexpr int RSTEP = NT / VPR;
+  static_assert(ROWS * VPR % NT == 0 && NV >= 1, "tile rows x k must split evenly over the threads");
+  static constexpr int NS = NV;  // store units (one 16-byte LDS write each)
+  u32x4 r[NSET][NV];
+  int voff, sidx, step;
+  __device__ inline void init(int ld, int row0) {
+    const int row = threadIdx.x / VPR, kv = threadIdx.x % VPR;
+    voff = ((row0 + row) * ld + kv * 8) * 2;
+    sidx = row * LDSK + kv * 8;
+    step = RSTEP * ld * 2;
+  }
+  template <int SET, int LO, int HI>
+  __device__ inline void load(__amdgpu_buffer_rsrc_t R, int k0) {
+#pragma unroll
+    for (int i = LO; i < HI; ++i) r[SET][i] = bload_v(R, voff + (k0 * 2 + i * step));
+  }
+  template <int SET, int LO, int HI>
+  __device__ inline void store(uint16_t* S) const {
+#pragma unroll
+    for (int i = LO; i < HI; ++i) *(u32x4*)(S + sidx + i * RSTEP * LDSK) = r[SET][i];
+  }
+};
+
+// k-strided operand, P[k * ld + row]: one 8x8 block per thread (threads past
+// the block count repeat a block: same data to the same place), transposed in
+// registers with byte permutes.
+template <int ROWS, int BK, int NT, int LDSK, int NSET>
+struct PipeT {
+  static constexpr int KB = BK / 8, NBLK = (ROWS / 8) * KB;
+  static constexpr int NB = NBLK > NT ? NBLK / NT : 1;
+  static_assert(NBLK % NT == 0 || NT % NBLK == 0, "8x8 blocks must split evenly over the threads");
+  static constexpr int NV = NB * 8;  // loads
+  static constexpr int NS = NB * 4;  // store units (two 16-byte LDS writes each)
+  u32x4 r[NSET][NB * 8];
+  int voff[NB], sidx[NB];
+  int ld2;
+  __device__ inline void init(int ld, int row0) {
+    ld2 = ld * 2;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int b = (threadIdx.x + i * NT) % NBLK;
+      const int kb = b % KB, rb = b / KB;  // k block fastest: conflict-free 16-byte LDS writes
+      voff[i] = (kb * 8 * ld + row0 + rb * 8) * 2;
+      sidx[i] = rb * 8 * LDSK + kb * 8;
+    }
+  }
+  template <int SET, int LO, int HI>
+  __device__ inline void load(__amdgpu_buffer_rsrc_t R, int k0) {
+#pragma unroll
+    for (int v = LO; v < HI; ++v) r[SET][v] = bload_v(R, voff[v / 8] + (k0 + v % 8) * ld2);
+  }
+  // unit u = (block u / 4, row pair u % 4): rows m = 2mw, 2mw+1 of the block,
+  // word w = element (k = 2w, m) | element (k = 2w + 1, m) << 16
+  template <int SET, int LO, int HI>
+  __device__ inline void store(uint16_t* S) const {
+#pragma unroll
+    for (int u = LO; u < HI; ++u) {
+      const int i = u / 4, mw = u % 4;
+      const u32x4* in = r[SET] + i * 8;
+      u32x4 lo, hi;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        lo[w] = __builtin_amdgcn_perm(in[2 * w + 1][mw], in[2 * w][mw], 0x05040100u);
+        hi[w] = __builtin_amdgcn_perm(in[2 * w + 1][mw], in[2 * w][mw], 0x07060302u);
+      }
+      *(u32x4*)(S + sidx[i] + (2 * mw) * LDSK) = lo;
+      *(u32x4*)(S + sidx[i] + (2 * mw + 1) * LDSK) = hi;
+    }
+  }
+};
+
+template <bool T, int ROWS, int BK, int NT, int LDSK, int NSET>
+struct PipeSel { typedef PipeN<ROWS, BK, NT, LDSK, NSET> type; };
+template <int ROWS, int BK, int NT, int LDSK, int NSET>
+struct PipeSel<true, ROWS, BK, NT, LDSK, NSET> { typedef PipeT<ROWS, BK, NT, LDSK, NSET> type; };
+
+// Instruction interleave of one MFMA step: MF MFMAs, with R LDS reads, W LDS
+// writes and L global loads dealt out between them (reads and writes
+// alternating, then loads), in that order.
+template <int O, int HI, int R, int W>
+__device__ __forceinline__ void sched_ops() {
+  if constexpr (O < HI) {
+    constexpr int RW = 2 * (R < W ? R : W);
+    constexpr int kind = O < RW ? O % 2 : (O < R + W ? (R > W ? 0 : 1) : 2);
+    __builtin_amdgcn_sched_group_barrier(kind == 0 ? 0x100 : (kind == 1 ? 0x200 : 0x020), 1, 0);
+    sched_ops<O + 1, HI, R, W>();
+  }
+}
+template <int MF, int R, int W, int L, int I = 0>
+__device__ __forceinline__ void pipe_sched() {
+  if constexpr (I < MF) {
+    constexpr int T = R + W + L;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    sched_ops<I * T / MF, (I + 1) * T / MF, R, W>();
+    pipe_sched<MF, R, W, L, I + 1>();
+  }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK>
+__global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
+  static_assert(BK == 64, "the schedule is written for four 16-deep MFMA steps per k tile");
+  constexpr int NT = WM * WN * 64;
+  constexpr int LDSK = BK + 8;
+  constexpr int TMW = BM / WM, TNW = BN / WN;
+  constexpr int FM = TMW / 32, FN = TNW / 32;
+  constexpr int STAGE = (BM + BN) * LDSK;
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  // 4-wave tiles keep two register sets (loads two k tiles ahead); 8-wave
+  // tiles have half the registers per wave and keep one
+  constexpr int NSET = NT == 256 ? 2 : 1;
+  typedef typename PipeSel<TA, BM, BK, NT, LDSK, NSET>::type LA;
+  typedef typename PipeSel<TB, BN, BK, NT, LDSK, NSET>::type LB;
+  LA la;
+  LB lb;
+  la.init(g.lda, m0);
+  lb.init(g.ldb, n0);
+  const long ext_a = TA ? ((long)(g.K - 1) * g.lda + g.M) * 2 : ((long)(g.M - 1) * g.lda + g.K) * 2;
+  const long ext_b = TB ? ((long)(g.K - 1) * g.ldb + g.N) * 2 : ((long)(g.N - 1) * g.ldb + g.K) * 2;
+  const __amdgpu_buffer_rsrc_t RA = make_rsrc(g.A, ext_a), RB = make_rsrc(g.B, ext_b);
+
+  f32x16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
-        float4 x = make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]);
-        *(float4*)(T + c32 * ES + 8 * gq + 4 * h) = x;
-      }
-      __syncthreads();
-      const int row = m0 + wm * TMW + i * 32 + rr;
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int fro = (lane & 31) * LDSK + (lane >> 5) * 8;  // this lane's fragment offset
+  bf16x8 fa[2][FM], fb[2][FN];
+  auto ldfrag = [&](const uint16_t* S, int kk, int buf) {
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        float v[8];
+    for (int i = 0; i < FM; ++i)
+      fa[buf][i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(S + (wm * TMW + i * 32) * LDSK + fro + kk * 16));
 #pragma unroll
-        for (int q = 0; q < 8; ++q) v[q] = T[(cc + 8 * half + q) * ES + rr];
-        const int col = n0 + wn * TNW + j * 32 + cc + 8 * half;
-        if (row < g.M) {
-          if (vec_ok && col + 8 <= g.N) {
-            epi8<EK>(g.epi, row, col, v);
-          } else {
+    for (int j = 0; j < FN; ++j)
+      fb[buf][j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(S + (BM + wn * TNW + j * 32) * LDSK + fro + kk * 16));
+  };
+  auto mfma_step = [&](int buf) {
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-              if (col + q < g.N) epi1<EK>(g.epi, row, col + q, v[q]);
-          }
-        }
-      }
-      __syncthreads();
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+  };
+
+  // prologue: tile 0 into LDS stage 0; tiles 1 .. NSET into the register sets
+  // (tile t lives in set t % NSET)
+  la.template load<0, 0, LA::NV>(RA, 0);
+  lb.template load<0, 0, LB::NV>(RB, 0);
+  if constexpr (NSET == 2) {
+    la.template load<1, 0, LA::NV>(RA, BK);
+    lb.template load<1, 0, LB::NV>(RB, BK);
+  }
+  la.template store<0, 0, LA::NS>(lds);
+  lb.template store<0, 0, LB::NS>(lds + BM * LDSK);
+  la.template load<0, 0, LA::NV>(RA, NSET * BK);
+  lb.template load<0, 0, LB::NV>(RB, NSET * BK);
+  __syncthreads();
+  ldfrag(lds, 0, 0);
+
+  // Per k tile kt: stage kt&1 is read, stage (kt+1)&1 is written from register
+  // set (kt+1) % NSET, which is then refilled with tile kt+1+NSET:
+  //   k-contiguous operand: its vectors stored and reloaded in thirds over
+  //     MFMA steps 0, 1, 2;
+  //   k-strided operand: A's block stored and reloaded in step 0, B's in step 1.
+  constexpr int MF = FM * FN, RD = FM + FN;
+  constexpr int A1 = LA::NV / 3, A2 = 2 * LA::NV / 3, B1 = LB::NV / 3, B2 = 2 * LB::NV / 3;
+  constexpr int WA0 = TA ? 2 * LA::NS : A1, WA1 = TA ? 0 : A2 - A1, WA2 = TA ? 0 : LA::NV - A2;
+  constexpr int LA0 = TA ? LA::NV : A1, LA1 = TA ? 0 : A2 - A1, LA2 = TA ? 0 : LA::NV - A2;
+  constexpr int WB0 = TB ? 0 : B1, WB1 = TB ? 2 * LB::NS : B2 - B1, WB2 = TB ? 0 : LB::NV - B2;
+  constexpr int LB0 = TB ? 0 : B1, LB1 = TB ? LB::NV : B2 - B1, LB2 = TB ? 0 : LB::NV - B2;
+  const int nk = g.K / BK;
+  auto iter = [&](auto setc, int kt) {
+    constexpr int SET = decltype(setc)::value;
+    const uint16_t* S = lds + (kt & 1) * STAGE;
+    uint16_t* Sn = lds + ((kt + 1) & 1) * STAGE;
+    const int kl = (kt + 1 + NSET) * BK;
+    // step 0
+    ldfrag(S, 1, 1);
+    if constexpr (TA) { la.template store<SET, 0, LA::NS>(Sn); la.template load<SET, 0, LA::NV>(RA, kl); }
+    else { la.template store<SET, 0, A1>(Sn); la.template load<SET, 0, A1>(RA, kl); }
+    if constexpr (!TB) { lb.template store<SET, 0, B1>(Sn + BM * LDSK); lb.template load<SET, 0, B1>(RB, kl); }
+    mfma_step(0);
+    pipe_sched<MF, RD, WA0 + WB0, LA0 + LB0>();
+    __builtin_amdgcn_sched_barrier(0);
+    // step 1
+    ldfrag(S, 2, 0);
+    if constexpr (!TA) { la.template store<SET, A1, A2>(Sn); la.template load<SET, A1, A2>(RA, kl); }
+    if constexpr (TB) { lb.template store<SET, 0, LB::NS>(Sn + BM * LDSK); lb.template load<SET, 0, LB::NV>(RB, kl); }
+    else { lb.template store<SET, B1, B2>(Sn + BM * LDSK); lb.template load<SET, B1, B2>(RB, kl); }
+    mfma_step(1);
+    pipe_sched<MF, RD, WA1 + WB1, LA1 + LB1>();
+    __builtin_amdgcn_sched_barrier(0);
+    // step 2
+    ldfrag(S, 3, 1);
+    if constexpr (!TA) { la.template store<SET, A2, LA::NV>(Sn); la.template load<SET, A2, LA::NV>(RA, kl); }
+    if constexpr (!TB) { lb.template store<SET, B2, LB::NV>(Sn + BM * LDSK); lb.template load<SET, B2, LB::NV>(RB, kl); }
+    mfma_step(0);
+    pipe_sched<MF, RD, WA2 + WB2, LA2 + LB2>();
+    __builtin_amdgcn_sched_barrier(0);
+    // every write of tile kt+1 and every read of tile kt is done past this barrier
+    __syncthreads();
+    // step 3, hiding the first fragment reads of tile kt+1
+    ldfrag(Sn, 0, 0);
+    mfma_step(1);
+    pipe_sched<MF, RD, 0, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  if constexpr (NSET == 2) {
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      iter(std::integral_constant<int, 1>(), kt);
+      iter(std::integral_constant<int, 0>(), kt + 1);
     }
+    if (kt < nk) iter(std::integral_constant<int, 1>(), kt);
+  } else {
+    for (int kt = 0; kt < nk; ++kt) iter(std::integral_constant<int, 0>(), kt);
+  }
+  __syncthreads();
+  mfma_epilogue<BM, BN, WM, WN, EK>(g, acc, m0, n0, lds);
 }
 
 // ---------------------------------------------------------------- VALU GEMM
@@ -410,14 +684,19 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(GemmArgs g) {
 }
 
 // ------------------------------------------------------------------ launch
-template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK>
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK, bool PIPE>
 static int launch_mfma(const GemmArgs& g, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const size_t lds = 2 * (size_t)(BM + BN) * (BK + 8) * sizeof(uint16_t);
-  auto kern = gemm_mfma_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
+  void (*kern)(GemmArgs);
+  if constexpr (PIPE) kern = gemm_pipe_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
+  else kern = gemm_mfma_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
   static bool attr = false;
   if (!attr) {
-    hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
+      set_error("gemm_mfma: cannot reserve the LDS tile stages");
+      return 3;
+    }
     attr = true;
   }
   hipLaunchKernelGGL(kern, dim3(tiles), dim3(WM * WN * 64), lds, s, g);
@@ -431,13 +710,13 @@ void gemm_set_tile_cfg(int c) { g_tile_cfg = c; }
 
 template <bool TA, bool TB, int EK>
 static int launch_cfg(const GemmArgs& g, hipStream_t s, int cfg) {
+  // K not a multiple of the 64-deep k tile: the edge-checked kernel
+  if (g.K % 64 != 0) return launch_mfma<128, 128, 64, 2, 2, TA, TB, EK, false>(g, s);
   switch (cfg) {
-    case 1: return launch_mfma<128, 128, 64, 2, 2, TA, TB, EK>(g, s);
-    case 2: return launch_mfma<256, 128, 64, 2, 2, TA, TB, EK>(g, s);
-    case 4: return launch_mfma<256, 256, 64, 2, 2, TA, TB, EK>(g, s);
-    case 6: return launch_mfma<256, 256, 64, 2, 4, TA, TB, EK>(g, s);
-    case 7: return launch_mfma<256, 256, 32, 2, 4, TA, TB, EK>(g, s);
-    default: return launch_mfma<256, 256, 64, 2, 2, TA, TB, EK>(g, s);
+    case 1: return launch_mfma<128, 128, 64, 2, 2, TA, TB, EK, true>(g, s);
+    case 2: return launch_mfma<256, 128, 64, 2, 2, TA, TB, EK, true>(g, s);
+    case 6: return launch_mfma<256, 256, 64, 2, 4, TA, TB, EK, true>(g, s);
+    default: return launch_mfma<256, 256, 64, 2, 2, TA, TB, EK, true>(g, s);
   }
 }
 
@@ -505,16 +784,14 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   const double eb = 2.0 * (g.tb ? (double)g.K * g.ldb : (double)g.N * g.ldb);
   if (ea >= 2147483000.0 || eb >= 2147483000.0) mfma = false;
   if (mfma && ek >= 0) {
-    // default tiles: 256x256 whenever that grid still covers the 256 CUs
-    // (4 waves for the products with a transposed operand, 8 waves for the
-    // forward product), else 128x128
-    // (the GELU epilogues keep too many values live for the 4-wave 256x256
-    // tile: the backward one takes the 8-wave tile, the forward one 128x128)
+    // default tiles: 256x256 (8 waves for the forward product, whose
+    // operands both load without a transpose, 4 waves otherwise); 128x128
+    // only for grids too small to cover a quarter of the chip with 256x256
     int cfg = g_tile_cfg;
     if (cfg == 0) {
       const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-      if (t256 < 256 || ek == EK_GELU) cfg = 1;
-      else if (ek == EK_DGELU || (!g.ta && !g.tb)) cfg = 6;
+      if (t256 < 64) cfg = 1;
+      else if (!g.ta && !g.tb) cfg = 6;
       else cfg = 4;
     }
     if (!g.ta && !g.tb) return launch_kind<false, false>(g, s, cfg, ek);
