@@ -636,6 +636,204 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
   mfma_epilogue<BM, BN, WM, WN, EK>(g, acc, m0, n0, lds);
 }
 
+// --------------------------------------------- direct-to-LDS MFMA GEMM
+// 256x256 workgroup tile, 4 waves (128x128 each), 32-deep k tiles through 4
+// LDS stages, for K a multiple of 32.  Operands go from memory straight into
+// LDS (buffer loads with the LDS bit: no register staging and no LDS write
+// instructions), three k tiles ahead of the MFMAs.  LDS rows are unpadded and
+// 16-byte chunks are XOR-swizzled by row so that both the 1 KB contiguous
+// direct loads and the fragment reads are free of bank conflicts:
+//   k-contiguous operand, tile [row][32 k] (64 B rows):
+//     chunk' = chunk ^ (((row >> 1) ^ (row >> 3)) & 3),
+//     fragments are single 16-byte reads;
+//   k-strided operand, tile [32 k][256 rows] (512 B rows):
+//     chunk' = chunk ^ (((k & 3) << 1) | ((k & 1) << 3)),
+//     fragments are two transposing 8-byte reads (ds_read_b64_tr_b16), each
+//     of which hands lane i of a 16-lane group element (row e, column i) of
+//     the 4 x 16 block the group fetched.
+// Ragged M / N edges rely on the buffer range check like the kernels above.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+#define JG_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+// Workgroup barrier for the direct-loaded stages: this wave's LDS reads done
+// (lgkmcnt 0) and at most 16 direct loads still in flight (vmcnt 16: the
+// loads of the two newest k tiles), then s_barrier.  Unlike __syncthreads
+// there is no release fence, which would wait for every direct load (they
+// are LDS writes) and drain the prefetch; the empty asm statements keep the
+// compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier_vm16() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((16 & 15) | ((16 >> 4) << 14) | 0x70);  // vmcnt(16) expcnt(7) lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ int swz_n(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+__device__ __forceinline__ int swz_t(int k) { return ((k & 3) << 1) | ((k & 1) << 3); }
+
+// One operand of the direct-to-LDS kernel: 16 KB per k tile, 4 direct loads
+// of 1 KB per wave.
+template <bool T>
+struct DtlOp {
+  int voff[4];   // per load: byte offset at k = 0
+  int kmul;      // bytes per unit of k
+  int fo[4];     // fragment read offsets (bytes) per 32-row fragment
+  __device__ inline void init(int ld, int row0, int wrow0) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int b = wave * 4 + t;  // 1 KB block of the tile
+      if (!T) {
+        const int row = 16 * b + lane / 4, q = (lane % 4) ^ swz_n(row);
+        voff[t] = ((row0 + row) * ld + 8 * q) * 2;
+      } else {
+        const int kr = 2 * b + lane / 32, c = (lane % 32) ^ swz_t(kr);
+        voff[t] = (kr * ld + row0 + 8 * c) * 2;
+      }
+    }
+    kmul = T ? ld * 2 : 2;
+    if (!T) {
+      const int r = lane & 31;  // fragment row within a 32-row fragment
+      fo[0] = (wrow0 + r) * 64 + (((lane >> 5)) ^ swz_n(r)) * 16;        // k16 step 0
+      fo[1] = (wrow0 + r) * 64 + (((lane >> 5) + 2) ^ swz_n(r)) * 16;    // k16 step 1
+      fo[2] = fo[3] = 0;
+    } else {
+      const int g = (lane >> 4) & 3, i16 = lane & 15;
+      const int kr = 8 * (g >> 1) + (i16 >> 2);  // row within the k16 step (first read)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = wrow0 + 32 * i + 16 * (g & 1) + 4 * (i16 & 3);
+        fo[i] = kr * 512 + (((m >> 3) ^ swz_t(kr)) << 4) + ((m >> 2) & 1) * 8;
+      }
+    }
+  }
+  // direct loads of the k tile at k0 into the stage at S (byte pointer)
+  __device__ inline void load(__amdgpu_buffer_rsrc_t R, char* S, int k0) const {
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, JG_LDS(S + (wave * 4 + t) * 1024), 16, voff[t] + k0 * kmul, 0, 0, 0);
+  }
+  // fragment i (32 rows) of k16 step kk from the stage at S
+  __device__ inline bf16x8 frag(const char* S, int i, int kk) const {
+    if (!T) {
+      return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + fo[kk] + i * 32 * 64));
+    } else {
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(S + fo[i] + kk * 16 * 512));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(S + fo[i] + kk * 16 * 512 + 4 * 512));
+      typedef short s16x8 __attribute__((ext_vector_type(8)));
+      const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      return __builtin_bit_cast(bf16x8, v);
+    }
+  }
+};
+
+template <bool TA, bool TB, int EK>
+__global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
+  constexpr int BM = 256, BN = 256, BK = 32, WM = 2, WN = 2, FM = 4, FN = 4;
+  constexpr int STG = 32768;  // bytes per stage: A 16 KB, B 16 KB
+  // one variable per stage: every LDS access names its stage statically, so
+  // the compiler can tell the fragment reads of one stage from the direct
+  // loads still landing in another and does not wait for the latter
+  __shared__ __attribute__((aligned(1024))) char st0[STG];
+  __shared__ __attribute__((aligned(1024))) char st1[STG];
+  __shared__ __attribute__((aligned(1024))) char st2[STG];
+  __shared__ __attribute__((aligned(1024))) char st3[STG];
+
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  DtlOp<TA> oa;
+  DtlOp<TB> ob;
+  oa.init(g.lda, m0, wm * 128);
+  ob.init(g.ldb, n0, wn * 128);
+  const long ext_a = TA ? ((long)(g.K - 1) * g.lda + g.M) * 2 : ((long)(g.M - 1) * g.lda + g.K) * 2;
+  const long ext_b = TB ? ((long)(g.K - 1) * g.ldb + g.N) * 2 : ((long)(g.N - 1) * g.ldb + g.K) * 2;
+  const __amdgpu_buffer_rsrc_t RA = make_rsrc(g.A, ext_a), RB = make_rsrc(g.B, ext_b);
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  auto stage = [&](auto ic) -> char* {
+    constexpr int c = decltype(ic)::value & 3;
+    if constexpr (c == 0) return st0;
+    else if constexpr (c == 1) return st1;
+    else if constexpr (c == 2) return st2;
+    else return st3;
+  };
+  bf16x8 fa[2][FM], fb[2][FN];
+  auto ldfrag = [&](const char* S, int kk, int buf) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[buf][i] = oa.frag(S, i, kk);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[buf][j] = ob.frag(S + 16384, j, kk);
+  };
+  auto mfma_step = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+  };
+  auto load_tile = [&](char* S, int t) {
+    oa.load(RA, S, t * BK);
+    ob.load(RB, S + 16384, t * BK);
+  };
+
+  // prologue: tiles 0, 1, 2 in flight; wait for tile 0
+  const int nk = g.K / BK;
+  load_tile(st0, 0);
+  load_tile(st1, 1);
+  load_tile(st2, 2);
+  lds_barrier_vm16();  // tiles 1 and 2 may still fly
+  ldfrag(st0, 0, 0);
+
+  constexpr int RD = (TA ? 2 : 1) * FM + (TB ? 2 : 1) * FN;  // LDS reads per k16 step
+  // k tile kt is read from stage kt % 4, tile kt+3 loads into stage (kt+3) % 4
+  auto iter = [&](auto ic, int kt) {
+    constexpr int c = decltype(ic)::value;
+    const char* S = stage(std::integral_constant<int, c>());
+    const char* Sn = stage(std::integral_constant<int, c + 1>());
+    // step 0: fragments of step 1 and the direct loads of tile kt+3 (its stage
+    // was last read before the previous barrier)
+    ldfrag(S, 1, 1);
+    load_tile(stage(std::integral_constant<int, c + 3>()), kt + 3);
+    mfma_step(0);
+    pipe_sched<16, RD, 0, 8>();
+    __builtin_amdgcn_sched_barrier(0);
+    // tile kt+1 has landed once at most the 16 loads of tiles kt+2, kt+3 fly
+    lds_barrier_vm16();
+    // step 1, hiding the first fragment reads of tile kt+1
+    ldfrag(Sn, 0, 0);
+    mfma_step(1);
+    pipe_sched<16, RD, 0, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  int kt = 0;
+  for (; kt + 3 < nk; kt += 4) {
+    iter(std::integral_constant<int, 0>(), kt);
+    iter(std::integral_constant<int, 1>(), kt + 1);
+    iter(std::integral_constant<int, 2>(), kt + 2);
+    iter(std::integral_constant<int, 3>(), kt + 3);
+  }
+  if (kt < nk) iter(std::integral_constant<int, 0>(), kt);
+  if (kt + 1 < nk) iter(std::integral_constant<int, 1>(), kt + 1);
+  if (kt + 2 < nk) iter(std::integral_constant<int, 2>(), kt + 2);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  mfma_epilogue<BM, BN, WM, WN, EK>(g, acc, m0, n0, (uint16_t*)st0);
+}
+
 // ---------------------------------------------------------------- VALU GEMM
 // 64x64 tile, 256 threads, 4x4 outputs per thread, fp32 accumulation, any
 // layout and operand dtype.
@@ -709,7 +907,25 @@ static int g_tile_cfg = 0;
 void gemm_set_tile_cfg(int c) { g_tile_cfg = c; }
 
 template <bool TA, bool TB, int EK>
+static int launch_dtl(const GemmArgs& g, hipStream_t s) {
+  const int tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  hipLaunchKernelGGL((gemm_dtl_kernel<TA, TB, EK>), dim3(tiles), dim3(256), 0, s, g);
+  JG_CHECK_LAUNCH("gemm_dtl");
+  return 0;
+}
+
+// The direct-to-LDS kernel computes 32-bit byte offsets up to three k tiles
+// past K; they must stay below 2^31.
+static bool dtl_fits(const GemmArgs& g) {
+  const double kx = (double)g.K + 128.0;
+  const double ea = 2.0 * (g.ta ? kx * g.lda + g.M : (double)g.M * g.lda + kx);
+  const double eb = 2.0 * (g.tb ? kx * g.ldb + g.N : (double)g.N * g.ldb + kx);
+  return g.K % 32 == 0 && ea < 2147483000.0 && eb < 2147483000.0;
+}
+
+template <bool TA, bool TB, int EK>
 static int launch_cfg(const GemmArgs& g, hipStream_t s, int cfg) {
+  if (cfg == 8 && dtl_fits(g)) return launch_dtl<TA, TB, EK>(g, s);
   // K not a multiple of the 64-deep k tile: the edge-checked kernel
   if (g.K % 64 != 0) return launch_mfma<128, 128, 64, 2, 2, TA, TB, EK, false>(g, s);
   switch (cfg) {
@@ -784,15 +1000,16 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   const double eb = 2.0 * (g.tb ? (double)g.K * g.ldb : (double)g.N * g.ldb);
   if (ea >= 2147483000.0 || eb >= 2147483000.0) mfma = false;
   if (mfma && ek >= 0) {
-    // default tiles: 256x256 (8 waves for the forward product, whose
-    // operands both load without a transpose, 4 waves otherwise); 128x128
-    // only for grids too small to cover a quarter of the chip with 256x256
+    // default tiles: 256x256; products with a k-strided operand (weight and
+    // input gradients) take the direct-to-LDS kernel, the forward product the
+    // 8-wave register-staged one; 128x128 only for grids too small to cover a
+    // quarter of the chip with 256x256
     int cfg = g_tile_cfg;
     if (cfg == 0) {
       const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
       if (t256 < 64) cfg = 1;
       else if (!g.ta && !g.tb) cfg = 6;
-      else cfg = 4;
+      else cfg = dtl_fits(g) ? 8 : 4;
     }
     if (!g.ta && !g.tb) return launch_kind<false, false>(g, s, cfg, ek);
     if (!g.ta && g.tb) return launch_kind<false, true>(g, s, cfg, ek);
