@@ -19,6 +19,7 @@
 // padded queries are not written).
 #include "attention.h"
 #include "prof.h"
+#include <type_traits>
 
 namespace jg {
 
@@ -523,6 +524,325 @@ __global__ __launch_bounds__(256) void attn_bwd_q_mfma_k(AttnBwd a) {
     }
 }
 
+// ====================================================== backward, v2
+// Tiles of 64 rows x 128 (one head) are fetched straight into LDS by buffer
+// loads with the LDS bit (no register staging), three k tiles in flight, one
+// barrier per tile.  A tile is stored unpadded, 256 B per row, with the 16-byte
+// chunks of row r XOR-swizzled by asw(r); the table makes both fragment
+// patterns conflict-free whether the LDS serves 8 or 16 lanes per cycle:
+//   row fragments (16-byte reads, 8/16 consecutive rows, one chunk) and
+//   transposed fragments (ds_read_b64_tr_b16: 4 consecutive rows x 32 B per
+//   16 lanes), which replace the transposed tile copies: lane i of a 16-lane
+//   group receives element (row e, column i) of the 4 x 16 block the group
+//   fetched, so two such reads give the A operand of a product that contracts
+//   over the tile rows, in the row order the accumulator-fed B operand uses.
+constexpr unsigned long long ASW = 0xf953e842db71ca60ull;
+__device__ __forceinline__ int asw(int r) { return (int)((ASW >> (4 * (r & 15))) & 15); }
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+#define ALDS(p) ((__attribute__((address_space(3))) void*)(p))
+constexpr int AOOB = 0x7ffffff0;  // buffer offset past any resource: loads return zero
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t arsrc(const void* p, long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, (int)bytes, 0x00020000);
+}
+
+// Per-lane constants of one 64-row tile: direct-load slots and fragment offsets.
+struct ATile {
+  int lrow[4], lchunk[4];  // direct loads: tile row and source chunk of this lane, per load
+  int roff[8];             // row fragment, k16 step kb: byte offset for tile row (lane % 32)
+  int t1[4], t2[4];        // transposed fragment, 32-column block dt: the two reads
+  __device__ inline void init() {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      lrow[t] = 4 * (wave * 4 + t) + lane / 16;
+      lchunk[t] = (lane % 16) ^ asw(lrow[t]);
+    }
+    const int rr = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int kb = 0; kb < 8; ++kb) roff[kb] = rr * 256 + (((2 * kb + h) ^ asw(rr)) << 4);
+    const int g = lane >> 4, j = lane & 15;
+    const int q1 = 4 * (g >> 1) + (j >> 2), q2 = q1 + 8;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const int ch = 4 * dt + 2 * (g & 1) + ((j & 3) >> 1);
+      t1[dt] = q1 * 256 + ((ch ^ asw(q1)) << 4) + (j & 1) * 8;
+      t2[dt] = q2 * 256 + ((ch ^ asw(q2)) << 4) + (j & 1) * 8;
+    }
+  }
+  // 16 direct loads of 1 KB (4 rows each), 4 per wave; rowoff(r) = byte offset
+  // of tile row r in the resource, or a negative value for a padding row
+  template <class RowOff>
+  __device__ inline void load(__amdgpu_buffer_rsrc_t R, char* S, RowOff rowoff) const {
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int ro = rowoff(lrow[t]);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, ALDS(S + (wave * 4 + t) * 1024), 16, ro < 0 ? AOOB : ro + lchunk[t] * 16,
+                                               0, 0, 0);
+    }
+  }
+  // A fragment of rows 32t + (lane % 32), elements 16kb + 8(lane / 32) .. +7
+  __device__ inline bf16x8 row(const char* S, int t, int kb) const {
+    return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + roff[kb] + t * 8192));
+  }
+  // A fragment of the transposed tile: row d = 32dt + (lane % 32), contraction
+  // slots = tile rows 16c + 4(lane / 32) + 0..3 and 16c + 8 + 4(lane / 32) + 0..3
+  __device__ inline bf16x8 tr(const char* S, int c, int dt) const {
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + t1[dt] + c * 4096));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + t2[dt] + c * 4096));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+  }
+};
+
+// LDS barrier for the direct-loaded stages: this wave's loads older than its
+// newest NL are done (they are LDS writes), its LDS reads are done, then
+// s_barrier.  No release fence: __syncthreads would wait for every direct
+// load still in flight.  The empty asm statements keep the compiler from
+// moving memory accesses across it.
+template <int NL>
+__device__ __forceinline__ void attn_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((NL & 15) | ((NL >> 4) << 14) | 0x70);  // vmcnt(NL) expcnt(7) lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// ------------------------------------------------------------ dK, dV (v2)
+// 128 keys per workgroup (32 per wave, K and V fragments in registers); query
+// tiles of 64 rows of Q and dO, with their log-sum-exp and delta, stream
+// through three LDS stages.
+constexpr int KV2_KB = 128, KV2_QT = 64;
+
+__global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
+  __shared__ __attribute__((aligned(1024))) char Q0[16384], G0[16384], Q1[16384], G1[16384], Q2[16384], G2[16384];
+  __shared__ __attribute__((aligned(256))) float L0[64], D0[64], L1[64], D1[64], L2[64], D2[64];
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const int key = blockIdx.x * KV2_KB + w * 32 + c32;
+  const int N = a.N;
+  const size_t base = (size_t)bh * N * DH;
+  const uint16_t* K = (const uint16_t*)a.K + base;
+  const uint16_t* V = (const uint16_t*)a.V + base;
+  const float sc = rsqrtf((float)DH), scl = sc * LOG2E;
+  const __amdgpu_buffer_rsrc_t RQ = arsrc((const uint16_t*)a.Q + base, (long)N * DH * 2);
+  const __amdgpu_buffer_rsrc_t RG = arsrc(a.dO, (long)a.rm.rows() * a.ld_do * 2);
+  const __amdgpu_buffer_rsrc_t RL = arsrc(a.lse + (size_t)bh * N, (long)N * 4);
+  const __amdgpu_buffer_rsrc_t RD = arsrc(a.delta + (size_t)bh * N, (long)N * 4);
+  ATile at;
+  at.init();
+
+  bf16x8 kf[8], vf[8];
+#pragma unroll
+  for (int kb = 0; kb < 8; ++kb) {
+    if (key < N) {
+      kf[kb] = ld8(K + (size_t)key * DH + kb * 16 + h * 8);
+      vf[kb] = ld8(V + (size_t)key * DH + kb * 16 + h * 8);
+    } else {
+      kf[kb] = vf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    }
+  }
+  f32x16 dv[4], dk[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
+
+  auto load_tile = [&](char* Qd, char* Gd, float* Ld, float* Dd, int q0) {
+    at.load(RQ, Qd, [&](int r) { return (q0 + r) * (DH * 2); });
+    at.load(RG, Gd, [&](int r) {
+      const int q = q0 + r;
+      return q < N ? (row_of_tok_m(a.rm, b, q) * a.ld_do + hd * DH) * 2 : -1;
+    });
+    if (w == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(RL, ALDS(Ld), 4, (q0 + lane) * 4, 0, 0, 0);
+    if (w == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(RD, ALDS(Dd), 4, (q0 + lane) * 4, 0, 0, 0);
+  };
+  const int ntile = (N + KV2_QT - 1) / KV2_QT;
+  load_tile(Q0, G0, L0, D0, 0);
+  load_tile(Q1, G1, L1, D1, KV2_QT);
+
+  auto iter = [&](auto ic, int it) {
+    constexpr int c = decltype(ic)::value;
+    char* Qc = c == 0 ? Q0 : (c == 1 ? Q1 : Q2);
+    char* Gc = c == 0 ? G0 : (c == 1 ? G1 : G2);
+    const float* Lc = c == 0 ? L0 : (c == 1 ? L1 : L2);
+    const float* Dc = c == 0 ? D0 : (c == 1 ? D1 : D2);
+    const int q0 = it * KV2_QT;
+    // tile it has landed once at most this wave's loads of tile it+1 fly
+    if (w < 2) attn_barrier<9>(); else attn_barrier<8>();
+    // the stage of tile it+2 was last read in the previous iteration
+    if constexpr (c == 0) load_tile(Q2, G2, L2, D2, q0 + 2 * KV2_QT);
+    else if constexpr (c == 1) load_tile(Q0, G0, L0, D0, q0 + 2 * KV2_QT);
+    else load_tile(Q1, G1, L1, D1, q0 + 2 * KV2_QT);
+    f32x16 s[2], dp[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      s[t] = zero16();
+      dp[t] = zero16();
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) {
+        s[t] = mfma(at.row(Qc, t, kb), kf[kb], s[t]);
+        dp[t] = mfma(at.row(Gc, t, kb), vf[kb], dp[t]);
+      }
+    }
+    // lane: key column, query rows 32t + 8(e/4) + 4h + e%4
+    const bool full = q0 + KV2_QT <= N;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 L4 = *(const float4*)(Lc + 32 * t + 8 * g + 4 * h);
+        const float4 D4 = *(const float4*)(Dc + 32 * t + 8 * g + 4 * h);
+        const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * g + i;
+          float p = __builtin_amdgcn_exp2f(s[t][e] * scl - Lv[i] * LOG2E);
+          if (!full && q0 + 32 * t + 8 * g + 4 * h + i >= N) p = 0.f;
+          s[t][e] = p;
+          dp[t][e] = p * (dp[t][e] - Dv[i]);
+        }
+      }
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+      const bf16x8 pb = pack8(s[cc >> 1], cc & 1), db = pack8(dp[cc >> 1], cc & 1);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        dv[dt] = mfma(at.tr(Gc, cc, dt), pb, dv[dt]);
+        dk[dt] = mfma(at.tr(Qc, cc, dt), db, dk[dt]);
+      }
+    }
+  };
+  int it = 0;
+  for (; it + 2 < ntile; it += 3) {
+    iter(std::integral_constant<int, 0>(), it);
+    iter(std::integral_constant<int, 1>(), it + 1);
+    iter(std::integral_constant<int, 2>(), it + 2);
+  }
+  if (it < ntile) iter(std::integral_constant<int, 0>(), it);
+  if (it + 1 < ntile) iter(std::integral_constant<int, 1>(), it + 1);
+  // no direct load may still be landing when the workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(0);
+  if (key >= N) return;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 vk, vv;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        vk[i] = (__bf16)(dk[dt][4 * g + i] * sc);
+        vv[i] = (__bf16)dv[dt][4 * g + i];
+      }
+      const size_t off = base + (size_t)key * DH + 32 * dt + 8 * g + 4 * h;
+      *(bf16x4*)((uint16_t*)a.dK + off) = vk;
+      *(bf16x4*)((uint16_t*)a.dV + off) = vv;
+    }
+}
+
+// ------------------------------------------------------------ dQ (v2)
+// 128 queries per workgroup (32 per wave, Q and dO fragments in registers);
+// key tiles of 64 rows of K and V stream through three LDS stages.
+constexpr int Q2_QB = 128, Q2_KT = 64;
+
+__global__ __launch_bounds__(256) void attn_bwd_q2_k(AttnBwd a) {
+  __shared__ __attribute__((aligned(1024))) char K0[16384], V0[16384], K1[16384], V1[16384], K2[16384], V2[16384];
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const int q = blockIdx.x * Q2_QB + w * 32 + c32;
+  const int N = a.N;
+  const size_t base = (size_t)bh * N * DH;
+  const uint16_t* Q = (const uint16_t*)a.Q + base;
+  const float sc = rsqrtf((float)DH), scl = sc * LOG2E;
+  const __amdgpu_buffer_rsrc_t RK = arsrc((const uint16_t*)a.K + base, (long)N * DH * 2);
+  const __amdgpu_buffer_rsrc_t RV = arsrc((const uint16_t*)a.V + base, (long)N * DH * 2);
+  ATile at;
+  at.init();
+
+  bf16x8 qf[8], gf[8];
+  const bool qv = q < N;
+  const uint16_t* G = (const uint16_t*)a.dO + (qv ? (size_t)row_of_tok_m(a.rm, b, q) * a.ld_do + hd * DH : 0);
+#pragma unroll
+  for (int kb = 0; kb < 8; ++kb) {
+    if (qv) {
+      qf[kb] = ld8(Q + (size_t)q * DH + kb * 16 + h * 8);
+      gf[kb] = ld8(G + kb * 16 + h * 8);
+    } else {
+      qf[kb] = gf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    }
+  }
+  const float L = qv ? a.lse[(size_t)bh * N + q] * LOG2E : INFINITY;
+  const float Dl = qv ? a.delta[(size_t)bh * N + q] : 0.f;
+  f32x16 dq[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dq[i] = zero16();
+
+  auto load_tile = [&](char* Kd, char* Vd, int k0) {
+    at.load(RK, Kd, [&](int r) { return (k0 + r) * (DH * 2); });
+    at.load(RV, Vd, [&](int r) { return (k0 + r) * (DH * 2); });
+  };
+  const int ntile = (N + Q2_KT - 1) / Q2_KT;
+  load_tile(K0, V0, 0);
+  load_tile(K1, V1, Q2_KT);
+
+  auto iter = [&](auto ic, int it) {
+    constexpr int c = decltype(ic)::value;
+    char* Kc = c == 0 ? K0 : (c == 1 ? K1 : K2);
+    char* Vc = c == 0 ? V0 : (c == 1 ? V1 : V2);
+    const int k0 = it * Q2_KT;
+    attn_barrier<8>();
+    if constexpr (c == 0) load_tile(K2, V2, k0 + 2 * Q2_KT);
+    else if constexpr (c == 1) load_tile(K0, V0, k0 + 2 * Q2_KT);
+    else load_tile(K1, V1, k0 + 2 * Q2_KT);
+    f32x16 s[2], dp[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      s[t] = zero16();
+      dp[t] = zero16();
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) {
+        s[t] = mfma(at.row(Kc, t, kb), qf[kb], s[t]);
+        dp[t] = mfma(at.row(Vc, t, kb), gf[kb], dp[t]);
+      }
+    }
+    // lane: query column, key rows 32t + 8(e/4) + 4h + e%4
+    const bool full = k0 + Q2_KT <= N;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float p = __builtin_amdgcn_exp2f(s[t][e] * scl - L);
+        if (!full && k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3) >= N) p = 0.f;
+        dp[t][e] = p * (dp[t][e] - Dl);
+      }
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+      const bf16x8 db = pack8(dp[cc >> 1], cc & 1);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(at.tr(Kc, cc, dt), db, dq[dt]);
+    }
+  };
+  int it = 0;
+  for (; it + 2 < ntile; it += 3) {
+    iter(std::integral_constant<int, 0>(), it);
+    iter(std::integral_constant<int, 1>(), it + 1);
+    iter(std::integral_constant<int, 2>(), it + 2);
+  }
+  if (it < ntile) iter(std::integral_constant<int, 0>(), it);
+  if (it + 1 < ntile) iter(std::integral_constant<int, 1>(), it + 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  if (!qv) return;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(dq[dt][4 * g + i] * sc);
+      *(bf16x4*)((uint16_t*)a.dQ + base + (size_t)q * DH + 32 * dt + 8 * g + 4 * h) = v;
+    }
+}
+
 // ============================================================== dispatch
 static bool mfma_ok(int Dh, int dt, const void* O, int ld_o) {
   return Dh == DH && dt == BF16 && ((uintptr_t)O % 16 == 0) && (ld_o % 8 == 0);
@@ -544,12 +864,16 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   hipLaunchKernelGGL(attn_delta_mfma_k, dim3((a.rm.rows() + 3) / 4), dim3(256), 0, s, a);
   JG_CHECK_LAUNCH("attention_delta_mfma");
   const double nn = (double)a.B * a.H * a.N * (double)a.N * DH;
+  // the direct-load kernels address dO with 32-bit byte offsets
+  const bool v2 = (double)a.rm.rows() * a.ld_do * 2.0 < 2147483000.0 && (double)a.N * DH * 2.0 * 3 < 2147483000.0;
   int pi = prof_begin(PROF_ATTN_BWD_KV, s);
-  hipLaunchKernelGGL(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0, s, a);
+  if (v2) hipLaunchKernelGGL(attn_bwd_kv2_k, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0, s, a);
   prof_end(pi, s, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
   pi = prof_begin(PROF_ATTN_BWD_Q, s);
-  hipLaunchKernelGGL(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0, s, a);
+  if (v2) hipLaunchKernelGGL(attn_bwd_q2_k, dim3((a.N + Q2_QB - 1) / Q2_QB, a.B * a.H), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0, s, a);
   prof_end(pi, s, 2.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_q_mfma");
   return 0;
