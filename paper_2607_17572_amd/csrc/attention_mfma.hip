@@ -661,8 +661,12 @@ __global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
   load_tile(Q0, G0, L0, D0, 0);
   load_tile(Q1, G1, L1, D1, KV2_QT);
 
-  auto iter = [&](auto ic, int it) {
+  // one query tile: for each 32-row half, S and dP, the softmax terms, then
+  // the dV and dK products of that half (the halves overlap MFMA and VALU work
+  // and keep only one half's scores live); MASK: the ragged last tile
+  auto iter = [&](auto ic, auto mc, int it) {
     constexpr int c = decltype(ic)::value;
+    constexpr bool MASK = decltype(mc)::value;
     char* Qc = c == 0 ? Q0 : (c == 1 ? Q1 : Q2);
     char* Gc = c == 0 ? G0 : (c == 1 ? G1 : G2);
     const float* Lc = c == 0 ? L0 : (c == 1 ? L1 : L2);
@@ -671,24 +675,21 @@ __global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
     // tile it has landed once at most this wave's loads of tile it+1 fly
     if (w < 2) attn_barrier<9>(); else attn_barrier<8>();
     // the stage of tile it+2 was last read in the previous iteration
-    if constexpr (c == 0) load_tile(Q2, G2, L2, D2, q0 + 2 * KV2_QT);
-    else if constexpr (c == 1) load_tile(Q0, G0, L0, D0, q0 + 2 * KV2_QT);
-    else load_tile(Q1, G1, L1, D1, q0 + 2 * KV2_QT);
-    f32x16 s[2], dp[2];
+    if constexpr (!MASK) {
+      if constexpr (c == 0) load_tile(Q2, G2, L2, D2, q0 + 2 * KV2_QT);
+      else if constexpr (c == 1) load_tile(Q0, G0, L0, D0, q0 + 2 * KV2_QT);
+      else load_tile(Q1, G1, L1, D1, q0 + 2 * KV2_QT);
+    }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      s[t] = zero16();
-      dp[t] = zero16();
+      f32x16 st = mfma(at.row(Qc, t, 0), kf[0], zero16());
+      f32x16 dpt = mfma(at.row(Gc, t, 0), vf[0], zero16());
 #pragma unroll
-      for (int kb = 0; kb < 8; ++kb) {
-        s[t] = mfma(at.row(Qc, t, kb), kf[kb], s[t]);
-        dp[t] = mfma(at.row(Gc, t, kb), vf[kb], dp[t]);
+      for (int kb = 1; kb < 8; ++kb) {
+        st = mfma(at.row(Qc, t, kb), kf[kb], st);
+        dpt = mfma(at.row(Gc, t, kb), vf[kb], dpt);
       }
-    }
-    // lane: key column, query rows 32t + 8(e/4) + 4h + e%4
-    const bool full = q0 + KV2_QT <= N;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
+      // lane: key column, query rows 32t + 8(e/4) + 4h + e%4
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const float4 L4 = *(const float4*)(Lc + 32 * t + 8 * g + 4 * h);
@@ -697,30 +698,42 @@ __global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int e = 4 * g + i;
-          float p = __builtin_amdgcn_exp2f(s[t][e] * scl - Lv[i] * LOG2E);
-          if (!full && q0 + 32 * t + 8 * g + 4 * h + i >= N) p = 0.f;
-          s[t][e] = p;
-          dp[t][e] = p * (dp[t][e] - Dv[i]);
+          float p = __builtin_amdgcn_exp2f(fmaf(st[e], scl, -Lv[i] * LOG2E));
+          if (MASK && q0 + 32 * t + 8 * g + 4 * h + i >= N) p = 0.f;
+          st[e] = p;
+          dpt[e] = p * (dpt[e] - Dv[i]);
         }
       }
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc) {
-      const bf16x8 pb = pack8(s[cc >> 1], cc & 1), db = pack8(dp[cc >> 1], cc & 1);
+      for (int half = 0; half < 2; ++half) {
+        const int cc = 2 * t + half;
+        const bf16x8 pb = pack8(st, half), db = pack8(dpt, half);
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        dv[dt] = mfma(at.tr(Gc, cc, dt), pb, dv[dt]);
-        dk[dt] = mfma(at.tr(Qc, cc, dt), db, dk[dt]);
+        for (int dt = 0; dt < 4; ++dt) {
+          dv[dt] = mfma(at.tr(Gc, cc, dt), pb, dv[dt]);
+          dk[dt] = mfma(at.tr(Qc, cc, dt), db, dk[dt]);
+        }
       }
     }
   };
+  using F = std::false_type;
+  using T = std::true_type;
+  const int nfull = N / KV2_QT;
   int it = 0;
-  for (; it + 2 < ntile; it += 3) {
-    iter(std::integral_constant<int, 0>(), it);
-    iter(std::integral_constant<int, 1>(), it + 1);
-    iter(std::integral_constant<int, 2>(), it + 2);
+  for (; it + 2 < nfull; it += 3) {
+    iter(std::integral_constant<int, 0>(), F(), it);
+    iter(std::integral_constant<int, 1>(), F(), it + 1);
+    iter(std::integral_constant<int, 2>(), F(), it + 2);
   }
-  if (it < ntile) iter(std::integral_constant<int, 0>(), it);
-  if (it + 1 < ntile) iter(std::integral_constant<int, 1>(), it + 1);
+  if (it < nfull) iter(std::integral_constant<int, 0>(), F(), it);
+  if (it + 1 < nfull) iter(std::integral_constant<int, 1>(), F(), it + 1);
+  if (nfull < ntile) {  // ragged last tile (no further loads)
+    switch (nfull % 3) {
+      case 0: iter(std::integral_constant<int, 0>(), T(), nfull); break;
+      case 1: iter(std::integral_constant<int, 1>(), T(), nfull); break;
+      default: iter(std::integral_constant<int, 2>(), T(), nfull); break;
+    }
+  }
   // no direct load may still be landing when the workgroup's LDS is released
   __builtin_amdgcn_s_waitcnt(0);
   if (key >= N) return;
@@ -785,51 +798,60 @@ __global__ __launch_bounds__(256) void attn_bwd_q2_k(AttnBwd a) {
   load_tile(K0, V0, 0);
   load_tile(K1, V1, Q2_KT);
 
-  auto iter = [&](auto ic, int it) {
+  auto iter = [&](auto ic, auto mc, int it) {
     constexpr int c = decltype(ic)::value;
+    constexpr bool MASK = decltype(mc)::value;
     char* Kc = c == 0 ? K0 : (c == 1 ? K1 : K2);
     char* Vc = c == 0 ? V0 : (c == 1 ? V1 : V2);
     const int k0 = it * Q2_KT;
     attn_barrier<8>();
-    if constexpr (c == 0) load_tile(K2, V2, k0 + 2 * Q2_KT);
-    else if constexpr (c == 1) load_tile(K0, V0, k0 + 2 * Q2_KT);
-    else load_tile(K1, V1, k0 + 2 * Q2_KT);
-    f32x16 s[2], dp[2];
+    if constexpr (!MASK) {
+      if constexpr (c == 0) load_tile(K2, V2, k0 + 2 * Q2_KT);
+      else if constexpr (c == 1) load_tile(K0, V0, k0 + 2 * Q2_KT);
+      else load_tile(K1, V1, k0 + 2 * Q2_KT);
+    }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      s[t] = zero16();
-      dp[t] = zero16();
+      f32x16 st = mfma(at.row(Kc, t, 0), qf[0], zero16());
+      f32x16 dpt = mfma(at.row(Vc, t, 0), gf[0], zero16());
 #pragma unroll
-      for (int kb = 0; kb < 8; ++kb) {
-        s[t] = mfma(at.row(Kc, t, kb), qf[kb], s[t]);
-        dp[t] = mfma(at.row(Vc, t, kb), gf[kb], dp[t]);
+      for (int kb = 1; kb < 8; ++kb) {
+        st = mfma(at.row(Kc, t, kb), qf[kb], st);
+        dpt = mfma(at.row(Vc, t, kb), gf[kb], dpt);
       }
-    }
-    // lane: query column, key rows 32t + 8(e/4) + 4h + e%4
-    const bool full = k0 + Q2_KT <= N;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
+      // lane: query column, key rows 32t + 8(e/4) + 4h + e%4
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        float p = __builtin_amdgcn_exp2f(s[t][e] * scl - L);
-        if (!full && k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3) >= N) p = 0.f;
-        dp[t][e] = p * (dp[t][e] - Dl);
+        float p = __builtin_amdgcn_exp2f(fmaf(st[e], scl, -L));
+        if (MASK && k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3) >= N) p = 0.f;
+        dpt[e] = p * (dpt[e] - Dl);
       }
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc) {
-      const bf16x8 db = pack8(dp[cc >> 1], cc & 1);
+      for (int half = 0; half < 2; ++half) {
+        const bf16x8 db = pack8(dpt, half);
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(at.tr(Kc, cc, dt), db, dq[dt]);
+        for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(at.tr(Kc, 2 * t + half, dt), db, dq[dt]);
+      }
     }
   };
+  using F = std::false_type;
+  using T = std::true_type;
+  const int nfull = N / Q2_KT;
   int it = 0;
-  for (; it + 2 < ntile; it += 3) {
-    iter(std::integral_constant<int, 0>(), it);
-    iter(std::integral_constant<int, 1>(), it + 1);
-    iter(std::integral_constant<int, 2>(), it + 2);
+  for (; it + 2 < nfull; it += 3) {
+    iter(std::integral_constant<int, 0>(), F(), it);
+    iter(std::integral_constant<int, 1>(), F(), it + 1);
+    iter(std::integral_constant<int, 2>(), F(), it + 2);
   }
-  if (it < ntile) iter(std::integral_constant<int, 0>(), it);
-  if (it + 1 < ntile) iter(std::integral_constant<int, 1>(), it + 1);
+  if (it < nfull) iter(std::integral_constant<int, 0>(), F(), it);
+  if (it + 1 < nfull) iter(std::integral_constant<int, 1>(), F(), it + 1);
+  if (nfull < ntile) {
+    switch (nfull % 3) {
+      case 0: iter(std::integral_constant<int, 0>(), T(), nfull); break;
+      case 1: iter(std::integral_constant<int, 1>(), T(), nfull); break;
+      default: iter(std::integral_constant<int, 2>(), T(), nfull); break;
+    }
+  }
   __builtin_amdgcn_s_waitcnt(0);
   if (!qv) return;
 #pragma unroll
