@@ -142,6 +142,9 @@ __global__ __launch_bounds__(256) void small_linear_bwd_k(const float* __restric
   float x[SL_MAXB], acc[SL_MAXB];
   for (int b = 0; b < B; ++b) { x[b] = in[(size_t)b * Din + d]; acc[b] = 0.f; }
   const int jn = min(SL_JT, Dout - j0);
+  // rows are independent apart from the input-gradient sums: unrolled so that
+  // the loads of several rows are in flight together
+#pragma unroll 8
   for (int jj = 0; jj < jn; ++jj) {
     const size_t idx = (size_t)(j0 + jj) * Din + d;
     const float w = ldf(W, idx);
@@ -157,12 +160,22 @@ __global__ __launch_bounds__(256) void small_linear_bwd_k(const float* __restric
     for (int b = 0; b < B; ++b) part[((size_t)jt * B + b) * Din + d] = acc[b];
 }
 
-__global__ void sum_parts_k(const float* __restrict__ part, int nparts, size_t n, float* __restrict__ out) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  float s = 0.f;
-  for (int p = 0; p < nparts; ++p) s += part[(size_t)p * n + i];
-  out[i] = s;
+// out[i] = sum over p of part[p * n + i], parts added in a fixed order: 64
+// consecutive outputs per block, 4 slices of the parts per output (slice q
+// sums parts q, q+4, ...), slices combined in order in LDS.
+__global__ __launch_bounds__(256) void sum_parts_k(const float* __restrict__ part, int nparts, size_t n,
+                                                   float* __restrict__ out) {
+  __shared__ float sl[4][64];
+  const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const size_t i = (size_t)blockIdx.x * 64 + c;
+  float acc = 0.f;
+  if (i < n) {
+#pragma unroll 8
+    for (int p = q; p < nparts; p += 4) acc += part[(size_t)p * n + i];
+  }
+  sl[q][c] = acc;
+  __syncthreads();
+  if (q == 0 && i < n) out[i] = ((sl[0][c] + sl[1][c]) + sl[2][c]) + sl[3][c];
 }
 
 // Small batches: 8 consecutive input columns per thread (16-byte loads and
@@ -202,6 +215,9 @@ __global__ __launch_bounds__(128) void small_linear_bwd_vec_k(const float* __res
     }
   }
   const int jn = min(SL_JT, Dout - j0);
+  // rows are independent apart from the input-gradient sums: unrolled so that
+  // the loads of several rows are in flight together
+#pragma unroll 8
   for (int jj = 0; jj < jn; ++jj) {
     const size_t idx = (size_t)(j0 + jj) * Din + d;
     float w[8], gw[8];
@@ -250,7 +266,7 @@ int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din
     LAUNCH_OK("small_linear_bwd_vec");
     if (din) {
       const size_t n = (size_t)B * Din;
-      hipLaunchKernelGGL(sum_parts_k, dim3((n + 255) / 256), dim3(256), 0, s, part, njt, n, din);
+      hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njt, n, din);
       LAUNCH_OK("small_linear_bwd_sum");
     }
     return 0;
@@ -268,7 +284,7 @@ int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din
   LAUNCH_OK("small_linear_bwd");
   if (din) {
     const size_t n = (size_t)B * Din;
-    hipLaunchKernelGGL(sum_parts_k, dim3((n + 255) / 256), dim3(256), 0, s, part, njt, n, din);
+    hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njt, n, din);
     LAUNCH_OK("small_linear_bwd_sum");
   }
   return 0;
