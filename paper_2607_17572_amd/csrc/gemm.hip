@@ -637,56 +637,69 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
 }
 
 // --------------------------------------------- direct-to-LDS MFMA GEMM
-// 256x256 workgroup tile, 4 waves (128x128 each), 32-deep k tiles through 4
-// LDS stages, for K a multiple of 32.  Operands go from memory straight into
-// LDS (buffer loads with the LDS bit: no register staging and no LDS write
-// instructions), three k tiles ahead of the MFMAs.  LDS rows are unpadded and
-// 16-byte chunks are XOR-swizzled by row so that both the 1 KB contiguous
-// direct loads and the fragment reads are free of bank conflicts:
-//   k-contiguous operand, tile [row][32 k] (64 B rows):
+// BM x BN workgroup tile (each 192 or 256), 4 waves (2 x 2), 32-deep k tiles
+// through 4 LDS stages, for K a multiple of 32.  Operands go from memory
+// straight into LDS (buffer loads with the LDS bit: no register staging and no
+// LDS write instructions), three k tiles ahead of the MFMAs.  LDS rows are
+// unpadded and 16-byte chunks are XOR-swizzled by row so that both the 1 KB
+// contiguous direct loads and the fragment reads are free of bank conflicts:
+//   k-contiguous operand, tile [rows][32 k] (64 B rows):
 //     chunk' = chunk ^ (((row >> 1) ^ (row >> 3)) & 3),
 //     fragments are single 16-byte reads;
-//   k-strided operand, tile [32 k][256 rows] (512 B rows):
-//     chunk' = chunk ^ (((k & 3) << 1) | ((k & 1) << 3)),
+//   k-strided operand, tile [32 k][rows] (2 * rows bytes per k row):
+//     chunk' = chunk ^ (((k & 3) << 1) | ((k & 1) << 3))  (256 rows),
+//     chunk' = chunk ^ ((k & 3) << 1)                      (192 rows: the XOR
+//     must stay inside aligned groups of 8 chunks),
 //     fragments are two transposing 8-byte reads (ds_read_b64_tr_b16), each
 //     of which hands lane i of a 16-lane group element (row e, column i) of
 //     the 4 x 16 block the group fetched.
-// Ragged M / N edges rely on the buffer range check like the kernels above.
+// The 192-wide tiles exist for the wave count: 256 CUs take 256x256 tiles of
+// the block's products in 1.5 to 2.25 rounds, 256x192 or 192x192 tiles in
+// whole rounds.  Ragged M / N edges rely on the buffer range check like the
+// kernels above.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 #define JG_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 // Workgroup barrier for the direct-loaded stages: this wave's LDS reads done
-// (lgkmcnt 0) and at most 16 direct loads still in flight (vmcnt 16: the
-// loads of the two newest k tiles), then s_barrier.  Unlike __syncthreads
-// there is no release fence, which would wait for every direct load (they
-// are LDS writes) and drain the prefetch; the empty asm statements keep the
-// compiler from moving memory accesses across it.
-__device__ __forceinline__ void lds_barrier_vm16() {
+// (lgkmcnt 0) and at most NV direct loads still in flight (the loads of the
+// two newest k tiles), then s_barrier.  Unlike __syncthreads there is no
+// release fence, which would wait for every direct load (they are LDS writes)
+// and drain the prefetch; the empty asm statements keep the compiler from
+// moving memory accesses across it.
+template <int NV>
+__device__ __forceinline__ void lds_barrier_vm() {
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt((16 & 15) | ((16 >> 4) << 14) | 0x70);  // vmcnt(16) expcnt(7) lgkmcnt(0)
+  __builtin_amdgcn_s_waitcnt((NV & 15) | ((NV >> 4) << 14) | 0x70);  // vmcnt(NV) expcnt(7) lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
 
 __device__ __forceinline__ int swz_n(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
-__device__ __forceinline__ int swz_t(int k) { return ((k & 3) << 1) | ((k & 1) << 3); }
+template <int ROWS>
+__device__ __forceinline__ int swz_t(int k) {
+  return ROWS == 256 ? (((k & 3) << 1) | ((k & 1) << 3)) : ((k & 3) << 1);
+}
 
-// One operand of the direct-to-LDS kernel: 16 KB per k tile, 4 direct loads
-// of 1 KB per wave.
-template <bool T>
+// One operand of the direct-to-LDS kernel: ROWS x 32 elements = ROWS * 64 B per
+// k tile, NL = ROWS / 64 direct loads of 1 KB per wave.
+template <bool T, int ROWS>
 struct DtlOp {
-  int voff[4];   // per load: byte offset at k = 0
+  static constexpr int NL = ROWS / 64;
+  static constexpr int RB = ROWS * 2;   // bytes per k row (k-strided layout)
+  static constexpr int CPR = ROWS / 8;  // chunks per k row
+  static constexpr int FR = ROWS / 64;  // 32-row fragments per wave (2 waves share the rows)
+  int voff[NL];  // per load: byte offset at k = 0
   int kmul;      // bytes per unit of k
-  int fo[4];     // fragment read offsets (bytes) per 32-row fragment
+  int fo[FR > 2 ? FR : 2];  // fragment read offsets (bytes)
   __device__ inline void init(int ld, int row0, int wrow0) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int b = wave * 4 + t;  // 1 KB block of the tile
+    for (int t = 0; t < NL; ++t) {
+      const int b = wave * NL + t;  // 1 KB block of the tile
       if (!T) {
         const int row = 16 * b + lane / 4, q = (lane % 4) ^ swz_n(row);
         voff[t] = ((row0 + row) * ld + 8 * q) * 2;
       } else {
-        const int kr = 2 * b + lane / 32, c = (lane % 32) ^ swz_t(kr);
+        const int G = 64 * b + lane, kr = G / CPR, c = (G % CPR) ^ swz_t<ROWS>(kr);
         voff[t] = (kr * ld + row0 + 8 * c) * 2;
       }
     }
@@ -695,14 +708,13 @@ struct DtlOp {
       const int r = lane & 31;  // fragment row within a 32-row fragment
       fo[0] = (wrow0 + r) * 64 + (((lane >> 5)) ^ swz_n(r)) * 16;        // k16 step 0
       fo[1] = (wrow0 + r) * 64 + (((lane >> 5) + 2) ^ swz_n(r)) * 16;    // k16 step 1
-      fo[2] = fo[3] = 0;
     } else {
       const int g = (lane >> 4) & 3, i16 = lane & 15;
       const int kr = 8 * (g >> 1) + (i16 >> 2);  // row within the k16 step (first read)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < FR; ++i) {
         const int m = wrow0 + 32 * i + 16 * (g & 1) + 4 * (i16 & 3);
-        fo[i] = kr * 512 + (((m >> 3) ^ swz_t(kr)) << 4) + ((m >> 2) & 1) * 8;
+        fo[i] = kr * RB + (((m >> 3) ^ swz_t<ROWS>(kr)) << 4) + ((m >> 2) & 1) * 8;
       }
     }
   }
@@ -710,8 +722,8 @@ struct DtlOp {
   __device__ inline void load(__amdgpu_buffer_rsrc_t R, char* S, int k0) const {
     const int wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, JG_LDS(S + (wave * 4 + t) * 1024), 16, voff[t] + k0 * kmul, 0, 0, 0);
+    for (int t = 0; t < NL; ++t)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, JG_LDS(S + (wave * NL + t) * 1024), 16, voff[t] + k0 * kmul, 0, 0, 0);
   }
   // fragment i (32 rows) of k16 step kk from the stage at S
   __device__ inline bf16x8 frag(const char* S, int i, int kk) const {
@@ -719,9 +731,9 @@ struct DtlOp {
       return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + fo[kk] + i * 32 * 64));
     } else {
       const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) s16x4*)(S + fo[i] + kk * 16 * 512));
+          (__attribute__((address_space(3))) s16x4*)(S + fo[i] + kk * 16 * RB));
       const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) s16x4*)(S + fo[i] + kk * 16 * 512 + 4 * 512));
+          (__attribute__((address_space(3))) s16x4*)(S + fo[i] + kk * 16 * RB + 4 * RB));
       typedef short s16x8 __attribute__((ext_vector_type(8)));
       const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       return __builtin_bit_cast(bf16x8, v);
@@ -729,10 +741,11 @@ struct DtlOp {
   }
 };
 
-template <bool TA, bool TB, int EK>
+template <bool TA, bool TB, int EK, int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
-  constexpr int BM = 256, BN = 256, BK = 32, WM = 2, WN = 2, FM = 4, FN = 4;
-  constexpr int STG = 32768;  // bytes per stage: A 16 KB, B 16 KB
+  constexpr int BK = 32, WM = 2, WN = 2, FM = BM / 64, FN = BN / 64;
+  constexpr int SB = BM * 64;  // byte offset of the B tile in a stage
+  constexpr int STG = 32768;   // bytes per stage (room for 256 + 256 rows)
   // one variable per stage: every LDS access names its stage statically, so
   // the compiler can tell the fragment reads of one stage from the direct
   // loads still landing in another and does not wait for the latter
@@ -748,10 +761,10 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
   const int wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
-  DtlOp<TA> oa;
-  DtlOp<TB> ob;
-  oa.init(g.lda, m0, wm * 128);
-  ob.init(g.ldb, n0, wn * 128);
+  DtlOp<TA, BM> oa;
+  DtlOp<TB, BN> ob;
+  oa.init(g.lda, m0, wm * (BM / 2));
+  ob.init(g.ldb, n0, wn * (BN / 2));
   const long ext_a = TA ? ((long)(g.K - 1) * g.lda + g.M) * 2 : ((long)(g.M - 1) * g.lda + g.K) * 2;
   const long ext_b = TB ? ((long)(g.K - 1) * g.ldb + g.N) * 2 : ((long)(g.N - 1) * g.ldb + g.K) * 2;
   const __amdgpu_buffer_rsrc_t RA = make_rsrc(g.A, ext_a), RB = make_rsrc(g.B, ext_b);
@@ -776,7 +789,7 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) fa[buf][i] = oa.frag(S, i, kk);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) fb[buf][j] = ob.frag(S + 16384, j, kk);
+    for (int j = 0; j < FN; ++j) fb[buf][j] = ob.frag(S + SB, j, kk);
   };
   auto mfma_step = [&](int buf) {
 #pragma unroll
@@ -787,15 +800,16 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
   };
   auto load_tile = [&](char* S, int t) {
     oa.load(RA, S, t * BK);
-    ob.load(RB, S + 16384, t * BK);
+    ob.load(RB, S + SB, t * BK);
   };
 
   // prologue: tiles 0, 1, 2 in flight; wait for tile 0
+  constexpr int NL = DtlOp<TA, BM>::NL + DtlOp<TB, BN>::NL;  // direct loads per wave per k tile
   const int nk = g.K / BK;
   load_tile(st0, 0);
   load_tile(st1, 1);
   load_tile(st2, 2);
-  lds_barrier_vm16();  // tiles 1 and 2 may still fly
+  lds_barrier_vm<2 * NL>();  // tiles 1 and 2 may still fly
   ldfrag(st0, 0, 0);
 
   constexpr int RD = (TA ? 2 : 1) * FM + (TB ? 2 : 1) * FN;  // LDS reads per k16 step
@@ -809,14 +823,14 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
     ldfrag(S, 1, 1);
     load_tile(stage(std::integral_constant<int, c + 3>()), kt + 3);
     mfma_step(0);
-    pipe_sched<16, RD, 0, 8>();
+    pipe_sched<FM * FN, RD, 0, NL>();
     __builtin_amdgcn_sched_barrier(0);
-    // tile kt+1 has landed once at most the 16 loads of tiles kt+2, kt+3 fly
-    lds_barrier_vm16();
+    // tile kt+1 has landed once at most the loads of tiles kt+2, kt+3 fly
+    lds_barrier_vm<2 * NL>();
     // step 1, hiding the first fragment reads of tile kt+1
     ldfrag(Sn, 0, 0);
     mfma_step(1);
-    pipe_sched<16, RD, 0, 0>();
+    pipe_sched<FM * FN, RD, 0, 0>();
     __builtin_amdgcn_sched_barrier(0);
   };
   int kt = 0;
@@ -906,13 +920,48 @@ static int launch_mfma(const GemmArgs& g, hipStream_t s) {
 static int g_tile_cfg = 0;
 void gemm_set_tile_cfg(int c) { g_tile_cfg = c; }
 
-template <bool TA, bool TB, int EK>
+template <bool TA, bool TB, int EK, int BM, int BN>
 static int launch_dtl(const GemmArgs& g, hipStream_t s) {
-  const int tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  hipLaunchKernelGGL((gemm_dtl_kernel<TA, TB, EK>), dim3(tiles), dim3(256), 0, s, g);
+  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_dtl_kernel<TA, TB, EK, BM, BN>), dim3(tiles), dim3(256), 0, s, g);
   JG_CHECK_LAUNCH("gemm_dtl");
   return 0;
 }
+
+// Tile shape of the direct-to-LDS kernel: the one with the least estimated
+// time = whole rounds of 256 workgroups x tile area / relative tile efficiency
+// (smaller tiles re-read more operand bytes per MFMA).  0: 256x256,
+// 1: 256x192, 2: 192x256, 3: 192x192.
+static int dtl_shape(int M, int N) {
+  static const int bm[4] = {256, 256, 192, 192}, bn[4] = {256, 192, 256, 192};
+  static const double eff[4] = {1.0, 0.95, 0.95, 0.9};
+  int best = 0;
+  double bt = 1e300;
+  for (int i = 0; i < 4; ++i) {
+    const long tiles = (long)((M + bm[i] - 1) / bm[i]) * ((N + bn[i] - 1) / bn[i]);
+    const double t = (double)((tiles + 255) / 256) * bm[i] * bn[i] / eff[i];
+    if (t < bt * 0.999) { bt = t; best = i; }
+  }
+  return best;
+}
+
+// The direct-to-LDS kernel serves the products with a k-strided B operand
+// (input and weight gradients); -1 for the others.
+template <bool TA, bool TB, int EK>
+struct DtlLaunch {
+  static int run(const GemmArgs& g, hipStream_t s, int shape) {
+    switch (shape) {
+      case 1: return launch_dtl<TA, TB, EK, 256, 192>(g, s);
+      case 2: return launch_dtl<TA, TB, EK, 192, 256>(g, s);
+      case 3: return launch_dtl<TA, TB, EK, 192, 192>(g, s);
+      default: return launch_dtl<TA, TB, EK, 256, 256>(g, s);
+    }
+  }
+};
+template <bool TA, int EK>
+struct DtlLaunch<TA, false, EK> {
+  static int run(const GemmArgs&, hipStream_t, int) { return -1; }
+};
 
 // The direct-to-LDS kernel computes 32-bit byte offsets up to three k tiles
 // past K; they must stay below 2^31.
@@ -925,7 +974,10 @@ static bool dtl_fits(const GemmArgs& g) {
 
 template <bool TA, bool TB, int EK>
 static int launch_cfg(const GemmArgs& g, hipStream_t s, int cfg) {
-  if (cfg == 8 && dtl_fits(g)) return launch_dtl<TA, TB, EK>(g, s);
+  if (TB && cfg >= 8 && cfg <= 12 && dtl_fits(g)) {
+    const int rc = DtlLaunch<TA, TB, EK>::run(g, s, cfg == 8 ? dtl_shape(g.M, g.N) : cfg - 9);
+    if (rc >= 0) return rc;
+  }
   // K not a multiple of the 64-deep k tile: the edge-checked kernel
   if (g.K % 64 != 0) return launch_mfma<128, 128, 64, 2, 2, TA, TB, EK, false>(g, s);
   switch (cfg) {
@@ -1000,16 +1052,18 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   const double eb = 2.0 * (g.tb ? (double)g.K * g.ldb : (double)g.N * g.ldb);
   if (ea >= 2147483000.0 || eb >= 2147483000.0) mfma = false;
   if (mfma && ek >= 0) {
-    // default tiles: 256x256; products with a k-strided operand (weight and
-    // input gradients) take the direct-to-LDS kernel, the forward product the
-    // 8-wave register-staged one; 128x128 only for grids too small to cover a
-    // quarter of the chip with 256x256
+    // default: products with a k-strided B operand (weight and input
+    // gradients) take the direct-to-LDS kernel with the tile shape that best
+    // fills whole rounds of 256 CUs; the forward product takes the 8-wave
+    // register-staged 256x256 kernel, or 128x128 for grids too small to
+    // cover a quarter of the chip
     int cfg = g_tile_cfg;
     if (cfg == 0) {
       const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-      if (t256 < 64) cfg = 1;
+      if (g.tb && dtl_fits(g)) cfg = 8;
+      else if (t256 < 64) cfg = 1;
       else if (!g.ta && !g.tb) cfg = 6;
-      else cfg = dtl_fits(g) ? 8 : 4;
+      else cfg = 4;
     }
     if (!g.ta && !g.tb) return launch_kind<false, false>(g, s, cfg, ek);
     if (!g.ta && g.tb) return launch_kind<false, true>(g, s, cfg, ek);
@@ -1025,4 +1079,21 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   return 0;
 }
 
+// Explicit instantiations of the direct-to-LDS kernels the dispatch can reach
+// (the host-side launch stubs of kernel templates reached only through the
+// shape switch are otherwise not always emitted).
+#define JG_DTL_SHAPES(TA, EK)                                            \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 256>(GemmArgs); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 192>(GemmArgs); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 256>(GemmArgs); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 192>(GemmArgs);
+#define JG_DTL_KINDS(TA) \
+  JG_DTL_SHAPES(TA, 0) JG_DTL_SHAPES(TA, 1) JG_DTL_SHAPES(TA, 2) JG_DTL_SHAPES(TA, 3) JG_DTL_SHAPES(TA, 4) \
+  JG_DTL_SHAPES(TA, 5) JG_DTL_SHAPES(TA, 6)
+JG_DTL_KINDS(false)
+JG_DTL_KINDS(true)
+#undef JG_DTL_KINDS
+#undef JG_DTL_SHAPES
+
 }  // namespace jg
+
