@@ -444,66 +444,73 @@ __global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA
   }
 }
 
-// One wave per row (rows of the chunk dealt round-robin to the 4 waves), each
-// lane owning NV runs of 8 consecutive columns (16-byte loads); the per-column
-// partial sums of the 4 waves are combined through LDS in wave order.
+// One wave per row (rows of the chunk dealt round-robin to the LN_W waves),
+// each lane owning NV runs of 8 consecutive columns (16-byte loads).  The row
+// is read once into registers and the next row of the wave is fetched while
+// the current one is finished (one block per CU: 256 KB of registers per wave
+// slot are free for that); the per-column partial sums of the waves are
+// combined through LDS in wave order.
+constexpr int LN_W = 4;
 template <typename T, int NV>
-__global__ __launch_bounds__(256) void ln_mod_bwd_vec_k(const float* __restrict__ dA, const T* __restrict__ x,
-                                                        Chunks ch, int c0, const float* __restrict__ mean,
-                                                        const float* __restrict__ rstd, const float* __restrict__ mt,
-                                                        const float* __restrict__ mi, int mod_w, int sc_off,
-                                                        float* __restrict__ g, float* __restrict__ psc,
-                                                        float* __restrict__ psh) {
+__global__ __launch_bounds__(64 * LN_W) __attribute__((amdgpu_waves_per_eu(1, 1))) void ln_mod_bwd_vec_k(
+    const float* __restrict__ dA, const T* __restrict__ x, Chunks ch, int c0, const float* __restrict__ mean,
+    const float* __restrict__ rstd, const float* __restrict__ mt, const float* __restrict__ mi, int mod_w,
+    int sc_off, float* __restrict__ g, float* __restrict__ psc, float* __restrict__ psh) {
   constexpr int D = NV * 512;
-  extern __shared__ float red[];  // [4][D] reduction space, then [D] of (1 + scale)
-  float* m = red + 4 * D;
+  extern __shared__ float red[];  // [LN_W][D] reduction space
   const int q = c0 + blockIdx.x;
   int r0, n, b;
   chunk_rows(ch, q, r0, n, b);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const float* mg = ((r0 < ch.B * ch.nt) ? mt : mi) + (size_t)b * mod_w + sc_off;
-  for (int c = threadIdx.x; c < D; c += 256) m[c] = 1.f + mg[c];
-  __syncthreads();
+  float m[NV * 8];  // 1 + scale of this lane's columns
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    ld8f(mg + 8 * lane + 512 * i, m + 8 * i);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) m[8 * i + e] += 1.f;
+  }
   float asc[NV * 8], ash[NV * 8];
 #pragma unroll
   for (int i = 0; i < NV * 8; ++i) asc[i] = ash[i] = 0.f;
-  for (int rr = w; rr < n; rr += 4) {
-    const int r = r0 + rr;
-    const float mu = mean[r], rs = rstd[r];
-    // pass 1: row sums and the column partials; pass 2 re-reads the (cached)
-    // row and updates g, so no per-row arrays stay live
-    float s1 = 0.f, s2 = 0.f;
+  float xv[NV * 8], da[NV * 8], xn[NV * 8], dn[NV * 8];
+  auto load_row = [&](int r, float* xo, float* dout) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int c = 8 * lane + 512 * i;
-      float xv[8], da[8];
-      ld8f(x + (size_t)r * D + c, xv);
-      ld8f(dA + (size_t)r * D + c, da);
+      ld8f(x + (size_t)r * D + 8 * lane + 512 * i, xo + 8 * i);
+      ld8f(dA + (size_t)r * D + 8 * lane + 512 * i, dout + 8 * i);
+    }
+  };
+  if (w < n) load_row(r0 + w, xv, da);
+  for (int rr = w; rr < n; rr += LN_W) {
+    const int r = r0 + rr;
+    if (rr + LN_W < n) load_row(r + LN_W, xn, dn);  // next row in flight
+    const float mu = mean[r], rs = rstd[r];
+    float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float xhat = (xv[e] - mu) * rs;
-        const float d = da[e] * m[c + e];
-        asc[8 * i + e] = fmaf(da[e], xhat, asc[8 * i + e]);
-        ash[8 * i + e] += da[e];
-        s1 += d;
-        s2 += d * xhat;
-      }
+    for (int i = 0; i < NV * 8; ++i) {
+      const float xhat = (xv[i] - mu) * rs;
+      const float d = da[i] * m[i];
+      asc[i] = fmaf(da[i], xhat, asc[i]);
+      ash[i] += da[i];
+      s1 += d;
+      s2 += d * xhat;
     }
     const float m1 = wave_sum(s1) / D, m2 = wave_sum(s2) / D;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int c = 8 * lane + 512 * i;
-      float xv[8], da[8], gv[8];
-      ld8f(x + (size_t)r * D + c, xv);
-      ld8f(dA + (size_t)r * D + c, da);
+      float gv[8];
       ld8f(g + (size_t)r * D + c, gv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float xhat = (xv[e] - mu) * rs;
-        gv[e] += rs * (da[e] * m[c + e] - m1 - xhat * m2);
+        const float xhat = (xv[8 * i + e] - mu) * rs;
+        gv[e] += rs * (da[8 * i + e] * m[8 * i + e] - m1 - xhat * m2);
       }
       st8f(g + (size_t)r * D + c, gv);
     }
+#pragma unroll
+    for (int i = 0; i < NV * 8; ++i) { xv[i] = xn[i]; da[i] = dn[i]; }
   }
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
@@ -512,7 +519,12 @@ __global__ __launch_bounds__(256) void ln_mod_bwd_vec_k(const float* __restrict_
     for (int i = 0; i < NV; ++i) st8f(red + w * D + 8 * lane + 512 * i, a + 8 * i);
     __syncthreads();
     float* out = (pass == 0 ? psc : psh) + (size_t)q * D;
-    for (int c = threadIdx.x; c < D; c += 256) out[c] = red[c] + red[D + c] + red[2 * D + c] + red[3 * D + c];
+    for (int c = threadIdx.x; c < D; c += 64 * LN_W) {
+      float t = red[c];
+#pragma unroll
+      for (int k = 1; k < LN_W; ++k) t += red[k * D + c];
+      out[c] = t;
+    }
     __syncthreads();
   }
 }
@@ -525,21 +537,21 @@ int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   if (nc == 0) return 0;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
-  if (D % 512 == 0 && D <= 4096 && al16(dA) && al16(x) && al16(g)) {
-    const size_t lds = 5 * (size_t)D * sizeof(float);
+  if (D % 512 == 0 && D <= 3584 && al16(dA) && al16(x) && al16(g)) {
+    const size_t lds = LN_W * (size_t)D * sizeof(float);
 #define LNB(T, NV)                                                                                             \
   case NV: {                                                                                                   \
     auto k = ln_mod_bwd_vec_k<T, NV>;                                                                          \
     if (lds > 65536) hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds); \
-    hipLaunchKernelGGL(k, dim3(nc), dim3(256), lds, s, dA, (const T*)x, ch, c0, mean, rstd, mod_txt, mod_img, \
+    hipLaunchKernelGGL(k, dim3(nc), dim3(64 * LN_W), lds, s, dA, (const T*)x, ch, c0, mean, rstd, mod_txt, mod_img, \
                        mod_w, sc_off, g, part_scale, part_shift);                                              \
   } break;
     if (act_dt == BF16) {
       switch (D / 512) { LNB(uint16_t, 1) LNB(uint16_t, 2) LNB(uint16_t, 3) LNB(uint16_t, 4) LNB(uint16_t, 5)
-                         LNB(uint16_t, 6) LNB(uint16_t, 7) LNB(uint16_t, 8) }
+                         LNB(uint16_t, 6) LNB(uint16_t, 7) }
     } else {
       switch (D / 512) { LNB(float, 1) LNB(float, 2) LNB(float, 3) LNB(float, 4) LNB(float, 5) LNB(float, 6)
-                         LNB(float, 7) LNB(float, 8) }
+                         LNB(float, 7) }
     }
 #undef LNB
     LAUNCH_OK("ln_mod_bwd_vec");
@@ -921,29 +933,43 @@ int colsum_partials(const void* X, int dt, int ld, int N, RowMap rm, int row0, i
 
 // Per sample: the sample's chunks inside [c0, c0 + nc) form at most two runs
 // (its text chunks, its image chunks); 32 columns x 8 slices per block.
-__global__ __launch_bounds__(256) void reduce_per_sample_k(const float* __restrict__ part, int N, Chunks ch, int c0,
-                                                           int nc, float* __restrict__ out, int out_stride,
-                                                           int out_off) {
-  __shared__ float sh[8][33];
+// Column sums of chunk partials are latency-bound (few columns, many chunks):
+// a block takes 64 consecutive columns (one 256-byte row segment per wave
+// load) and 16 chunk slices (slice k sums chunks k, k+16, ...; loads unrolled
+// so several are in flight), and adds the 16 slice sums in slice order
+// (deterministic).
+constexpr int RC_COLS = 64, RC_SL = 16;
+
+__device__ inline float slice_total(float acc, float (*sh)[RC_COLS + 1]) {
+  const int cl = threadIdx.x % RC_COLS, sl = threadIdx.x / RC_COLS;
+  sh[sl][cl] = acc;
+  __syncthreads();
+  float t = 0.f;
+  if (sl == 0) {
+#pragma unroll
+    for (int k = 0; k < RC_SL; ++k) t += sh[k][cl];
+  }
+  return t;
+}
+
+__global__ __launch_bounds__(1024) void reduce_per_sample_k(const float* __restrict__ part, int N, Chunks ch, int c0,
+                                                            int nc, float* __restrict__ out, int out_stride,
+                                                            int out_off) {
+  __shared__ float sh[RC_SL][RC_COLS + 1];
   const int b = blockIdx.y;
-  const int cl = threadIdx.x & 31, sl = threadIdx.x >> 5;
-  const int c = blockIdx.x * 32 + cl;
+  const int cl = threadIdx.x % RC_COLS, sl = threadIdx.x / RC_COLS;
+  const int c = blockIdx.x * RC_COLS + cl;
   const int ct = ch.ct(), ci = ch.ci();
   const int runs[2][2] = {{b * ct, b * ct + ct}, {ch.B * ct + b * ci, ch.B * ct + b * ci + ci}};
   float acc = 0.f;
   if (c < N)
     for (int r = 0; r < 2; ++r) {
       const int lo = max(runs[r][0], c0), hi = min(runs[r][1], c0 + nc);
-      for (int q = lo + sl; q < hi; q += 8) acc += part[(size_t)q * N + c];
+#pragma unroll 4
+      for (int q = lo + sl; q < hi; q += RC_SL) acc += part[(size_t)q * N + c];
     }
-  sh[sl][cl] = acc;
-  __syncthreads();
-  if (sl == 0 && c < N) {
-    float t = 0.f;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) t += sh[k][cl];
-    out[(size_t)b * out_stride + out_off + c] = t;
-  }
+  const float t = slice_total(acc, sh);
+  if (sl == 0 && c < N) out[(size_t)b * out_stride + out_off + c] = t;
 }
 
 int reduce_per_sample(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
@@ -951,29 +977,27 @@ int reduce_per_sample(const float* part, int N, RowMap rm, int row0, int nrows, 
   int c0, nc;
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
-  hipLaunchKernelGGL(reduce_per_sample_k, dim3((N + 31) / 32, rm.B), dim3(256), 0, s, part, N, ch, c0, nc, out,
-                     out_stride, out_off);
+  hipLaunchKernelGGL(reduce_per_sample_k, dim3((N + RC_COLS - 1) / RC_COLS, rm.B), dim3(RC_COLS * RC_SL), 0, s, part,
+                     N, ch, c0, nc, out, out_stride, out_off);
   LAUNCH_OK("reduce_per_sample");
   return 0;
 }
 
-// 32 columns x 8 chunk slices per block; the 8 slice sums are added in slice
-// order (deterministic), then beta * g is added once.
+// g[c] (+)= sum over chunks [chunk0, chunk0 + nchunk) of part[q * ld + c];
+// beta * g is added once, after the slices.
 template <typename TG>
-__global__ __launch_bounds__(256) void reduce_to_grad_k(const float* __restrict__ part, int ld, int chunk0, int nchunk,
-                                                        int N, TG* __restrict__ g, float beta) {
-  __shared__ float sh[8][33];
-  const int cl = threadIdx.x & 31, sl = threadIdx.x >> 5;
-  const int c = blockIdx.x * 32 + cl;
+__global__ __launch_bounds__(1024) void reduce_to_grad_k(const float* __restrict__ part, int ld, int chunk0,
+                                                         int nchunk, int N, TG* __restrict__ g, float beta) {
+  __shared__ float sh[RC_SL][RC_COLS + 1];
+  const int cl = threadIdx.x % RC_COLS, sl = threadIdx.x / RC_COLS;
+  const int c = blockIdx.x * RC_COLS + cl;
   float acc = 0.f;
-  if (c < N)
-    for (int q = chunk0 + sl; q < chunk0 + nchunk; q += 8) acc += part[(size_t)q * ld + c];
-  sh[sl][cl] = acc;
-  __syncthreads();
+  if (c < N) {
+#pragma unroll 4
+    for (int q = chunk0 + sl; q < chunk0 + nchunk; q += RC_SL) acc += part[(size_t)q * ld + c];
+  }
+  float t = slice_total(acc, sh);
   if (sl == 0 && c < N) {
-    float t = 0.f;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) t += sh[k][cl];
     if (beta != 0.f) t += beta * ldf(g, c);
     stf(g, c, t);
   }
@@ -981,12 +1005,13 @@ __global__ __launch_bounds__(256) void reduce_to_grad_k(const float* __restrict_
 
 int reduce_to_grad(const float* part, int ld, int chunk0, int nchunk, int N, void* g, int g_dt,
                    float beta, hipStream_t s) {
-  dim3 grid((N + 31) / 32);
+  dim3 grid((N + RC_COLS - 1) / RC_COLS);
   if (g_dt == BF16)
-    hipLaunchKernelGGL(reduce_to_grad_k<uint16_t>, grid, dim3(256), 0, s, part, ld, chunk0, nchunk, N, (uint16_t*)g,
-                       beta);
+    hipLaunchKernelGGL(reduce_to_grad_k<uint16_t>, grid, dim3(RC_COLS * RC_SL), 0, s, part, ld, chunk0, nchunk, N,
+                       (uint16_t*)g, beta);
   else
-    hipLaunchKernelGGL(reduce_to_grad_k<float>, grid, dim3(256), 0, s, part, ld, chunk0, nchunk, N, (float*)g, beta);
+    hipLaunchKernelGGL(reduce_to_grad_k<float>, grid, dim3(RC_COLS * RC_SL), 0, s, part, ld, chunk0, nchunk, N,
+                       (float*)g, beta);
   LAUNCH_OK("reduce_to_grad");
   return 0;
 }
