@@ -767,6 +767,25 @@ int qk_norm_rope_fwd(const void* proj, int ld, int act_dt, RowMap rm, Rope rp, G
 
 constexpr int QK_SUB = RED_ROWS / QK_PARTS;  // rows per block of the q/k norm backward
 
+// two consecutive elements (an RoPE pair) as one 4- or 8-byte access
+__device__ inline void ld2f(const uint16_t* p, float& a, float& c) {
+  const uint32_t u = *(const uint32_t*)p;
+  a = bf2f(u & 0xffffu);
+  c = bf2f(u >> 16);
+}
+__device__ inline void ld2f(const float* p, float& a, float& c) {
+  const float2 v = *(const float2*)p;
+  a = v.x;
+  c = v.y;
+}
+__device__ inline void st2f(uint16_t* p, float a, float c) {
+  *(uint32_t*)p = (uint32_t)f2bf(a) | ((uint32_t)f2bf(c) << 16);
+}
+__device__ inline void st2f(float* p, float a, float c) { *(float2*)p = make_float2(a, c); }
+
+// One wave per row (the rows of the sub-chunk dealt to the 4 waves), looping
+// over the heads; lane p owns RoPE pair p, whose rotation depends only on the
+// token and so is computed once per row.
 template <typename T, typename TD>
 __global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__ dQh, const TD* __restrict__ dKh,
                                                           const TD* __restrict__ dVh, const T* __restrict__ proj,
@@ -783,58 +802,52 @@ __global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__
   r0 += sub * QK_SUB;
   n = min(QK_SUB, n - sub * QK_SUB);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int D = rp.H * rp.Dh, N = rm.nt + rm.ni;
-  const bool act = lane < rp.Dh / 2;
+  const int H = rp.H, Dh = rp.Dh, D = H * Dh, N = rm.nt + rm.ni;
+  const bool act = lane < Dh / 2;
   const int p = act ? lane : 0;
   const T* qg = (const T*)gn.q[st];
   const T* kg = (const T*)gn.k[st];
   float gq0 = 0, gq1 = 0, gk0 = 0, gk1 = 0;
   const float qga = act ? ldf(qg, 2 * p) : 0.f, qgb = act ? ldf(qg, 2 * p + 1) : 0.f;
   const float kga = act ? ldf(kg, 2 * p) : 0.f, kgb = act ? ldf(kg, 2 * p + 1) : 0.f;
-  for (int it = wave; it < max(n, 0) * rp.H; it += 4) {
-    const int r = r0 + it / rp.H, h = it % rp.H;
+  const float inv_dh = 1.f / Dh;
+  for (int rr = wave; rr < n; rr += 4) {
+    const int r = r0 + rr;
     int bb, j;
     tok_of_row(rm, r, bb, j);
-    const size_t o = (((size_t)bb * rp.H + h) * N + j) * rp.Dh + 2 * p;
-    const T* pr = proj + (size_t)r * ld;
-    T* dp = dproj + (size_t)r * ld_d;
     float sn = 0.f, cs = 1.f;
     if (act) sincosf(rope_angle(rp, j, p), &sn, &cs);
-    // q
-    float d0 = 0, d1 = 0, x0 = 0, x1 = 0;
-    if (act) {
-      const float a = ldf(dQh, o), c = ldf(dQh, o + 1);
-      d0 = a * cs + c * sn;
-      d1 = -a * sn + c * cs;
-      x0 = ldf(pr, h * rp.Dh + 2 * p);
-      x1 = ldf(pr, h * rp.Dh + 2 * p + 1);
-    }
-    float ri = rq[(size_t)r * rp.H + h];
-    float dot = wave_sum(d0 * qga * x0 + d1 * qgb * x1);
-    if (act) {
-      stf(dp, h * rp.Dh + 2 * p, d0 * qga * ri - x0 * ri * ri * ri * dot / rp.Dh);
-      stf(dp, h * rp.Dh + 2 * p + 1, d1 * qgb * ri - x1 * ri * ri * ri * dot / rp.Dh);
-      gq0 = fmaf(d0, x0 * ri, gq0);
-      gq1 = fmaf(d1, x1 * ri, gq1);
-    }
-    // k
-    if (act) {
-      const float a = ldf(dKh, o), c = ldf(dKh, o + 1);
-      d0 = a * cs + c * sn;
-      d1 = -a * sn + c * cs;
-      x0 = ldf(pr, D + h * rp.Dh + 2 * p);
-      x1 = ldf(pr, D + h * rp.Dh + 2 * p + 1);
-    }
-    ri = rk[(size_t)r * rp.H + h];
-    dot = wave_sum(d0 * kga * x0 + d1 * kgb * x1);
-    if (act) {
-      stf(dp, D + h * rp.Dh + 2 * p, d0 * kga * ri - x0 * ri * ri * ri * dot / rp.Dh);
-      stf(dp, D + h * rp.Dh + 2 * p + 1, d1 * kgb * ri - x1 * ri * ri * ri * dot / rp.Dh);
-      gk0 = fmaf(d0, x0 * ri, gk0);
-      gk1 = fmaf(d1, x1 * ri, gk1);
-      // v
-      stf(dp, 2 * D + h * rp.Dh + 2 * p, ldf(dVh, o));
-      stf(dp, 2 * D + h * rp.Dh + 2 * p + 1, ldf(dVh, o + 1));
+    const T* pr = proj + (size_t)r * ld + 2 * p;
+    T* dp = dproj + (size_t)r * ld_d + 2 * p;
+    const size_t ob = ((size_t)bb * H * N + j) * Dh + 2 * p;  // head h adds h * N * Dh
+#pragma unroll 4
+    for (int h = 0; h < H; ++h) {
+      const size_t o = ob + (size_t)h * N * Dh;
+      float qa = 0, qc = 0, ka = 0, kc = 0, va = 0, vc = 0, x0 = 0, x1 = 0, y0 = 0, y1 = 0;
+      if (act) {
+        ld2f(dQh + o, qa, qc);
+        ld2f(dKh + o, ka, kc);
+        ld2f(dVh + o, va, vc);
+        ld2f(pr + h * Dh, x0, x1);
+        ld2f(pr + D + h * Dh, y0, y1);
+      }
+      const float riq = rq[(size_t)r * H + h], rik = rk[(size_t)r * H + h];
+      // q: undo the rotation, then the RMS norm with gain
+      const float d0 = qa * cs + qc * sn, d1 = -qa * sn + qc * cs;
+      const float dotq = wave_sum(d0 * qga * x0 + d1 * qgb * x1);
+      // k
+      const float e0 = ka * cs + kc * sn, e1 = -ka * sn + kc * cs;
+      const float dotk = wave_sum(e0 * kga * y0 + e1 * kgb * y1);
+      if (act) {
+        const float cq = riq * riq * riq * dotq * inv_dh, ck = rik * rik * rik * dotk * inv_dh;
+        st2f(dp + h * Dh, d0 * qga * riq - x0 * cq, d1 * qgb * riq - x1 * cq);
+        st2f(dp + D + h * Dh, e0 * kga * rik - y0 * ck, e1 * kgb * rik - y1 * ck);
+        st2f(dp + 2 * D + h * Dh, va, vc);
+        gq0 = fmaf(d0, x0 * riq, gq0);
+        gq1 = fmaf(d1, x1 * riq, gq1);
+        gk0 = fmaf(e0, y0 * rik, gk0);
+        gk1 = fmaf(e1, y1 * rik, gk1);
+      }
     }
   }
   red[wave][0][lane] = gq0;
@@ -858,6 +871,13 @@ int qk_norm_rope_bwd(const void* dQh, const void* dKh, const void* dVh, int dt_d
                      int act_dt, RowMap rm, Rope rp, Gains gn, const float* rinv_q,
                      const float* rinv_k, void* dproj, int ld_d, float* part_gain, hipStream_t s) {
   if (rp.Dh > 128 || rp.Dh % 4) { set_error("qk_norm_rope_bwd: head_dim"); return 1; }
+  // RoPE pairs are read and written as one access: even leading dimensions,
+  // 8-byte aligned bases
+  auto al8 = [](const void* p) { return ((uintptr_t)p & 7u) == 0; };
+  if ((ld | ld_d) & 1 || !al8(dQh) || !al8(dKh) || !al8(dVh) || !al8(proj) || !al8(dproj)) {
+    set_error("qk_norm_rope_bwd: operands must be 8-byte aligned with even leading dimensions");
+    return 1;
+  }
   int c0, nc;
   if (chunk_range(rm, 0, rm.rows(), &c0, &nc)) return 1;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
