@@ -616,7 +616,7 @@ __device__ __forceinline__ void attn_barrier() {
 // through three LDS stages.
 constexpr int KV2_KB = 128, KV2_QT = 64;
 
-__global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_kv2_k(AttnBwd a) {
   __shared__ __attribute__((aligned(1024))) char Q0[16384], G0[16384], Q1[16384], G1[16384], Q2[16384], G2[16384];
   __shared__ __attribute__((aligned(256))) float L0[64], D0[64], L1[64], D1[64], L2[64], D2[64];
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
@@ -682,13 +682,23 @@ __global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      f32x16 st = mfma(at.row(Qc, t, 0), kf[0], zero16());
-      f32x16 dpt = mfma(at.row(Gc, t, 0), vf[0], zero16());
+      // all fragments of the half's S and dP first: the reads overlap each
+      // other instead of each MFMA waiting for its own
+      bf16x8 fq[8], fg[8];
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) {
+        fq[kb] = at.row(Qc, t, kb);
+        fg[kb] = at.row(Gc, t, kb);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 st = mfma(fq[0], kf[0], zero16());
+      f32x16 dpt = mfma(fg[0], vf[0], zero16());
 #pragma unroll
       for (int kb = 1; kb < 8; ++kb) {
-        st = mfma(at.row(Qc, t, kb), kf[kb], st);
-        dpt = mfma(at.row(Gc, t, kb), vf[kb], dpt);
+        st = mfma(fq[kb], kf[kb], st);
+        dpt = mfma(fg[kb], vf[kb], dpt);
       }
+      __builtin_amdgcn_sched_barrier(0);
       // lane: key column, query rows 32t + 8(e/4) + 4h + e%4
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -704,15 +714,32 @@ __global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
           dpt[e] = p * (dpt[e] - Dv[i]);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
+      // dV / dK, 16 query rows at a time: the transposed fragments of one
+      // block are read before its MFMAs, the next block's during them
+      bf16x8 tg[2][4], tq[2][4];
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        tg[0][dt] = at.tr(Gc, 2 * t, dt);
+        tq[0][dt] = at.tr(Qc, 2 * t, dt);
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
-        const int cc = 2 * t + half;
         const bf16x8 pb = pack8(st, half), db = pack8(dpt, half);
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
-          dv[dt] = mfma(at.tr(Gc, cc, dt), pb, dv[dt]);
-          dk[dt] = mfma(at.tr(Qc, cc, dt), db, dk[dt]);
+          dv[dt] = mfma(tg[half][dt], pb, dv[dt]);
+          dk[dt] = mfma(tq[half][dt], db, dk[dt]);
         }
+        if (half == 0) {  // issued behind the MFMAs that free the registers
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt) {
+            tg[1][dt] = at.tr(Gc, 2 * t + 1, dt);
+            tq[1][dt] = at.tr(Qc, 2 * t + 1, dt);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   };
@@ -758,7 +785,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv2_k(AttnBwd a) {
 // key tiles of 64 rows of K and V stream through three LDS stages.
 constexpr int Q2_QB = 128, Q2_KT = 64;
 
-__global__ __launch_bounds__(256) void attn_bwd_q2_k(AttnBwd a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_q2_k(AttnBwd a) {
   __shared__ __attribute__((aligned(1024))) char K0[16384], V0[16384], K1[16384], V1[16384], K2[16384], V2[16384];
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
@@ -812,13 +839,21 @@ __global__ __launch_bounds__(256) void attn_bwd_q2_k(AttnBwd a) {
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      f32x16 st = mfma(at.row(Kc, t, 0), qf[0], zero16());
-      f32x16 dpt = mfma(at.row(Vc, t, 0), gf[0], zero16());
+      bf16x8 fk[8], fv[8];
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) {
+        fk[kb] = at.row(Kc, t, kb);
+        fv[kb] = at.row(Vc, t, kb);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 st = mfma(fk[0], qf[0], zero16());
+      f32x16 dpt = mfma(fv[0], gf[0], zero16());
 #pragma unroll
       for (int kb = 1; kb < 8; ++kb) {
-        st = mfma(at.row(Kc, t, kb), qf[kb], st);
-        dpt = mfma(at.row(Vc, t, kb), gf[kb], dpt);
+        st = mfma(fk[kb], qf[kb], st);
+        dpt = mfma(fv[kb], gf[kb], dpt);
       }
+      __builtin_amdgcn_sched_barrier(0);
       // lane: query column, key rows 32t + 8(e/4) + 4h + e%4
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
@@ -826,12 +861,20 @@ __global__ __launch_bounds__(256) void attn_bwd_q2_k(AttnBwd a) {
         if (MASK && k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3) >= N) p = 0.f;
         dpt[e] = p * (dpt[e] - Dl);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8 tk[2][4];
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) tk[half][dt] = at.tr(Kc, 2 * t + half, dt);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         const bf16x8 db = pack8(dpt, half);
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(at.tr(Kc, 2 * t + half, dt), db, dq[dt]);
+        for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(tk[half][dt], db, dq[dt]);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   using F = std::false_type;
