@@ -45,6 +45,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="first run a plain 256 MiB device copy (calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--only", choices=["all", "jagg"], default="all",
                     help="jagg: time the JAGG windows only (for a kernel trace of exactly those launches)")
     args = ap.parse_args()
@@ -57,6 +59,14 @@ def main():
     import synth
 
     pk.lib()  # fails loudly if the HIP library is not built
+    if args.calib_copy:
+        # a copy kernel of known size: reads and writes exactly 256 MiB
+        src = torch.ones(128 << 20, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cfg = pk.config("block")
     D, F, nt, ni = cfg.hidden, cfg.mlp_hidden, cfg.n_txt, cfg.n_img
     N = nt + ni

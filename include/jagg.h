@@ -163,6 +163,25 @@ jagg_status jagg_group_backward(jagg_ctx* ctx, const void* theta, const void* sa
 jagg_status perstep_group_backward(jagg_ctx* ctx, const void* theta, const void* const* saved, int batch,
                                    const void* const* s, int W, void* dtheta, float beta);
 
+/* One product of a linear layer's backward, the kernel the VJP issues for every
+ * projection of a block (backward-cost appendix: the backward of a linear map
+ * is two products, the input gradient and the weight gradient).  Weights are
+ * stored [n_out][n_in]; dY, X, W and pre are bf16 (JAGG_BF16), row-major,
+ * densely packed, device, 16-byte aligned; accumulation is fp32.
+ *   JAGG_DGRAD:      result[rows][n_in]  = dY[rows][n_out] W[n_out][n_in]
+ *                    (result_dtype JAGG_F32 or JAGG_BF16; beta must be 0)
+ *   JAGG_DGRAD_GELU: result[rows][n_in]  = (dY W) * gelu'(pre[rows][n_in])
+ *                    (tanh-GELU derivative; result bf16; beta must be 0)
+ *   JAGG_WGRAD:      result[n_out][n_in] = beta * result + dY^T X[rows][n_in]
+ *                    (result_dtype JAGG_F32 or JAGG_BF16; beta 0 or 1)
+ * `other` is W for the two input-gradient kinds and X for JAGG_WGRAD; `pre`
+ * is read only by JAGG_DGRAD_GELU.  rows, n_out, n_in >= 1.  Enqueued on the
+ * context's stream; needs no workspace.  EINVAL on a null or unaligned
+ * pointer, a bad kind, dtype or beta, or a size out of range. */
+typedef enum { JAGG_DGRAD = 0, JAGG_DGRAD_GELU = 1, JAGG_WGRAD = 2 } jagg_linear_kind;
+jagg_status jagg_linear_grad(jagg_ctx* ctx, int kind, const void* dY, const void* other, const void* pre, int rows,
+                             int n_out, int n_in, void* result, int result_dtype, float beta);
+
 /* Measurement hook (no effect on results).  jagg_prof_begin(cls) arms one
  * kernel class for this process; every later launch of that class, on any
  * context, is bracketed by a pair of HIP events on its stream.

@@ -14,6 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libjagg.so")
 
 F32, BF16 = 0, 1
+DGRAD, DGRAD_GELU, WGRAD = 0, 1, 2
 
 
 class _DitConfig(ctypes.Structure):
@@ -55,6 +56,7 @@ def lib() -> ctypes.CDLL:
             "jagg_route": [ctypes.POINTER(d), i, d, d, ctypes.POINTER(ctypes.c_ubyte), ctypes.POINTER(d)],
             "jagg_group_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, vp, f],
             "perstep_group_backward": [vp, vp, ctypes.POINTER(vp), i, ctypes.POINTER(vp), i, vp, f],
+            "jagg_linear_grad": [vp, i, vp, vp, vp, i, i, i, vp, i, f],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -265,6 +267,17 @@ class Context:
         _check(lib().jagg_group_backward(self._h, theta.data_ptr(), saved_pair.data_ptr(), batch, _ptrs(s_list), tt,
                                          W, dtheta.data_ptr(), float(beta)))
         return dtheta
+
+    def linear_grad(self, kind: int, dY, other, result, beta: float = 0.0, pre=None):
+        """One product of a linear layer's backward (DGRAD, DGRAD_GELU or WGRAD)."""
+        torch = _torch()
+        rows, n_out = dY.shape
+        n_in = other.shape[1]
+        rdt = BF16 if result.dtype == torch.bfloat16 else F32
+        _check(lib().jagg_linear_grad(self._h, kind, dY.data_ptr(), other.data_ptr(),
+                                      None if pre is None else pre.data_ptr(), rows, n_out, n_in, result.data_ptr(),
+                                      rdt, float(beta)))
+        return result
 
     def perstep_group_backward(self, theta, saved_list, batch: int, s_list, dtheta, beta: float = 0.0):
         self.ensure_workspace(batch)

@@ -28,9 +28,15 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found: the JAGG library needs ROCm's hipcc")
 
 
+# per-source flags: the attention kernels keep their MFMA results in VGPRs
+# (the softmax reads them there), which removes the accumulator-register
+# copies the default heuristic emits for them
+EXTRA = {"attention_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [_hipcc(), *FLAGS, "-c", src, "-o", obj]
+    cmd = [_hipcc(), *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")

@@ -17,7 +17,8 @@ struct AttnFwd {
 int attention_fwd(const AttnFwd& a, hipStream_t s);
 
 // dO token-major (ld_do), O token-major (ld_o); dQ/dK/dV head-major (dt_d).
-// `delta` is workspace [B][H][N] fp32.
+// `delta` is workspace 2 x [B][H][N] fp32 (delta, then the log-sum-exp in
+// log2 units for the MFMA kernels).
 struct AttnBwd {
   const void* Q; const void* K; const void* V;
   const void* O; int ld_o;

@@ -300,7 +300,11 @@ __global__ __launch_bounds__(256) void attn_delta_mfma_k(AttnBwd a) {
     s += __shfl_xor(s, 8, 64);
     if ((lane & 15) == 0 && c < D) {
       const int hd = c / DH;
-      a.delta[((size_t)b * a.H + hd) * a.N + j] = s;
+      const size_t i = ((size_t)b * a.H + hd) * a.N + j;
+      a.delta[i] = s;
+      // second half of the delta buffer: the log-sum-exp in log2 units, so
+      // the backward kernels form exp2(s * scale * log2e - lse2) with one fma
+      a.delta[(size_t)a.B * a.H * a.N + i] = a.lse[i] * LOG2E;
     }
   }
 }
@@ -575,7 +579,8 @@ struct ATile {
   // of tile row r in the resource, or a negative value for a padding row
   template <class RowOff>
   __device__ inline void load(__amdgpu_buffer_rsrc_t R, char* S, RowOff rowoff) const {
-    const int wave = threadIdx.x >> 6;
+    // wave-uniform: the LDS destination (M0) is then computed on the scalar unit
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int ro = rowoff(lrow[t]);
@@ -620,7 +625,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   __shared__ __attribute__((aligned(1024))) char Q0[16384], G0[16384], Q1[16384], G1[16384], Q2[16384], G2[16384];
   __shared__ __attribute__((aligned(256))) float L0[64], D0[64], L1[64], D1[64], L2[64], D2[64];
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
   const int key = blockIdx.x * KV2_KB + w * 32 + c32;
   const int N = a.N;
   const size_t base = (size_t)bh * N * DH;
@@ -629,7 +634,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const float sc = rsqrtf((float)DH), scl = sc * LOG2E;
   const __amdgpu_buffer_rsrc_t RQ = arsrc((const uint16_t*)a.Q + base, (long)N * DH * 2);
   const __amdgpu_buffer_rsrc_t RG = arsrc(a.dO, (long)a.rm.rows() * a.ld_do * 2);
-  const __amdgpu_buffer_rsrc_t RL = arsrc(a.lse + (size_t)bh * N, (long)N * 4);
+  const __amdgpu_buffer_rsrc_t RL = arsrc(a.delta + (size_t)a.B * a.H * N + (size_t)bh * N, (long)N * 4);
   const __amdgpu_buffer_rsrc_t RD = arsrc(a.delta + (size_t)bh * N, (long)N * 4);
   ATile at;
   at.init();
@@ -708,7 +713,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int e = 4 * g + i;
-          float p = __builtin_amdgcn_exp2f(fmaf(st[e], scl, -Lv[i] * LOG2E));
+          float p = __builtin_amdgcn_exp2f(fmaf(st[e], scl, -Lv[i]));
           if (MASK && q0 + 32 * t + 8 * g + 4 * h + i >= N) p = 0.f;
           st[e] = p;
           dpt[e] = p * (dpt[e] - Dv[i]);
@@ -788,7 +793,7 @@ constexpr int Q2_QB = 128, Q2_KT = 64;
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_q2_k(AttnBwd a) {
   __shared__ __attribute__((aligned(1024))) char K0[16384], V0[16384], K1[16384], V1[16384], K2[16384], V2[16384];
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
   const int q = blockIdx.x * Q2_QB + w * 32 + c32;
   const int N = a.N;
   const size_t base = (size_t)bh * N * DH;

@@ -277,7 +277,7 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   W.dQh = a.take(hn * m.Dh * es);
   W.dKh = a.take(hn * m.Dh * es);
   W.dVh = a.take(hn * m.Dh * es);
-  W.delta = a.f32(hn);
+  W.delta = a.f32(2 * hn);  // delta, then the log-sum-exp in log2 units
   W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, QK_PARTS * 2 * m.Dh + m.D, m.pd});
   const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   W.p1 = a.f32((size_t)nch * W.maxcols);
@@ -873,6 +873,41 @@ jagg_status jagg_route(const double* scores, int n_groups, double tau, double fr
   for (int g = 0; g < n_groups; ++g) use_jagg_out[g] = g < n ? 1 : 0;
   if (frac_out) *frac_out = (double)n / n_groups;
   return JAGG_OK;
+}
+
+jagg_status jagg_linear_grad(jagg_ctx* ctx, int kind, const void* dY, const void* other, const void* pre, int rows,
+                             int n_out, int n_in, void* result, int result_dtype, float beta) {
+  if (!ctx || !dY || !other || !result) return fail(JAGG_EINVAL, "jagg_linear_grad: null argument");
+  if (kind != JAGG_DGRAD && kind != JAGG_DGRAD_GELU && kind != JAGG_WGRAD)
+    return fail(JAGG_EINVAL, "jagg_linear_grad: unknown kind");
+  if (rows < 1 || n_out < 1 || n_in < 1) return fail(JAGG_EINVAL, "jagg_linear_grad: sizes must be >= 1");
+  if (result_dtype != JAGG_F32 && result_dtype != JAGG_BF16)
+    return fail(JAGG_EINVAL, "jagg_linear_grad: unknown result dtype");
+  if (kind == JAGG_DGRAD_GELU && (!pre || result_dtype != JAGG_BF16))
+    return fail(JAGG_EINVAL, "jagg_linear_grad: the GELU kind needs pre and a bf16 result");
+  if ((kind == JAGG_WGRAD ? (beta != 0.f && beta != 1.f) : beta != 0.f))
+    return fail(JAGG_EINVAL, "jagg_linear_grad: beta must be 0 (or 1 for the weight gradient)");
+  if (((uintptr_t)dY | (uintptr_t)other | (uintptr_t)pre | (uintptr_t)result) % 16)
+    return fail(JAGG_EINVAL, "jagg_linear_grad: device pointers must be 16-byte aligned");
+  jg::GemmArgs g;
+  g.A = dY; g.a_dt = jg::BF16;
+  g.B = other; g.b_dt = jg::BF16; g.tb = 1;
+  g.epi.C = result; g.epi.c_dt = result_dtype;
+  if (kind == JAGG_WGRAD) {
+    g.lda = n_out; g.ta = 1;
+    g.ldb = n_in;
+    g.M = n_out; g.N = n_in; g.K = rows;
+    g.epi.ldc = n_in; g.epi.beta = beta;
+  } else {
+    g.lda = n_out; g.ta = 0;
+    g.ldb = n_in;
+    g.M = rows; g.N = n_in; g.K = n_out;
+    g.epi.ldc = n_in;
+    if (kind == JAGG_DGRAD_GELU) {
+      g.epi.mode = jg::EPI_GELU_BWD; g.epi.aux = (void*)pre; g.epi.ldaux = n_in; g.epi.aux_dt = jg::BF16;
+    }
+  }
+  return to_status(jg::gemm(g, ctx->stream));
 }
 
 jagg_status jagg_group_backward(jagg_ctx* ctx, const void* theta, const void* saved_pair, int batch,

@@ -741,6 +741,123 @@ struct DtlOp {
   }
 };
 
+// Epilogue of the direct-to-LDS kernel.  Each wave stages its accumulator
+// tiles transposed in its own LDS region (one k stage per wave) and reads them
+// back as 16 consecutive outputs of one row per lane; no workgroup barrier is
+// needed because a wave reads back only what it wrote and one wave's LDS
+// operations complete in issue order.  A tile that lies inside C takes the
+// fast path: a whole row of FN accumulator tiles is staged at once and every
+// global load its epilogue kind needs (old C, GELU input, bias) is issued
+// before the first use, so the load latency is paid once per row of tiles
+// instead of once per 32x32 tile.  Edge tiles take the checked path.
+template <int BM, int BN, int EK>
+__device__ __forceinline__ void dtl_epilogue(const GemmArgs& g, f32x16 (&acc)[BM / 64][BN / 64], int m0, int n0,
+                                             float* T) {
+  constexpr int FM = BM / 64, FN = BN / 64, ES = 36, TS = 32 * ES;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / 2, wn = wave % 2;
+  const int h = lane >> 5, c32 = lane & 31;
+  const int rr = lane & 31, cc = (lane >> 5) * 16;  // read-back: row rr, columns cc .. cc+15
+  const int rbase = m0 + wm * (BM / 2), cbase = n0 + wn * (BN / 2);
+  const bool vec_ok = (g.N % 8 == 0) && (g.epi.ldc % 8 == 0);
+  const bool inner = vec_ok && m0 + BM <= g.M && n0 + BN <= g.N;
+  const Epi& e = g.epi;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq)
+        *(float4*)(T + j * TS + c32 * ES + 8 * gq + 4 * h) =
+            make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]);
+    asm volatile("" ::: "memory");
+    const int row = rbase + i * 32 + rr;
+    if (inner) {
+      float v[FN][2][8];
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[j][hf][q] = T[j * TS + (cc + 8 * hf + q) * ES + rr];
+      asm volatile("" ::: "memory");
+      // inputs of the epilogue kind, all in flight together
+      u32x4 in0[FN][2], in1[FN][2];
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int col = cbase + j * 32 + cc + 8 * hf;
+          if constexpr (EK == EK_F32_ACC) {
+            const u32x4* cp = (const u32x4*)((const float*)e.C + (size_t)row * e.ldc + col);
+            in0[j][hf] = cp[0];
+            in1[j][hf] = cp[1];
+          } else if constexpr (EK == EK_BF16_ACC) {
+            in0[j][hf] = *(const u32x4*)((const uint16_t*)e.C + (size_t)row * e.ldc + col);
+          } else if constexpr (EK == EK_DGELU) {
+            in0[j][hf] = *(const u32x4*)((const uint16_t*)e.aux + (size_t)row * e.ldaux + col);
+          } else if constexpr (EK == EK_BIAS || EK == EK_GELU) {
+            in0[j][hf] = *(const u32x4*)((const uint16_t*)e.bias + col);
+          }
+        }
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int col = cbase + j * 32 + cc + 8 * hf;
+          float* x = v[j][hf];
+          if constexpr (EK == EK_F32 || EK == EK_F32_ACC) {
+            if constexpr (EK == EK_F32_ACC) {
+              const float4 o0 = __builtin_bit_cast(float4, in0[j][hf]), o1 = __builtin_bit_cast(float4, in1[j][hf]);
+              x[0] += o0.x; x[1] += o0.y; x[2] += o0.z; x[3] += o0.w;
+              x[4] += o1.x; x[5] += o1.y; x[6] += o1.z; x[7] += o1.w;
+            }
+            float4* cp = (float4*)((float*)e.C + (size_t)row * e.ldc + col);
+            cp[0] = make_float4(x[0], x[1], x[2], x[3]);
+            cp[1] = make_float4(x[4], x[5], x[6], x[7]);
+          } else {
+            float o[8];
+            if constexpr (EK != EK_BF16) unpack8(in0[j][hf], o);
+            if constexpr (EK == EK_BF16_ACC || EK == EK_BIAS || EK == EK_GELU) {
+#pragma unroll
+              for (int q = 0; q < 8; ++q) x[q] += o[q];
+            }
+            if constexpr (EK == EK_GELU) {
+              *(u32x4*)((uint16_t*)e.aux + (size_t)row * e.ldaux + col) = pack8(x);
+#pragma unroll
+              for (int q = 0; q < 8; ++q) x[q] = gelu_tanh(x[q]);
+            }
+            if constexpr (EK == EK_DGELU) {
+#pragma unroll
+              for (int q = 0; q < 8; ++q) x[q] *= gelu_tanh_grad(o[q]);
+            }
+            *(u32x4*)((uint16_t*)e.C + (size_t)row * e.ldc + col) = pack8(x);
+          }
+        }
+    } else {
+#pragma unroll 1
+      for (int j = 0; j < FN; ++j)
+#pragma unroll 1
+        for (int hf = 0; hf < 2; ++hf) {
+          const int col = cbase + j * 32 + cc + 8 * hf;
+          if (row >= g.M) continue;
+          float v[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] = T[j * TS + (cc + 8 * hf + q) * ES + rr];
+          if (vec_ok && col + 8 <= g.N) {
+            epi8<EK>(e, row, col, v);
+          } else {
+#pragma unroll 1
+            for (int q = 0; q < 8; ++q)
+              if (col + q < g.N) epi1<EK>(e, row, col + q, v[q]);
+          }
+        }
+    }
+    // the next row's staging writes must not move above this row's reads
+    asm volatile("" ::: "memory");
+  }
+}
+
 template <bool TA, bool TB, int EK, int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
   constexpr int BK = 32, WM = 2, WN = 2, FM = BM / 64, FN = BN / 64;
@@ -843,9 +960,12 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
   if (kt < nk) iter(std::integral_constant<int, 0>(), kt);
   if (kt + 1 < nk) iter(std::integral_constant<int, 1>(), kt + 1);
   if (kt + 2 < nk) iter(std::integral_constant<int, 2>(), kt + 2);
+  // every direct load has landed and every wave is past its last fragment
+  // read before the stages are reused as per-wave epilogue staging
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  mfma_epilogue<BM, BN, WM, WN, EK>(g, acc, m0, n0, (uint16_t*)st0);
+  float* T = (float*)(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
+  dtl_epilogue<BM, BN, EK>(g, acc, m0, n0, T);
 }
 
 // ---------------------------------------------------------------- VALU GEMM

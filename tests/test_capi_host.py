@@ -107,3 +107,20 @@ def test_invalid_arguments_are_rejected_before_any_launch():
     import ctypes
     assert L.dit_vjp(None, None, None, 1, None, None, 0.0) == 1
     assert L.jagg_group_backward(None, None, None, 1, None, None, 4, None, 0.0) == 1
+    # linear-layer products: every argument error is caught on the host
+    c = pk.config("tiny").c()
+    h = ctypes.c_void_p()
+    assert L.jagg_ctx_create(ctypes.byref(c), None, ctypes.byref(h)) == 0
+    try:
+        p16, p8 = 4096, 4104  # never dereferenced: every call below fails validation first
+        assert L.jagg_linear_grad(h, 3, p16, p16, None, 8, 8, 8, p16, 0, 0.0) == 1       # unknown kind
+        assert L.jagg_linear_grad(h, 0, p16, None, None, 8, 8, 8, p16, 0, 0.0) == 1      # null operand
+        assert L.jagg_linear_grad(h, 0, p8, p16, None, 8, 8, 8, p16, 0, 0.0) == 1        # unaligned
+        assert L.jagg_linear_grad(h, 0, p16, p16, None, 0, 8, 8, p16, 0, 0.0) == 1       # empty
+        assert L.jagg_linear_grad(h, 0, p16, p16, None, 8, 8, 8, p16, 0, 1.0) == 1       # beta on dgrad
+        assert L.jagg_linear_grad(h, 1, p16, p16, None, 8, 8, 8, p16, 1, 0.0) == 1       # GELU without pre
+        assert L.jagg_linear_grad(h, 1, p16, p16, p16, 8, 8, 8, p16, 0, 0.0) == 1        # GELU to fp32
+        assert L.jagg_linear_grad(h, 2, p16, p16, None, 8, 8, 8, p16, 0, 0.5) == 1       # beta not 0/1
+        assert L.jagg_linear_grad(h, 2, p16, p16, None, 8, 8, 8, p16, 7, 0.0) == 1       # unknown dtype
+    finally:
+        L.jagg_ctx_destroy(h)
