@@ -157,6 +157,77 @@ jagg_status jagg_route(const double* scores, int n_groups, double tau, double fr
 jagg_status jagg_group_backward(jagg_ctx* ctx, const void* theta, const void* saved_pair, int batch,
                                 const void* const* s, const float* t, int W, void* dtheta, float beta);
 
+/* Sequential-graph JAGG (appendix, sequential-graph variant): the backward of
+ * ONE endpoint of the window, so that only that endpoint's saved activations
+ * must exist at a time (the caller can run dit_forward_save for z_0, this call
+ * with endpoint 0, then dit_forward_save for z_{W-1} into the same buffer and
+ * this call with endpoint 1).  endpoint 0: dtheta = beta * dtheta +
+ * J_0^T s_base; endpoint 1: dtheta = beta * dtheta + J_{W-1}^T s_corr, with the
+ * composites of Eq. s_base / s_corr formed from the W upstream gradients (s:
+ * host array of W device pointers, each a batch-B output; t: host W
+ * timesteps).  saved: a batch-B forward of z_0 at t_0 (endpoint 0) or of
+ * z_{W-1} at t_{W-1} (endpoint 1).  Endpoint 0 then endpoint 1 (beta 1) gives
+ * the joint call's gradient up to fp32 summation order.  Workspace:
+ * dit_workspace_bytes(batch).  2 <= W <= 64. */
+jagg_status jagg_endpoint_backward(jagg_ctx* ctx, const void* theta, const void* saved, int batch, const void* const* s,
+                                   const float* t, int W, int endpoint, void* dtheta, float beta);
+
+/* Gradient quality (gradient-quality appendix: cos(g_jagg, g_exact) and the
+ * norm ratio rho = |g_jagg| / |g_exact|): the fp64 sums a.b, a.a and b.b over n
+ * elements of two device vectors of `dtype` (16-byte aligned), returned in
+ * out[0..2] (host).  cos = out[0] / sqrt(out[1] out[2]), rho = sqrt(out[1] /
+ * out[2]).  Every element of the n is included: flat gradient buffers must
+ * hold zeros in their padding.  Deterministic (fixed block order).  Uses the
+ * bound workspace; synchronises the context's stream. */
+jagg_status jagg_grad_compare(jagg_ctx* ctx, const void* a, const void* b, size_t n, int dtype, double* out);
+
+/* Phase 2 of JAGG for a GRPO window on rectified flow (GRPO section: Eq.
+ * grpo_loss, Eq. logprob and the Euler-step mean; hyperparameter appendix:
+ * clip range, advantage clamp).  Per sample b and step j:
+ *   mu_j = z_j + v_j (t_{j+1} - t_j)
+ *   log pi_j = -|z_{j+1} - mu_j|^2 / (2 sigma_j^2) - n log(sqrt(2 pi) sigma_j)
+ *              (n = elements per sample; squared norm over the sample)
+ *   rho_j = exp(log pi_j - logp_old[j][b]), A = clamp(adv[b], -adv_clip, adv_clip)
+ *   L_j = (1/W) max(-A rho_j, -A clip(rho_j, 1 - clip_eps, 1 + clip_eps))
+ *   s_j = dL_j / dv_j = c_j (z_{j+1} - mu_j), c_j = dL_j/drho_j * rho_j *
+ *         (t_{j+1} - t_j) / sigma_j^2, with dL_j/drho_j = 0 when the clipped
+ *         term is strictly the larger (the PPO-clip remark's zero gradient)
+ *         and -A/W otherwise.
+ * The squared norms are accumulated in fp64 and the clip decision is taken
+ * in fp64; the gradients are formed in fp32.  All arrays use the batch-B
+ * output layout of the model (block-only: stream-major token rows); every
+ * per-sample segment must be a multiple of 8 elements. */
+typedef struct {
+  const void* const* v_hat; /* host array of W device pointers: model outputs v_j */
+  const void* const* z;     /* host array of W+1 device pointers: z_0 .. z_W */
+  const float* t;           /* host, W+1 timesteps t_0 .. t_W (t_W: the step after the window) */
+  const float* sigma;       /* host, W: sigma_j > 0 */
+  const double* logp_old;   /* device, W x batch, [j][b]: log pi_old(z_{j+1} | z_j) */
+  const float* adv;         /* device, batch: advantages */
+  float clip_eps;           /* PPO clip range (0.1 in the paper's runs) */
+  float adv_clip;           /* advantage clamp (5.0 in the paper's runs) */
+  int W;                    /* 2..8, 10, 12 or 16 */
+} jagg_grpo_window;
+
+/* Phases 2 and 3 fused: the composites s_base, s_corr (Eq. s_base / s_corr with
+ * alpha from t_0 .. t_{W-1}) of the window's GRPO upstream gradients, without
+ * materialising any s_j.  s_base, s_corr: device, batch-B output layout.
+ * stats: device, W x batch x 3 doubles (log pi_j, rho_j, L_j) or NULL.  batch
+ * 1..16.  Uses the bound workspace. */
+jagg_status jagg_grpo_composites(jagg_ctx* ctx, const jagg_grpo_window* w, int batch, void* s_base, void* s_corr,
+                                 double* stats);
+
+/* Phase 2 alone: the W upstream gradients s_j (host array of W device
+ * pointers, batch-B output layout), for the per-step baseline. */
+jagg_status jagg_grpo_upstream(jagg_ctx* ctx, const jagg_grpo_window* w, int batch, void* const* s_out,
+                               double* stats);
+
+/* Phases 2-4: the fused composites written straight into the endpoint pair's
+ * cotangent, then one VJP over the batch-2B pair (as jagg_group_backward).
+ * dtheta = beta * dtheta + g_jagg. */
+jagg_status jagg_grpo_group_backward(jagg_ctx* ctx, const void* theta, const void* saved_pair, int batch,
+                                     const jagg_grpo_window* w, void* dtheta, float beta, double* stats);
+
 /* Per-step baseline: W VJPs, one per step, accumulated into dtheta
  * (dtheta = beta * dtheta + sum_j J_j^T s_j).  saved: host array of W device
  * pointers, each a batch-B forward. */
@@ -193,7 +264,8 @@ jagg_status jagg_linear_grad(jagg_ctx* ctx, int kind, const void* dY, const void
  * 3 weight-gradient GEMM (dW = dY^T X), 4 attention forward (work: the QK^T
  * and PV products), 5 attention backward dK/dV kernel (work: the dV, dP and
  * dK products; the score recompute is not counted), 6 attention backward dQ
- * kernel (work: the dQ product), 7 aggregation. */
+ * kernel (work: the dQ product), 7 aggregation, 8 gradient comparison (work:
+ * bytes read), 9 GRPO upstream gradients and their composites (work: bytes). */
 jagg_status jagg_prof_begin(int cls);
 jagg_status jagg_prof_end(long* launches, double* total_ms, double* total_work);
 

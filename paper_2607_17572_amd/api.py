@@ -23,6 +23,13 @@ class _DitConfig(ctypes.Structure):
         "lat_w", "n_txt", "txt_dim", "t_freq_dim", "block_only", "act_dtype", "grad_dtype", "checkpoint")]
 
 
+class _GrpoWindow(ctypes.Structure):
+    _fields_ = [("v_hat", ctypes.POINTER(ctypes.c_void_p)), ("z", ctypes.POINTER(ctypes.c_void_p)),
+                ("t", ctypes.POINTER(ctypes.c_float)), ("sigma", ctypes.POINTER(ctypes.c_float)),
+                ("logp_old", ctypes.c_void_p), ("adv", ctypes.c_void_p), ("clip_eps", ctypes.c_float),
+                ("adv_clip", ctypes.c_float), ("W", ctypes.c_int)]
+
+
 class _TensorDesc(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("offset", ctypes.c_size_t), ("numel", ctypes.c_size_t),
                 ("rows", ctypes.c_int), ("cols", ctypes.c_int)]
@@ -57,6 +64,11 @@ def lib() -> ctypes.CDLL:
             "jagg_group_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, vp, f],
             "perstep_group_backward": [vp, vp, ctypes.POINTER(vp), i, ctypes.POINTER(vp), i, vp, f],
             "jagg_linear_grad": [vp, i, vp, vp, vp, i, i, i, vp, i, f],
+            "jagg_endpoint_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, i, vp, f],
+            "jagg_grad_compare": [vp, vp, vp, sz, i, ctypes.POINTER(d)],
+            "jagg_grpo_composites": [vp, ctypes.POINTER(_GrpoWindow), i, vp, vp, vp],
+            "jagg_grpo_upstream": [vp, ctypes.POINTER(_GrpoWindow), i, ctypes.POINTER(vp), vp],
+            "jagg_grpo_group_backward": [vp, vp, vp, i, ctypes.POINTER(_GrpoWindow), vp, f, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -146,6 +158,7 @@ def route(n_groups: int, frac: float | None = None, scores=None, tau: float = 0.
 
 PROF_GEMM_FWD, PROF_GEMM_DGRAD, PROF_GEMM_WGRAD = 1, 2, 3
 PROF_ATTN_FWD, PROF_ATTN_BWD_KV, PROF_ATTN_BWD_Q, PROF_AGGREGATE = 4, 5, 6, 7
+PROF_COMPARE, PROF_UPSTREAM = 8, 9
 
 
 def prof_begin(cls: int):
@@ -266,6 +279,66 @@ class Context:
         tt = (ctypes.c_float * W)(*[float(x) for x in t])
         _check(lib().jagg_group_backward(self._h, theta.data_ptr(), saved_pair.data_ptr(), batch, _ptrs(s_list), tt,
                                          W, dtheta.data_ptr(), float(beta)))
+        return dtheta
+
+    def endpoint_backward(self, theta, saved, batch: int, s_list, t, endpoint: int, dtheta, beta: float = 0.0):
+        """Sequential-graph JAGG: the backward of one endpoint (0: s_base, 1: s_corr)."""
+        W = len(s_list)
+        self.ensure_workspace(batch)
+        tt = (ctypes.c_float * W)(*[float(x) for x in t])
+        _check(lib().jagg_endpoint_backward(self._h, theta.data_ptr(), saved.data_ptr(), batch, _ptrs(s_list), tt, W,
+                                            int(endpoint), dtheta.data_ptr(), float(beta)))
+        return dtheta
+
+    def grad_compare(self, a, b):
+        """(a.b, a.a, b.b) in fp64 over every element of two equal-size device tensors."""
+        self.ensure_workspace(1)
+        out = (ctypes.c_double * 3)()
+        dt = BF16 if a.dtype == _torch().bfloat16 else F32
+        assert a.numel() == b.numel() and a.dtype == b.dtype
+        _check(lib().jagg_grad_compare(self._h, a.data_ptr(), b.data_ptr(), a.numel(), dt, out))
+        return out[0], out[1], out[2]
+
+    @staticmethod
+    def _grpo_window(v_list, z_list, t, sigma, logp_old, adv, clip_eps, adv_clip):
+        """The C struct of one GRPO window; returns (struct, keep-alive list).
+        logp_old: device fp64 tensor [W][B]; adv: device fp32 tensor [B]."""
+        W = len(v_list)
+        assert len(z_list) == W + 1 and len(t) == W + 1 and len(sigma) == W
+        vp, zp = _ptrs(v_list), _ptrs(z_list)
+        tt = (ctypes.c_float * (W + 1))(*[float(x) for x in t])
+        sg = (ctypes.c_float * W)(*[float(x) for x in sigma])
+        w = _GrpoWindow(vp, zp, tt, sg, logp_old.data_ptr(), adv.data_ptr(), float(clip_eps), float(adv_clip), W)
+        return w, [vp, zp, tt, sg]
+
+    def grpo_composites(self, v_list, z_list, t, sigma, logp_old, adv, s_base, s_corr, clip_eps=0.1, adv_clip=5.0,
+                        stats=None, batch=None):
+        """Phases 2 + 3 fused: composites of the window's GRPO upstream gradients."""
+        B = adv.numel() if batch is None else batch
+        self.ensure_workspace(1)
+        w, keep = self._grpo_window(v_list, z_list, t, sigma, logp_old, adv, clip_eps, adv_clip)
+        _check(lib().jagg_grpo_composites(self._h, ctypes.byref(w), B, s_base.data_ptr(), s_corr.data_ptr(),
+                                          None if stats is None else stats.data_ptr()))
+        return s_base, s_corr
+
+    def grpo_upstream(self, v_list, z_list, t, sigma, logp_old, adv, s_out, clip_eps=0.1, adv_clip=5.0, stats=None,
+                      batch=None):
+        """Phase 2: the W upstream gradients s_j (written into s_out)."""
+        B = adv.numel() if batch is None else batch
+        self.ensure_workspace(1)
+        w, keep = self._grpo_window(v_list, z_list, t, sigma, logp_old, adv, clip_eps, adv_clip)
+        _check(lib().jagg_grpo_upstream(self._h, ctypes.byref(w), B, _ptrs(s_out),
+                                        None if stats is None else stats.data_ptr()))
+        return s_out
+
+    def grpo_group_backward(self, theta, saved_pair, batch: int, v_list, z_list, t, sigma, logp_old, adv, dtheta,
+                            beta: float = 0.0, clip_eps=0.1, adv_clip=5.0, stats=None):
+        """Phases 2-4: fused composites into the pair cotangent, one joint VJP."""
+        self.ensure_workspace(2 * batch)
+        w, keep = self._grpo_window(v_list, z_list, t, sigma, logp_old, adv, clip_eps, adv_clip)
+        _check(lib().jagg_grpo_group_backward(self._h, theta.data_ptr(), saved_pair.data_ptr(), batch,
+                                              ctypes.byref(w), dtheta.data_ptr(), float(beta),
+                                              None if stats is None else stats.data_ptr()))
         return dtheta
 
     def linear_grad(self, kind: int, dY, other, result, beta: float = 0.0, pre=None):

@@ -2,6 +2,7 @@
 // backward (Phases 3 and 4: composites, then one VJP over the batched endpoint
 // pair) and the per-step baseline.  Everything is stream-ordered on the
 // context's HIP stream; the caller owns every buffer.
+#include <algorithm>
 #include <array>
 #include <cmath>
 #include <cstring>
@@ -249,6 +250,7 @@ struct Ws {
   float* dfa = nullptr;
   void* cot = nullptr;
   double *spart = nullptr, *score = nullptr;
+  float* gcoef = nullptr;  // GRPO coefficients [W][B]
   int maxcols = 0;
 };
 
@@ -262,8 +264,10 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   const size_t hn = (size_t)B * m.H * m.N;
   W = Ws();
   // group-score buffers first: their offset does not depend on the batch
-  W.spart = (double*)a.take(score_part_doubles(8) * sizeof(double));
+  W.spart = (double*)a.take(std::max({score_part_doubles(8), compare_part_doubles(),
+                                       grpo_part_doubles(GRPO_MAX_W, 32)}) * sizeof(double));
   W.score = (double*)a.take(64);
+  W.gcoef = (float*)a.take((size_t)GRPO_MAX_W * 32 * sizeof(float));
   if (m.c.n_double) plan_dbl(m, a, B, W.sd, true);
   if (m.c.n_single) plan_sgl(m, a, B, W.ss, true);
   W.xa = a.take(rows * m.D * es);
@@ -947,6 +951,176 @@ jagg_status jagg_group_backward(jagg_ctx* ctx, const void* theta, const void* sa
   a.in_dt = a.out_dt = m.act;
   int rc = jg::aggregate(a, ctx->stream);
   if (rc) return (jagg_status)rc;
+  return to_status(jg::vjp(ctx, theta, saved_pair, B2, cot, dtheta, beta));
+}
+
+jagg_status jagg_endpoint_backward(jagg_ctx* ctx, const void* theta, const void* saved, int batch, const void* const* s,
+                                   const float* t, int W, int endpoint, void* dtheta, float beta) {
+  if (!ctx || !theta || !saved || !s || !t || !dtheta) return fail(JAGG_EINVAL, "jagg_endpoint_backward: null argument");
+  if (batch < 1 || batch > MAX_BATCH) return fail(JAGG_EINVAL, "jagg_endpoint_backward: batch must be 1..32");
+  if (endpoint != 0 && endpoint != 1) return fail(JAGG_EINVAL, "jagg_endpoint_backward: endpoint must be 0 or 1");
+  if (beta != 0.f && beta != 1.f) return fail(JAGG_EINVAL, "jagg_endpoint_backward: beta must be 0 or 1");
+  if (((uintptr_t)theta | (uintptr_t)saved | (uintptr_t)dtheta) % 16)
+    return fail(JAGG_EINVAL, "jagg_endpoint_backward: device pointers must be 16-byte aligned");
+  jagg_status st = need_ws(ctx, batch);
+  if (st) return st;
+  jg::AggArgs a;
+  std::memset(&a, 0, sizeof(a));
+  st = agg_weights(t, W, a);
+  if (st) return st;
+  for (int j = 0; j < W; ++j) {
+    if (!s[j] || (uintptr_t)s[j] % 16) return fail(JAGG_EINVAL, "jagg_endpoint_backward: null or unaligned s_j");
+    a.s[j] = s[j];
+  }
+  const jg::Model& m = ctx->m;
+  jg::Ws Wb;
+  jg::plan_ws(m, batch, ctx->ws, Wb);
+  // the composite of this endpoint only, in the batch-B output layout
+  a.n = (size_t)batch * jg::out_elems(m);
+  a.split = a.n;
+  if (endpoint == 0) a.base0 = a.base1 = Wb.cot;
+  else a.corr0 = a.corr1 = Wb.cot;
+  a.in_dt = a.out_dt = m.act;
+  int rc = jg::aggregate(a, ctx->stream);
+  if (rc) return (jagg_status)rc;
+  return to_status(jg::vjp(ctx, theta, saved, batch, Wb.cot, dtheta, beta));
+}
+
+jagg_status jagg_grad_compare(jagg_ctx* ctx, const void* a, const void* b, size_t n, int dtype, double* out) {
+  if (!ctx || !a || !b || !out) return fail(JAGG_EINVAL, "jagg_grad_compare: null argument");
+  if (n == 0) return fail(JAGG_EINVAL, "jagg_grad_compare: empty vectors");
+  if (dtype != JAGG_F32 && dtype != JAGG_BF16) return fail(JAGG_EINVAL, "jagg_grad_compare: unknown dtype");
+  if (((uintptr_t)a | (uintptr_t)b) % 16) return fail(JAGG_EINVAL, "jagg_grad_compare: vectors must be 16-byte aligned");
+  jg::Ws W0;
+  jg::plan_ws(ctx->m, 1, ctx->ws, W0);
+  static_assert(jg::CMP_BLOCKS * 3 <= 512 * 36, "compare partials must fit the score partial buffer");
+  const size_t need = jg::score_part_doubles(8) * sizeof(double) + 256;
+  if (!ctx->ws || ctx->ws_bytes < need) return fail(JAGG_EINVAL, "jagg_grad_compare: workspace not bound");
+  int rc = jg::grad_compare(a, b, n, dtype, W0.spart, W0.score, ctx->stream);
+  if (rc) return (jagg_status)rc;
+  if (hipMemcpyAsync(out, W0.score, 3 * sizeof(double), hipMemcpyDeviceToHost, ctx->stream) != hipSuccess ||
+      hipStreamSynchronize(ctx->stream) != hipSuccess)
+    return fail(JAGG_EDEVICE, "jagg_grad_compare: copy of the sums failed");
+  return JAGG_OK;
+}
+
+// Validates one GRPO window and fills the arguments shared by the three
+// GRPO entry points (everything but the outputs).
+static jagg_status grpo_args(const jagg_ctx* ctx, const jagg_grpo_window* w, int batch, jg::GrpoArgs& a,
+                             const char* who) {
+  const std::string f = who;
+  if (!w || !w->v_hat || !w->z || !w->t || !w->sigma || !w->logp_old || !w->adv)
+    return fail(JAGG_EINVAL, f + ": null argument");
+  if (batch < 1 || batch > 16) return fail(JAGG_EINVAL, f + ": batch must be 1..16");
+  const int W = w->W;
+  if (W < 2 || W > jg::GRPO_MAX_W) return fail(JAGG_EINVAL, f + ": W must be 2..16");
+  if (!(w->clip_eps >= 0.f) || !(w->adv_clip > 0.f)) return fail(JAGG_EINVAL, f + ": bad clip range or advantage clamp");
+  std::memset(&a, 0, sizeof(a));
+  const double t0 = w->t[0], den = (double)w->t[0] - (double)w->t[W - 1];
+  if (den == 0.0) return fail(JAGG_EINVAL, f + ": t_0 == t_{W-1}");
+  for (int j = 0; j < W; ++j) {
+    if (!(w->sigma[j] > 0.f)) return fail(JAGG_EINVAL, f + ": sigma_j must be positive");
+    if (!w->v_hat[j] || (uintptr_t)w->v_hat[j] % 16) return fail(JAGG_EINVAL, f + ": null or unaligned v_j");
+    const double al = (t0 - (double)w->t[j]) / den;
+    a.wb[j] = (float)(1.0 - al);
+    a.wc[j] = (float)al;
+    a.dts[j] = (double)w->t[j + 1] - (double)w->t[j];
+    a.sigma[j] = w->sigma[j];
+    a.v[j] = w->v_hat[j];
+  }
+  for (int j = 0; j <= W; ++j) {
+    if (!w->z[j] || (uintptr_t)w->z[j] % 16) return fail(JAGG_EINVAL, f + ": null or unaligned z_j");
+    a.z[j] = w->z[j];
+  }
+  const jg::Model& m = ctx->m;
+  a.W = W;
+  a.B = batch;
+  a.dt = m.act;
+  if (m.c.block_only) {  // stream-major rows: text rows of all samples, then image rows
+    a.len0 = (size_t)m.nt * m.D;
+    a.len1 = (size_t)m.ni * m.D;
+    a.split = (size_t)batch * a.len0;
+  } else {
+    a.len0 = 0;
+    a.len1 = jg::out_elems(m);
+    a.split = 0;
+  }
+  a.n = (size_t)batch * (a.len0 + a.len1);
+  a.logp_old = w->logp_old;
+  a.adv = w->adv;
+  a.eps = w->clip_eps;
+  a.adv_clip = w->adv_clip;
+  return JAGG_OK;
+}
+
+static jagg_status grpo_run(jagg_ctx* ctx, jg::GrpoArgs& a, double* stats) {
+  if (!ctx->ws) return fail(JAGG_EINVAL, "GRPO window: workspace not bound");
+  jg::Ws W0;
+  jg::plan_ws(ctx->m, 1, ctx->ws, W0);
+  if ((char*)W0.gcoef + (size_t)jg::GRPO_MAX_W * 32 * sizeof(float) > (char*)ctx->ws + ctx->ws_bytes)
+    return fail(JAGG_EINVAL, "GRPO window: workspace too small");
+  return to_status(jg::grpo_window(a, W0.spart, W0.gcoef, stats, ctx->stream));
+}
+
+jagg_status jagg_grpo_composites(jagg_ctx* ctx, const jagg_grpo_window* w, int batch, void* s_base, void* s_corr,
+                                 double* stats) {
+  if (!ctx || !s_base || !s_corr) return fail(JAGG_EINVAL, "jagg_grpo_composites: null argument");
+  if (((uintptr_t)s_base | (uintptr_t)s_corr) % 16) return fail(JAGG_EINVAL, "jagg_grpo_composites: unaligned output");
+  jg::GrpoArgs a;
+  jagg_status st = grpo_args(ctx, w, batch, a, "jagg_grpo_composites");
+  if (st) return st;
+  a.mode = 0;
+  a.osplit = a.n;
+  a.base0 = a.base1 = s_base;
+  a.corr0 = a.corr1 = s_corr;
+  return grpo_run(ctx, a, stats);
+}
+
+jagg_status jagg_grpo_upstream(jagg_ctx* ctx, const jagg_grpo_window* w, int batch, void* const* s_out,
+                               double* stats) {
+  if (!ctx || !s_out) return fail(JAGG_EINVAL, "jagg_grpo_upstream: null argument");
+  jg::GrpoArgs a;
+  jagg_status st = grpo_args(ctx, w, batch, a, "jagg_grpo_upstream");
+  if (st) return st;
+  for (int j = 0; j < a.W; ++j) {
+    if (!s_out[j] || (uintptr_t)s_out[j] % 16) return fail(JAGG_EINVAL, "jagg_grpo_upstream: null or unaligned s_j");
+    a.s_out[j] = s_out[j];
+  }
+  a.mode = 1;
+  return grpo_run(ctx, a, stats);
+}
+
+jagg_status jagg_grpo_group_backward(jagg_ctx* ctx, const void* theta, const void* saved_pair, int batch,
+                                     const jagg_grpo_window* w, void* dtheta, float beta, double* stats) {
+  if (!ctx || !theta || !saved_pair || !dtheta) return fail(JAGG_EINVAL, "jagg_grpo_group_backward: null argument");
+  if (beta != 0.f && beta != 1.f) return fail(JAGG_EINVAL, "jagg_grpo_group_backward: beta must be 0 or 1");
+  jg::GrpoArgs a;
+  jagg_status st = grpo_args(ctx, w, batch, a, "jagg_grpo_group_backward");
+  if (st) return st;
+  const int B2 = 2 * batch;
+  st = need_ws(ctx, B2);
+  if (st) return st;
+  const jg::Model& m = ctx->m;
+  jg::Ws Wp;
+  jg::plan_ws(m, B2, ctx->ws, Wp);
+  const size_t es = jg::dsize(m.act);
+  char* cot = (char*)Wp.cot;
+  // composites straight into the cotangent of the batch-2B endpoint pair
+  a.mode = 0;
+  if (m.c.block_only) {
+    const size_t txt = (size_t)batch * m.nt * m.D, img = (size_t)batch * m.ni * m.D;
+    a.osplit = txt;
+    a.base0 = cot;
+    a.corr0 = cot + txt * es;
+    a.base1 = cot + 2 * txt * es;
+    a.corr1 = cot + (2 * txt + img) * es;
+  } else {
+    a.osplit = a.n;
+    a.base0 = a.base1 = cot;
+    a.corr0 = a.corr1 = cot + a.n * es;
+  }
+  st = grpo_run(ctx, a, stats);
+  if (st) return st;
   return to_status(jg::vjp(ctx, theta, saved_pair, B2, cot, dtheta, beta));
 }
 

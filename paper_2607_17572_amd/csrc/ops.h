@@ -127,4 +127,34 @@ struct ScoreArgs {
 size_t score_part_doubles(int W);
 int group_scores(const ScoreArgs& a, double* part, double* score_dev, hipStream_t s);
 
+// ---- GRPO upstream gradients (Phase 2) and their composites (Phase 3) ----
+// Rollout data of one window in the batch-B output layout: element e belongs
+// to sample e / len0 when e < split, else to sample (e - split) / len1.
+constexpr int GRPO_MAX_W = 16;
+struct GrpoArgs {
+  const void* v[GRPO_MAX_W];      // model outputs v_j
+  const void* z[GRPO_MAX_W + 1];  // latents z_0 .. z_W
+  int W, B, dt;
+  size_t split, len0, len1, n;    // n = B * (len0 + len1)
+  double dts[GRPO_MAX_W];         // t_{j+1} - t_j (fp64; pass 2 rounds it to fp32)
+  float wb[GRPO_MAX_W], wc[GRPO_MAX_W];  // 1 - alpha_j, alpha_j
+  double sigma[GRPO_MAX_W];
+  const double* logp_old;         // [W][B], device
+  const float* adv;               // [B], device
+  float eps, adv_clip;
+  // outputs: composites (mode 0) with the aggregation's split mapping, or the
+  // W per-step gradients (mode 1) in the batch-B layout
+  int mode;
+  size_t osplit;
+  void *base0, *base1, *corr0, *corr1;
+  void* s_out[GRPO_MAX_W];
+};
+size_t grpo_part_doubles(int W, int B);
+int grpo_window(const GrpoArgs& a, double* part, float* coef, double* stats, hipStream_t s);
+
+// ---- gradient comparison: fp64 sums a.b, a.a, b.b over n elements ----
+constexpr int CMP_BLOCKS = 1024;
+size_t compare_part_doubles();
+int grad_compare(const void* a, const void* b, size_t n, int dt, double* part, double* out_dev, hipStream_t s);
+
 }  // namespace jg

@@ -1150,19 +1150,24 @@ __global__ __launch_bounds__(256) void aggregate_k(AggArgs a) {
     TO* dc;
     if (e0 < a.split) { db = (TO*)a.base0 + e0; dc = (TO*)a.corr0 + e0; }
     else { db = (TO*)a.base1 + (e0 - a.split); dc = (TO*)a.corr1 + (e0 - a.split); }
+    // a null destination skips that composite (one endpoint of the sequential variant)
     if constexpr (sizeof(TO) == 2) {
       uint4 ub, uc;
       ub.x = f2bf(sb[0]) | ((uint32_t)f2bf(sb[1]) << 16); ub.y = f2bf(sb[2]) | ((uint32_t)f2bf(sb[3]) << 16);
       ub.z = f2bf(sb[4]) | ((uint32_t)f2bf(sb[5]) << 16); ub.w = f2bf(sb[6]) | ((uint32_t)f2bf(sb[7]) << 16);
       uc.x = f2bf(sc[0]) | ((uint32_t)f2bf(sc[1]) << 16); uc.y = f2bf(sc[2]) | ((uint32_t)f2bf(sc[3]) << 16);
       uc.z = f2bf(sc[4]) | ((uint32_t)f2bf(sc[5]) << 16); uc.w = f2bf(sc[6]) | ((uint32_t)f2bf(sc[7]) << 16);
-      *(uint4*)db = ub;
-      *(uint4*)dc = uc;
+      if (a.base0) *(uint4*)db = ub;
+      if (a.corr0) *(uint4*)dc = uc;
     } else {
-      *(float4*)db = make_float4(sb[0], sb[1], sb[2], sb[3]);
-      *(float4*)(db + 4) = make_float4(sb[4], sb[5], sb[6], sb[7]);
-      *(float4*)dc = make_float4(sc[0], sc[1], sc[2], sc[3]);
-      *(float4*)(dc + 4) = make_float4(sc[4], sc[5], sc[6], sc[7]);
+      if (a.base0) {
+        *(float4*)db = make_float4(sb[0], sb[1], sb[2], sb[3]);
+        *(float4*)(db + 4) = make_float4(sb[4], sb[5], sb[6], sb[7]);
+      }
+      if (a.corr0) {
+        *(float4*)dc = make_float4(sc[0], sc[1], sc[2], sc[3]);
+        *(float4*)(dc + 4) = make_float4(sc[4], sc[5], sc[6], sc[7]);
+      }
     }
   }
 }
@@ -1177,8 +1182,13 @@ __global__ void aggregate_scalar_k(AggArgs a, size_t e_begin) {
       sb = fmaf(a.wb[j], x, sb);
       sc = fmaf(a.wc[j], x, sc);
     }
-    if (e < a.split) { st_any(a.base0, a.out_dt, e, sb); st_any(a.corr0, a.out_dt, e, sc); }
-    else { st_any(a.base1, a.out_dt, e - a.split, sb); st_any(a.corr1, a.out_dt, e - a.split, sc); }
+    if (e < a.split) {
+      if (a.base0) st_any(a.base0, a.out_dt, e, sb);
+      if (a.corr0) st_any(a.corr0, a.out_dt, e, sc);
+    } else {
+      if (a.base1) st_any(a.base1, a.out_dt, e - a.split, sb);
+      if (a.corr1) st_any(a.corr1, a.out_dt, e - a.split, sc);
+    }
   }
 }
 
@@ -1279,6 +1289,255 @@ int group_scores(const ScoreArgs& a, double* part, double* score_dev, hipStream_
   LAUNCH_OK("group_scores_pass1");
   hipLaunchKernelGGL(scores_pass2_k, dim3(1), dim3(64), 0, s, part, (int)grid, a.W, score_dev);
   LAUNCH_OK("group_scores_pass2");
+  return 0;
+}
+
+
+// ============================================================ gradient compare
+// Gradient-quality sums for cos(a, b) and |a| / |b|: a.b, a.a, b.b over n
+// elements, fp64 accumulation.  Pass 1: every thread walks 8-element vectors
+// (16- or 32-byte loads) grid-stride, a block writes its three partials; pass
+// 2: one block adds the block partials in block order (deterministic).
+// HBM traffic: one read of each vector.
+size_t compare_part_doubles() { return (size_t)CMP_BLOCKS * 3; }
+
+template <typename T>
+__device__ __forceinline__ void load8f(const T* p, float* x) {
+  if constexpr (sizeof(T) == 2) {
+    const uint4 u = *(const uint4*)p;
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { x[2 * e] = bf2f(w[e] & 0xffff); x[2 * e + 1] = bf2f(w[e] >> 16); }
+  } else {
+    const float4 u0 = *(const float4*)p, u1 = *(const float4*)(p + 4);
+    x[0] = u0.x; x[1] = u0.y; x[2] = u0.z; x[3] = u0.w;
+    x[4] = u1.x; x[5] = u1.y; x[6] = u1.z; x[7] = u1.w;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void compare_pass1_k(const T* a, const T* b, size_t n, double* part) {
+  __shared__ double sh[4][3];
+  double ab = 0.0, aa = 0.0, bb = 0.0;
+  const size_t nv = n / 8, stride = (size_t)gridDim.x * blockDim.x;
+  const size_t t0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (size_t v = t0; v < nv; v += stride) {
+    float x[8], y[8];
+    load8f<T>(a + v * 8, x);
+    load8f<T>(b + v * 8, y);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ab = fma((double)x[e], (double)y[e], ab);
+      aa = fma((double)x[e], (double)x[e], aa);
+      bb = fma((double)y[e], (double)y[e], bb);
+    }
+  }
+  // ragged tail (n % 8 elements), thread 0 of block 0
+  if (t0 == 0)
+    for (size_t e = nv * 8; e < n; ++e) {
+      const double x = ldf(a, e), y = ldf(b, e);
+      ab = fma(x, y, ab); aa = fma(x, x, aa); bb = fma(y, y, bb);
+    }
+  double v3[3] = {ab, aa, bb};
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    double v = v3[k];
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0) sh[wv][k] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) part[(size_t)blockIdx.x * 3 + threadIdx.x] = sh[0][threadIdx.x] + sh[1][threadIdx.x] +
+                                                                     sh[2][threadIdx.x] + sh[3][threadIdx.x];
+}
+
+__global__ void compare_pass2_k(const double* part, int nblk, double* out) {
+  if (threadIdx.x < 3) {
+    double s = 0.0;
+    for (int b = 0; b < nblk; ++b) s += part[(size_t)b * 3 + threadIdx.x];
+    out[threadIdx.x] = s;
+  }
+}
+
+int grad_compare(const void* a, const void* b, size_t n, int dt, double* part, double* out_dev, hipStream_t s) {
+  if (!a || !b || n == 0) { set_error("grad_compare: empty or null vectors"); return 1; }
+  if ((((uintptr_t)a | (uintptr_t)b) & 15) != 0) { set_error("grad_compare: vectors must be 16-byte aligned"); return 1; }
+  const size_t nv = n / 8;
+  const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nv + 255) / 256, CMP_BLOCKS));
+  const int pi = prof_begin(PROF_COMPARE, s);
+  if (dt == BF16) hipLaunchKernelGGL(compare_pass1_k<uint16_t>, dim3(grid), dim3(256), 0, s, (const uint16_t*)a,
+                                     (const uint16_t*)b, n, part);
+  else hipLaunchKernelGGL(compare_pass1_k<float>, dim3(grid), dim3(256), 0, s, (const float*)a, (const float*)b, n, part);
+  prof_end(pi, s, 2.0 * (double)n * dsize(dt));
+  LAUNCH_OK("grad_compare_pass1");
+  hipLaunchKernelGGL(compare_pass2_k, dim3(1), dim3(64), 0, s, part, (int)grid, out_dev);
+  LAUNCH_OK("grad_compare_pass2");
+  return 0;
+}
+
+
+// ================================================================ GRPO window
+// Phase 2 (upstream gradients of the PPO-clipped GRPO loss through the
+// rectified-flow Euler step) fused with Phase 3 (composites), three launches:
+//   pass 1: per sample b and step j, sq[j][b] = |z_{j+1} - z_j - dt_j v_j|^2
+//           in fp64 (block partials, fixed order);
+//   coef:   log pi_j = -sq / (2 sigma_j^2) - n log(sqrt(2 pi) sigma_j),
+//           rho_j = exp(log pi_j - log pi_old_j), A = clamp(A_b, +-adv_clip),
+//           dL/drho = 0 if the clipped PPO term is strictly the larger, else
+//           -A / W, and coef[j][b] = dL/drho * rho_j * dt_j / sigma_j^2;
+//   pass 2: r_j = z_{j+1} - z_j - dt_j v_j (fp32) and either the composites
+//           s_base = sum_j (1 - alpha_j) coef_j r_j, s_corr = sum_j alpha_j
+//           coef_j r_j (one rounding on store) or the W gradients coef_j r_j.
+// s_j = coef_j r_j never reaches memory in the composite mode.  HBM traffic
+// per element: (2W + 1) reads in each pass, plus 2 (or W) writes.
+constexpr int GRPO_CH = 64;  // pass-1 blocks per sample
+size_t grpo_part_doubles(int W, int B) { return (size_t)GRPO_CH * W * B; }
+
+template <typename T>
+__device__ __forceinline__ size_t grpo_elem(const GrpoArgs& a, int b, size_t i) {
+  return i < a.len0 ? (size_t)b * a.len0 + i : a.split + (size_t)b * a.len1 + (i - a.len0);
+}
+
+template <typename T, int W>
+__global__ __launch_bounds__(256) void grpo_sq_k(GrpoArgs a, double* part) {
+  __shared__ double sh[4][W];
+  const int b = blockIdx.y;
+  const size_t per = (a.len0 + a.len1) / 8;  // vectors per sample
+  double acc[W];
+#pragma unroll
+  for (int j = 0; j < W; ++j) acc[j] = 0.0;
+  for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < per; v += (size_t)gridDim.x * blockDim.x) {
+    const size_t e = grpo_elem<T>(a, b, v * 8);
+    float zc[8];
+    load8f<T>((const T*)a.z[0] + e, zc);
+#pragma unroll
+    for (int j = 0; j < W; ++j) {
+      float zn[8], vv[8];
+      load8f<T>((const T*)a.z[j + 1] + e, zn);
+      load8f<T>((const T*)a.v[j] + e, vv);
+      const double dtj = a.dts[j];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const double r = ((double)zn[q] - (double)zc[q]) - dtj * (double)vv[q];
+        acc[j] = fma(r, r, acc[j]);
+        zc[q] = zn[q];
+      }
+    }
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < W; ++j) {
+    double x = acc[j];
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    if (lane == 0) sh[wv][j] = x;
+  }
+  __syncthreads();
+  if (threadIdx.x < W)
+    part[((size_t)threadIdx.x * a.B + b) * gridDim.x + blockIdx.x] =
+        sh[0][threadIdx.x] + sh[1][threadIdx.x] + sh[2][threadIdx.x] + sh[3][threadIdx.x];
+}
+
+__global__ void grpo_coef_k(GrpoArgs a, const double* part, int nblk, float* coef, double* stats) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;  // k = j * B + b
+  if (k >= a.W * a.B) return;
+  const int j = k / a.B, b = k % a.B;
+  double sq = 0.0;
+  for (int i = 0; i < nblk; ++i) sq += part[(size_t)k * nblk + i];
+  const double sg = a.sigma[j];
+  const double n = (double)(a.len0 + a.len1);
+  const double lp = -sq / (2.0 * sg * sg) - n * log(sqrt(2.0 * M_PI) * sg);
+  const double rho = exp(lp - a.logp_old[k]);
+  const double A = fmin(fmax((double)a.adv[b], -(double)a.adv_clip), (double)a.adv_clip);
+  const double unc = -A * rho;
+  const double clp = -A * fmin(fmax(rho, 1.0 - (double)a.eps), 1.0 + (double)a.eps);
+  const double dl = clp > unc ? 0.0 : -A / a.W;
+  coef[k] = (float)(dl * rho * a.dts[j] / (sg * sg));
+  if (stats) {
+    stats[3 * k] = lp;
+    stats[3 * k + 1] = rho;
+    stats[3 * k + 2] = fmax(unc, clp) / a.W;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store8f(T* p, const float* x) {
+  if constexpr (sizeof(T) == 2) {
+    uint4 u;
+    u.x = f2bf(x[0]) | ((uint32_t)f2bf(x[1]) << 16); u.y = f2bf(x[2]) | ((uint32_t)f2bf(x[3]) << 16);
+    u.z = f2bf(x[4]) | ((uint32_t)f2bf(x[5]) << 16); u.w = f2bf(x[6]) | ((uint32_t)f2bf(x[7]) << 16);
+    *(uint4*)p = u;
+  } else {
+    *(float4*)p = make_float4(x[0], x[1], x[2], x[3]);
+    *(float4*)(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
+  }
+}
+
+template <typename T, int W>
+__global__ __launch_bounds__(256) void grpo_out_k(GrpoArgs a, const float* coef) {
+  const size_t nv = a.n / 8;
+  for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < nv; v += (size_t)gridDim.x * blockDim.x) {
+    const size_t e = v * 8;
+    const int b = (int)(e < a.split ? e / a.len0 : (e - a.split) / a.len1);
+    float zc[8], sb[8], sc[8];
+    load8f<T>((const T*)a.z[0] + e, zc);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) sb[q] = sc[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < W; ++j) {
+      float zn[8], vv[8], sj[8];
+      load8f<T>((const T*)a.z[j + 1] + e, zn);
+      load8f<T>((const T*)a.v[j] + e, vv);
+      const float c = coef[j * a.B + b], dtj = (float)a.dts[j];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        sj[q] = c * ((zn[q] - zc[q]) - dtj * vv[q]);
+        zc[q] = zn[q];
+      }
+      if (a.mode == 1) {
+        store8f<T>((T*)a.s_out[j] + e, sj);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) { sb[q] = fmaf(a.wb[j], sj[q], sb[q]); sc[q] = fmaf(a.wc[j], sj[q], sc[q]); }
+      }
+    }
+    if (a.mode == 0) {
+      if (e < a.osplit) { store8f<T>((T*)a.base0 + e, sb); store8f<T>((T*)a.corr0 + e, sc); }
+      else { store8f<T>((T*)a.base1 + (e - a.osplit), sb); store8f<T>((T*)a.corr1 + (e - a.osplit), sc); }
+    }
+  }
+}
+
+template <typename T, int W>
+static void grpo_launch(const GrpoArgs& a, double* part, float* coef, double* stats, hipStream_t s) {
+  hipLaunchKernelGGL((grpo_sq_k<T, W>), dim3(GRPO_CH, a.B), dim3(256), 0, s, a, part);
+  hipLaunchKernelGGL(grpo_coef_k, dim3((a.W * a.B + 63) / 64), dim3(64), 0, s, a, part, GRPO_CH, coef, stats);
+  const size_t nv = a.n / 8;
+  const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nv + 255) / 256, 256 * 16));
+  hipLaunchKernelGGL((grpo_out_k<T, W>), dim3(grid), dim3(256), 0, s, a, coef);
+}
+
+int grpo_window(const GrpoArgs& a, double* part, float* coef, double* stats, hipStream_t s) {
+  if (a.W < 2 || a.W > GRPO_MAX_W || a.B < 1) { set_error("grpo_window: W must be 2..16, B >= 1"); return 1; }
+  if (a.len0 % 8 || a.len1 % 8 || a.split % 8 || a.osplit % 8 || a.len0 + a.len1 == 0) {
+    set_error("grpo_window: per-sample segments must be multiples of 8 elements");
+    return 4;
+  }
+  const int pi = prof_begin(PROF_UPSTREAM, s);
+#define GRPO_W(T, w) case w: grpo_launch<T, w>(a, part, coef, stats, s); break;
+  if (a.dt == BF16) {
+    switch (a.W) { GRPO_W(uint16_t, 2) GRPO_W(uint16_t, 3) GRPO_W(uint16_t, 4) GRPO_W(uint16_t, 5) GRPO_W(uint16_t, 6)
+                   GRPO_W(uint16_t, 7) GRPO_W(uint16_t, 8) GRPO_W(uint16_t, 10) GRPO_W(uint16_t, 12)
+                   GRPO_W(uint16_t, 16)
+      default: set_error("grpo_window: W must be one of 2..8, 10, 12, 16"); return 4; }
+  } else {
+    switch (a.W) { GRPO_W(float, 2) GRPO_W(float, 3) GRPO_W(float, 4) GRPO_W(float, 5) GRPO_W(float, 6)
+                   GRPO_W(float, 7) GRPO_W(float, 8) GRPO_W(float, 10) GRPO_W(float, 12) GRPO_W(float, 16)
+      default: set_error("grpo_window: W must be one of 2..8, 10, 12, 16"); return 4; }
+  }
+#undef GRPO_W
+  const double es = dsize(a.dt);
+  prof_end(pi, s, (double)a.n * es * (2.0 * (2 * a.W + 1) + (a.mode == 1 ? a.W : 2)));
+  LAUNCH_OK("grpo_window");
   return 0;
 }
 

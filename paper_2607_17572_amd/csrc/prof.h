@@ -13,6 +13,8 @@ enum ProfClass {
   PROF_ATTN_BWD_KV = 5,
   PROF_ATTN_BWD_Q = 6,
   PROF_AGGREGATE = 7,
+  PROF_COMPARE = 8,     // gradient-quality sums
+  PROF_UPSTREAM = 9,    // GRPO upstream gradients and their composites
 };
 
 // Returns a record index (>= 0) when class `cls` is being profiled, else -1.

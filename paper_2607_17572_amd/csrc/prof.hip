@@ -58,7 +58,7 @@ extern "C" {
 jagg_status jagg_prof_begin(int cls) {
   auto& p = jg::P();
   std::lock_guard<std::mutex> g(p.mu);
-  if (cls < jg::PROF_GEMM_FWD || cls > jg::PROF_AGGREGATE) {
+  if (cls < jg::PROF_GEMM_FWD || cls > jg::PROF_UPSTREAM) {
     jg::set_error("jagg_prof_begin: unknown kernel class");
     return JAGG_EINVAL;
   }

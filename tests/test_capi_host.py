@@ -124,3 +124,29 @@ def test_invalid_arguments_are_rejected_before_any_launch():
         assert L.jagg_linear_grad(h, 2, p16, p16, None, 8, 8, 8, p16, 7, 0.0) == 1       # unknown dtype
     finally:
         L.jagg_ctx_destroy(h)
+
+
+def test_variant_entry_points_reject_bad_arguments():
+    """Sequential-graph endpoint backward and gradient comparison: argument
+    errors are reported on the host before any launch."""
+    L = _lib_or_skip()
+    import ctypes
+    c = pk.config("tiny").c()
+    h = ctypes.c_void_p()
+    assert L.jagg_ctx_create(ctypes.byref(c), None, ctypes.byref(h)) == 0
+    try:
+        p = 4096
+        s2 = (ctypes.c_void_p * 2)(p, p)
+        t2 = (ctypes.c_float * 2)(1.0, 0.5)
+        # endpoint must be 0 or 1; beta 0 or 1; W >= 2 and t_0 != t_{W-1} (workspace checked after these)
+        assert L.jagg_endpoint_backward(h, p, p, 1, s2, t2, 2, 2, p, 0.0) == 1
+        assert L.jagg_endpoint_backward(h, p, p, 1, s2, t2, 2, 0, p, 0.5) == 1
+        assert L.jagg_endpoint_backward(h, p, p, 0, s2, t2, 2, 0, p, 0.0) == 1
+        assert L.jagg_endpoint_backward(h, p, None, 1, s2, t2, 2, 0, p, 0.0) == 1
+        out = (ctypes.c_double * 3)()
+        assert L.jagg_grad_compare(h, p, p, 0, 0, out) == 1          # empty
+        assert L.jagg_grad_compare(h, p, p + 4, 8, 0, out) == 1      # unaligned
+        assert L.jagg_grad_compare(h, p, p, 8, 5, out) == 1          # dtype
+        assert L.jagg_grad_compare(h, p, p, 8, 0, out) == 1          # no workspace bound
+    finally:
+        L.jagg_ctx_destroy(h)
