@@ -207,6 +207,10 @@ typedef struct {
   float clip_eps;           /* PPO clip range (0.1 in the paper's runs) */
   float adv_clip;           /* advantage clamp (5.0 in the paper's runs) */
   int W;                    /* 2..8, 10, 12 or 16 */
+  const int* v_batch;       /* host, W, or NULL: v_j holds samples v_index[j] .. v_index[j] + batch - 1 */
+  const int* v_index;       /* of a batch-v_batch[j] array in the model's output layout (e.g. the output of */
+                            /* the batch-2B endpoint-pair forward or of a batched no-grad middle forward); */
+                            /* NULL: every v_j is a batch-B array.  v_batch[j] <= 64. */
 } jagg_grpo_window;
 
 /* Phases 2 and 3 fused: the composites s_base, s_corr (Eq. s_base / s_corr with

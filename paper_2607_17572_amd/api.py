@@ -27,7 +27,8 @@ class _GrpoWindow(ctypes.Structure):
     _fields_ = [("v_hat", ctypes.POINTER(ctypes.c_void_p)), ("z", ctypes.POINTER(ctypes.c_void_p)),
                 ("t", ctypes.POINTER(ctypes.c_float)), ("sigma", ctypes.POINTER(ctypes.c_float)),
                 ("logp_old", ctypes.c_void_p), ("adv", ctypes.c_void_p), ("clip_eps", ctypes.c_float),
-                ("adv_clip", ctypes.c_float), ("W", ctypes.c_int)]
+                ("adv_clip", ctypes.c_float), ("W", ctypes.c_int), ("v_batch", ctypes.POINTER(ctypes.c_int)),
+                ("v_index", ctypes.POINTER(ctypes.c_int))]
 
 
 class _TensorDesc(ctypes.Structure):
@@ -302,14 +303,21 @@ class Context:
     @staticmethod
     def _grpo_window(v_list, z_list, t, sigma, logp_old, adv, clip_eps, adv_clip):
         """The C struct of one GRPO window; returns (struct, keep-alive list).
-        logp_old: device fp64 tensor [W][B]; adv: device fp32 tensor [B]."""
+        logp_old: device fp64 tensor [W][B]; adv: device fp32 tensor [B].
+        An entry of v_list may be (tensor, batch, index): samples index ..
+        index + B - 1 of a batch-``batch`` model output."""
         W = len(v_list)
         assert len(z_list) == W + 1 and len(t) == W + 1 and len(sigma) == W
-        vp, zp = _ptrs(v_list), _ptrs(z_list)
+        vt = [x[0] if isinstance(x, tuple) else x for x in v_list]
+        B = adv.numel()
+        vb = (ctypes.c_int * W)(*[x[1] if isinstance(x, tuple) else B for x in v_list])
+        vk = (ctypes.c_int * W)(*[x[2] if isinstance(x, tuple) else 0 for x in v_list])
+        vp, zp = _ptrs(vt), _ptrs(z_list)
         tt = (ctypes.c_float * (W + 1))(*[float(x) for x in t])
         sg = (ctypes.c_float * W)(*[float(x) for x in sigma])
-        w = _GrpoWindow(vp, zp, tt, sg, logp_old.data_ptr(), adv.data_ptr(), float(clip_eps), float(adv_clip), W)
-        return w, [vp, zp, tt, sg]
+        w = _GrpoWindow(vp, zp, tt, sg, logp_old.data_ptr(), adv.data_ptr(), float(clip_eps), float(adv_clip), W,
+                        vb, vk)
+        return w, [vp, zp, tt, sg, vb, vk]
 
     def grpo_composites(self, v_list, z_list, t, sigma, logp_old, adv, s_base, s_corr, clip_eps=0.1, adv_clip=5.0,
                         stats=None, batch=None):

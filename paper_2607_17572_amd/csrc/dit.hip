@@ -1027,6 +1027,10 @@ static jagg_status grpo_args(const jagg_ctx* ctx, const jagg_grpo_window* w, int
     a.dts[j] = (double)w->t[j + 1] - (double)w->t[j];
     a.sigma[j] = w->sigma[j];
     a.v[j] = w->v_hat[j];
+    a.vb[j] = w->v_batch ? w->v_batch[j] : batch;
+    a.vk[j] = w->v_index ? w->v_index[j] : 0;
+    if (a.vk[j] < 0 || a.vb[j] < batch || a.vk[j] + batch > a.vb[j] || a.vb[j] > 64)
+      return fail(JAGG_EINVAL, f + ": v_batch / v_index out of range");
   }
   for (int j = 0; j <= W; ++j) {
     if (!w->z[j] || (uintptr_t)w->z[j] % 16) return fail(JAGG_EINVAL, f + ": null or unaligned z_j");

@@ -133,6 +133,7 @@ int group_scores(const ScoreArgs& a, double* part, double* score_dev, hipStream_
 constexpr int GRPO_MAX_W = 16;
 struct GrpoArgs {
   const void* v[GRPO_MAX_W];      // model outputs v_j
+  int vb[GRPO_MAX_W], vk[GRPO_MAX_W];  // v_j: samples vk .. vk+B-1 of a batch-vb array
   const void* z[GRPO_MAX_W + 1];  // latents z_0 .. z_W
   int W, B, dt;
   size_t split, len0, len1, n;    // n = B * (len0 + len1)

@@ -1390,12 +1390,21 @@ int grad_compare(const void* a, const void* b, size_t n, int dt, double* part, d
 //           coef_j r_j (one rounding on store) or the W gradients coef_j r_j.
 // s_j = coef_j r_j never reaches memory in the composite mode.  HBM traffic
 // per element: (2W + 1) reads in each pass, plus 2 (or W) writes.
-constexpr int GRPO_CH = 64;  // pass-1 blocks per sample
-size_t grpo_part_doubles(int W, int B) { return (size_t)GRPO_CH * W * B; }
+// pass-1 blocks per sample: enough blocks in total to stream at full HBM
+// bandwidth, while the W x B x blocks partials stay within a fixed buffer
+constexpr int GRPO_PART_MAX = 32768;
+static int grpo_blocks(int W, int B) { return std::max(1, std::min(2048 / B + 1, GRPO_PART_MAX / (W * B))); }
+size_t grpo_part_doubles(int W, int B) { (void)W; (void)B; return GRPO_PART_MAX; }
 
 template <typename T>
 __device__ __forceinline__ size_t grpo_elem(const GrpoArgs& a, int b, size_t i) {
   return i < a.len0 ? (size_t)b * a.len0 + i : a.split + (size_t)b * a.len1 + (i - a.len0);
+}
+// element i of sample b inside v_j, which holds samples vk .. vk+B-1 of a
+// batch-vb array in the same layout (an endpoint pair, a batch of middle steps)
+__device__ __forceinline__ size_t grpo_velem(const GrpoArgs& a, int j, int b, size_t i) {
+  const size_t bb = (size_t)a.vk[j] + b;
+  return i < a.len0 ? bb * a.len0 + i : (size_t)a.vb[j] * a.len0 + bb * a.len1 + (i - a.len0);
 }
 
 template <typename T, int W>
@@ -1414,7 +1423,7 @@ __global__ __launch_bounds__(256) void grpo_sq_k(GrpoArgs a, double* part) {
     for (int j = 0; j < W; ++j) {
       float zn[8], vv[8];
       load8f<T>((const T*)a.z[j + 1] + e, zn);
-      load8f<T>((const T*)a.v[j] + e, vv);
+      load8f<T>((const T*)a.v[j] + grpo_velem(a, j, b, v * 8), vv);
       const double dtj = a.dts[j];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
@@ -1437,12 +1446,20 @@ __global__ __launch_bounds__(256) void grpo_sq_k(GrpoArgs a, double* part) {
         sh[0][threadIdx.x] + sh[1][threadIdx.x] + sh[2][threadIdx.x] + sh[3][threadIdx.x];
 }
 
-__global__ void grpo_coef_k(GrpoArgs a, const double* part, int nblk, float* coef, double* stats) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;  // k = j * B + b
-  if (k >= a.W * a.B) return;
+// one block per (j, b): the block partials summed in a fixed order (strided
+// per thread, then a fixed shuffle and LDS tree), then the closed-form scalars
+__global__ __launch_bounds__(256) void grpo_coef_k(GrpoArgs a, const double* part, int nblk, float* coef,
+                                                   double* stats) {
+  __shared__ double sh[4];
+  const int k = blockIdx.x;  // k = j * B + b
   const int j = k / a.B, b = k % a.B;
-  double sq = 0.0;
-  for (int i = 0; i < nblk; ++i) sq += part[(size_t)k * nblk + i];
+  double x = 0.0;
+  for (int i = threadIdx.x; i < nblk; i += blockDim.x) x += part[(size_t)k * nblk + i];
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  const double sq = (sh[0] + sh[1]) + (sh[2] + sh[3]);
   const double sg = a.sigma[j];
   const double n = (double)(a.len0 + a.len1);
   const double lp = -sq / (2.0 * sg * sg) - n * log(sqrt(2.0 * M_PI) * sg);
@@ -1478,6 +1495,7 @@ __global__ __launch_bounds__(256) void grpo_out_k(GrpoArgs a, const float* coef)
   for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < nv; v += (size_t)gridDim.x * blockDim.x) {
     const size_t e = v * 8;
     const int b = (int)(e < a.split ? e / a.len0 : (e - a.split) / a.len1);
+    const size_t i = e < a.split ? e - (size_t)b * a.len0 : a.len0 + (e - a.split) - (size_t)b * a.len1;
     float zc[8], sb[8], sc[8];
     load8f<T>((const T*)a.z[0] + e, zc);
 #pragma unroll
@@ -1486,7 +1504,7 @@ __global__ __launch_bounds__(256) void grpo_out_k(GrpoArgs a, const float* coef)
     for (int j = 0; j < W; ++j) {
       float zn[8], vv[8], sj[8];
       load8f<T>((const T*)a.z[j + 1] + e, zn);
-      load8f<T>((const T*)a.v[j] + e, vv);
+      load8f<T>((const T*)a.v[j] + grpo_velem(a, j, b, i), vv);
       const float c = coef[j * a.B + b], dtj = (float)a.dts[j];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
@@ -1509,8 +1527,9 @@ __global__ __launch_bounds__(256) void grpo_out_k(GrpoArgs a, const float* coef)
 
 template <typename T, int W>
 static void grpo_launch(const GrpoArgs& a, double* part, float* coef, double* stats, hipStream_t s) {
-  hipLaunchKernelGGL((grpo_sq_k<T, W>), dim3(GRPO_CH, a.B), dim3(256), 0, s, a, part);
-  hipLaunchKernelGGL(grpo_coef_k, dim3((a.W * a.B + 63) / 64), dim3(64), 0, s, a, part, GRPO_CH, coef, stats);
+  const int ch = grpo_blocks(a.W, a.B);
+  hipLaunchKernelGGL((grpo_sq_k<T, W>), dim3(ch, a.B), dim3(256), 0, s, a, part);
+  hipLaunchKernelGGL(grpo_coef_k, dim3(a.W * a.B), dim3(256), 0, s, a, part, ch, coef, stats);
   const size_t nv = a.n / 8;
   const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nv + 255) / 256, 256 * 16));
   hipLaunchKernelGGL((grpo_out_k<T, W>), dim3(grid), dim3(256), 0, s, a, coef);

@@ -162,3 +162,35 @@ def test_grpo_group_backward_matches_oracle():
     want = mmdit.flatten(cs.oc, jagg.g_jagg(cs.oc, P, cs.inputs, s_want, cs.t))
     eg, worst = compare_grads(cs, d, want, 1e-4)
     say(f"  GRPO JAGG group backward rel L2 {eg:.2e}")
+
+
+def batch_of(c: pk.Config, B: int, arrays):
+    """Several batch-B arrays in the output layout as one batch-(k B) array
+    (stream-major rows for a block-only model: all text rows, then all image rows)."""
+    if not c.block_only:
+        return torch.cat(arrays, 0)
+    nt = B * c.n_txt
+    return torch.cat([x[:nt] for x in arrays] + [x[nt:] for x in arrays], 0)
+
+
+@pytest.mark.parametrize("name", ["tiny", "block"])
+def test_grpo_reads_v_from_sub_batches(name):
+    """v_0 and v_{W-1} taken from one endpoint-pair output (batch 2B) and the
+    middle steps from one batch-(W-2)B output give the same bits as separate
+    batch-B arrays."""
+    c = {"tiny": TINY, "block": BLOCK_SMALL}[name]
+    say(f"case: GRPO sub-batch addressing {name}")
+    B = 2
+    w = Window(c, B)
+    ctx = pk.Context(c)
+    v, z, lpo, adv = w.dev()
+    sb0 = torch.empty(w.shape, dtype=w.dt, device="cuda")
+    sc0 = torch.empty_like(sb0)
+    ctx.grpo_composites(v, z, w.t, w.sigma, lpo, adv, sb0, sc0, EPS, ADV_CLIP)
+    pair = batch_of(c, B, [v[0], v[-1]])
+    mid = batch_of(c, B, v[1:-1])
+    vs = [(pair, 2 * B, 0)] + [(mid, (w.W - 2) * B, j * B) for j in range(w.W - 2)] + [(pair, 2 * B, B)]
+    sb1, sc1 = torch.empty_like(sb0), torch.empty_like(sb0)
+    ctx.grpo_composites(vs, z, w.t, w.sigma, lpo, adv, sb1, sc1, EPS, ADV_CLIP)
+    torch.cuda.synchronize()
+    assert torch.equal(sb0, sb1) and torch.equal(sc0, sc1)
