@@ -39,9 +39,9 @@ HBM_PEAK = 8.0e12
 
 # HBM traffic of the weight-gradient GEMM class per launch in the block
 # workload, from two rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by
-# the same counters on a 256 MiB device copy; valid only for the GEMM source
+# the same counters on a 1 GiB device copy; valid only for the GEMM source
 # it was measured on (sha256 of gemm.hip, first 16 hex digits).
-WGRAD_TRAFFIC = {"gemm_src": None, "bytes_per_launch": None}
+WGRAD_TRAFFIC = {"gemm_src": "63362442aa7b18cc", "bytes_per_launch": 704.14e6}
 
 
 def block_flops(D, F, N, B):
@@ -130,7 +130,8 @@ def main():
     ap.add_argument("--W", type=int, default=0, help="window size (default: 4 for block and slice, 8 for flux and qwen)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--calib-copy", action="store_true",
-                    help="first run a plain 256 MiB device copy (calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
+                    help="first run a plain 1 GiB device copy, larger than the 256 MB last-level cache "
+                         "(calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--only", choices=["all", "jagg"], default="all",
                     help="jagg: time the JAGG windows only (for a kernel trace of exactly those launches)")
     args = ap.parse_args()
@@ -144,8 +145,8 @@ def main():
 
     pk.lib()  # fails loudly if the HIP library is not built
     if args.calib_copy:
-        # a copy kernel of known size: reads and writes exactly 256 MiB
-        src = torch.ones(128 << 20, dtype=torch.bfloat16, device="cuda")
+        # a copy kernel of known size: reads and writes exactly 1 GiB
+        src = torch.ones(512 << 20, dtype=torch.bfloat16, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(3):
             dst.copy_(src)
