@@ -19,6 +19,9 @@ enum ProfClass {
 
 // Returns a record index (>= 0) when class `cls` is being profiled, else -1.
 int prof_begin(int cls, hipStream_t s);
+// True while a kernel class is armed (the library then runs on one stream so
+// that every timed kernel runs alone).
+bool prof_armed();
 // Closes record `idx` and attributes `work` (flops or bytes) to it.
 void prof_end(int idx, hipStream_t s, double work);
 

@@ -32,6 +32,8 @@ hipEvent_t take_event(Prof& p) {
 }
 }  // namespace
 
+bool prof_armed() { return P().cls != PROF_NONE; }
+
 int prof_begin(int cls, hipStream_t s) {
   Prof& p = P();
   if (p.cls == PROF_NONE || cls != p.cls) return -1;
