@@ -28,7 +28,17 @@ struct AttnBwd {
   void* dQ; void* dK; void* dV; int dt_d;
   int B, H, N, Dh, dt;
   RowMap rm;
+  // bf16 MFMA path: the dK/dV kernel stores dS^T here, [B*H][nk_pad][ld_ds]
+  // (key rows, query columns), and dQ = dS K is formed from it without
+  // recomputing the scores (nullptr: the dQ kernel recomputes them)
+  void* dS = nullptr;
+  int ld_ds = 0, nk_pad = 0;
 };
 int attention_bwd(const AttnBwd& a, hipStream_t s);
+// Padded dS^T geometry of the bf16 MFMA path: rows (keys) and columns
+// (queries) to multiples of 128 (the key block of the dK/dV kernel and the
+// query block of the dQ kernel).
+inline int attn_ds_rows(int N) { return (N + 127) / 128 * 128; }
+inline int attn_ds_ld(int N) { return (N + 127) / 128 * 128; }
 
 }  // namespace jg

@@ -638,6 +638,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const __amdgpu_buffer_rsrc_t RD = arsrc(a.delta + (size_t)bh * N, (long)N * 4);
   ATile at;
   at.init();
+  // this lane's dS^T row (padded rows beyond N are written too: finite values
+  // that multiply zero key rows in the dQ pass)
+  uint16_t* const dsr = a.dS ? (uint16_t*)a.dS + ((size_t)bh * a.nk_pad + key) * a.ld_ds : nullptr;
 
   bf16x8 kf[8], vf[8];
 #pragma unroll
@@ -732,6 +735,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         const bf16x8 pb = pack8(st, half), db = pack8(dpt, half);
+        if (dsr) {
+          // dS^T row of this lane's key: queries 16 half + 4h + 0..3 and
+          // 16 half + 8 + 4h + 0..3 of this 32-query half
+          const u32x4 u = __builtin_bit_cast(u32x4, db);
+          uint16_t* pr = dsr + q0 + 32 * t + 16 * half + 4 * h;
+          *(u32x2*)pr = u32x2{u[0], u[1]};
+          *(u32x2*)(pr + 8) = u32x2{u[2], u[3]};
+        }
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
           dv[dt] = mfma(tg[half][dt], pb, dv[dt]);
@@ -913,6 +924,98 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
 }
 
+// ------------------------------------------------------------ dQ from dS^T
+// dQ = dS K with dS^T as stored by the dK/dV kernel: 128 queries per
+// workgroup (32 per wave), 64-key tiles of K and of dS^T stream through four
+// LDS stages.  Per 16-key block c: the K^T fragments of the four 32-row head
+// dimension blocks and the wave's dS^T fragment are transposing LDS reads in
+// the same contraction-slot order; dQ^T += K^T dS^T.  No scores are
+// recomputed: the pass is bound by reading dS^T once.
+constexpr int Q3_QB = 128, Q3_KT = 64;
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_q3_k(AttnBwd a) {
+  __shared__ __attribute__((aligned(1024))) char K0[16384], S0[16384], K1[16384], S1[16384], K2[16384], S2[16384],
+      K3[16384], S3[16384];
+  const int bh = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
+  const int qb = blockIdx.x * Q3_QB;
+  const int q = qb + w * 32 + c32;
+  const int N = a.N;
+  const size_t base = (size_t)bh * N * DH;
+  const float sc = rsqrtf((float)DH);
+  const __amdgpu_buffer_rsrc_t RK = arsrc((const uint16_t*)a.K + base, (long)N * DH * 2);
+  const __amdgpu_buffer_rsrc_t RS =
+      arsrc((const uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds, (long)a.nk_pad * a.ld_ds * 2);
+  ATile at;
+  at.init();
+  f32x16 dq[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dq[i] = zero16();
+  auto load_tile = [&](char* Kd, char* Sd, int k0) {
+    at.load(RK, Kd, [&](int r) { return k0 + r < N ? (k0 + r) * (DH * 2) : -1; });
+    at.load(RS, Sd, [&](int r) { return ((k0 + r) * a.ld_ds + qb) * 2; });
+  };
+  // four stages, three tiles in flight (the pass streams dS^T from HBM)
+  const int ntile = (N + Q3_KT - 1) / Q3_KT;
+  load_tile(K0, S0, 0);
+  if (ntile > 1) load_tile(K1, S1, Q3_KT);
+  if (ntile > 2) load_tile(K2, S2, 2 * Q3_KT);
+  auto iter = [&](auto ic, int it) {
+    constexpr int c = decltype(ic)::value;
+    char* Kc = c == 0 ? K0 : (c == 1 ? K1 : (c == 2 ? K2 : K3));
+    char* Sc = c == 0 ? S0 : (c == 1 ? S1 : (c == 2 ? S2 : S3));
+    const int k0 = it * Q3_KT;
+    // tile it has landed once at most the loads of the later tiles in flight
+    // (8 direct loads per tile and wave) are outstanding
+    if (it + 2 < ntile) attn_barrier<16>();
+    else if (it + 1 < ntile) attn_barrier<8>();
+    else attn_barrier<0>();
+    // the stage of tile it+3 was last read in iteration it-1
+    if (it + 3 < ntile) {
+      if constexpr (c == 0) load_tile(K3, S3, k0 + 3 * Q3_KT);
+      else if constexpr (c == 1) load_tile(K0, S0, k0 + 3 * Q3_KT);
+      else if constexpr (c == 2) load_tile(K1, S1, k0 + 3 * Q3_KT);
+      else load_tile(K2, S2, k0 + 3 * Q3_KT);
+    }
+    bf16x8 tk[2][4], ts[2];
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) tk[0][dt] = at.tr(Kc, 0, dt);
+    ts[0] = at.tr(Sc, 0, w);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int cur = cb & 1, nxt = cur ^ 1;
+      if (cb + 1 < 4) {
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) tk[nxt][dt] = at.tr(Kc, cb + 1, dt);
+        ts[nxt] = at.tr(Sc, cb + 1, w);
+      }
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(tk[cur][dt], ts[cur], dq[dt]);
+    }
+  };
+  int it = 0;
+  for (; it + 3 < ntile; it += 4) {
+    iter(std::integral_constant<int, 0>(), it);
+    iter(std::integral_constant<int, 1>(), it + 1);
+    iter(std::integral_constant<int, 2>(), it + 2);
+    iter(std::integral_constant<int, 3>(), it + 3);
+  }
+  if (it < ntile) iter(std::integral_constant<int, 0>(), it);
+  if (it + 1 < ntile) iter(std::integral_constant<int, 1>(), it + 1);
+  if (it + 2 < ntile) iter(std::integral_constant<int, 2>(), it + 2);
+  __builtin_amdgcn_s_waitcnt(0);
+  if (q >= N) return;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(dq[dt][4 * g + i] * sc);
+      *(bf16x4*)((uint16_t*)a.dQ + base + (size_t)q * DH + 32 * dt + 8 * g + 4 * h) = v;
+    }
+}
+
 // ============================================================== dispatch
 static bool mfma_ok(int Dh, int dt, const void* O, int ld_o) {
   return Dh == DH && dt == BF16 && ((uintptr_t)O % 16 == 0) && (ld_o % 8 == 0);
@@ -936,13 +1039,19 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   const double nn = (double)a.B * a.H * a.N * (double)a.N * DH;
   // the direct-load kernels address dO with 32-bit byte offsets
   const bool v2 = (double)a.rm.rows() * a.ld_do * 2.0 < 2147483000.0 && (double)a.N * DH * 2.0 * 3 < 2147483000.0;
+  // stored dS^T: the geometry the kernels assume, and 32-bit offsets per head
+  const bool ds = a.dS && a.nk_pad == attn_ds_rows(a.N) && a.ld_ds == attn_ds_ld(a.N) &&
+                  (double)a.nk_pad * a.ld_ds * 2.0 < 2147483000.0 && (uintptr_t)a.dS % 16 == 0;
+  AttnBwd ak = a;
+  if (!ds) ak.dS = nullptr;
   int pi = prof_begin(PROF_ATTN_BWD_KV, s);
-  if (v2) hipLaunchKernelGGL(attn_bwd_kv2_k, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0, s, a);
+  if (v2) hipLaunchKernelGGL(attn_bwd_kv2_k, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0, s, ak);
   else hipLaunchKernelGGL(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0, s, a);
   prof_end(pi, s, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
   pi = prof_begin(PROF_ATTN_BWD_Q, s);
-  if (v2) hipLaunchKernelGGL(attn_bwd_q2_k, dim3((a.N + Q2_QB - 1) / Q2_QB, a.B * a.H), dim3(256), 0, s, a);
+  if (v2 && ds) hipLaunchKernelGGL(attn_bwd_q3_k, dim3((a.N + Q3_QB - 1) / Q3_QB, a.B * a.H), dim3(256), 0, s, a);
+  else if (v2) hipLaunchKernelGGL(attn_bwd_q2_k, dim3((a.N + Q2_QB - 1) / Q2_QB, a.B * a.H), dim3(256), 0, s, a);
   else hipLaunchKernelGGL(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0, s, a);
   prof_end(pi, s, 2.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_q_mfma");

@@ -242,6 +242,7 @@ struct Ws {
   void* dO = nullptr;
   void *dQh = nullptr, *dKh = nullptr, *dVh = nullptr;
   float* delta = nullptr;
+  void* dS = nullptr;  // dS^T of the attention backward (bf16 MFMA path)
   float *p1 = nullptr, *p2 = nullptr;
   float *p1b = nullptr, *p2b = nullptr;  // the text stream's partials while it runs on the side stream
   float* dmod[2] = {nullptr, nullptr};
@@ -284,6 +285,8 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   W.dKh = a.take(hn * m.Dh * es);
   W.dVh = a.take(hn * m.Dh * es);
   W.delta = a.f32(2 * hn);  // delta, then the log-sum-exp in log2 units
+  if (m.act == BF16 && m.Dh == 128)
+    W.dS = a.take((size_t)B * m.H * attn_ds_rows(m.N) * attn_ds_ld(m.N) * 2);
   W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, QK_PARTS * 2 * m.Dh + m.D, m.pd});
   const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   W.p1 = a.f32((size_t)nch * W.maxcols);
@@ -596,7 +599,8 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
     TRY(dgrad(c, dY, D, nr[s], cx.P(L.o.w), D, D, D, row(W.dO, r0[s], D), D, act));
   }
   TRY(join_side(cx));
-  AttnBwd ab{A.Qh, A.Kh, A.Vh, A.O, D, W.dO, D, A.lse, W.delta, W.dQh, W.dKh, W.dVh, act, B, m.H, m.N, m.Dh, act, rm};
+  AttnBwd ab{A.Qh, A.Kh, A.Vh, A.O, D, W.dO, D, A.lse, W.delta, W.dQh, W.dKh, W.dVh, act, B, m.H, m.N, m.Dh, act, rm,
+             W.dS, attn_ds_ld(m.N), attn_ds_rows(m.N)};
   TRY(attention_bwd(ab, cx.s));
   Gains gn{{cx.P(st[0].qg), cx.P(st[1].qg)}, {cx.P(st[0].kg), cx.P(st[1].kg)}};
   TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.qkv, 3 * D, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
@@ -646,7 +650,8 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   TRY(dgrad(cx, W.dY, D, R, cx.P(L.out.w), LC, D, D, W.dO, D, act));
   TRY(dgrad(cx, W.dY, D, R, (const char*)cx.P(L.out.w) + (size_t)D * es, LC, D, F, (char*)W.dbig + 3 * D * es, LD,
             act, EPI_GELU_BWD, (char*)A.proj + 3 * D * es, LD));
-  AttnBwd ab{A.Qh, A.Kh, A.Vh, A.cat, LC, W.dO, D, A.lse, W.delta, W.dQh, W.dKh, W.dVh, act, B, m.H, m.N, m.Dh, act, rm};
+  AttnBwd ab{A.Qh, A.Kh, A.Vh, A.cat, LC, W.dO, D, A.lse, W.delta, W.dQh, W.dKh, W.dVh, act, B, m.H, m.N, m.Dh, act, rm,
+             W.dS, attn_ds_ld(m.N), attn_ds_rows(m.N)};
   TRY(attention_bwd(ab, cx.s));
   Gains gn{{cx.P(L.qg), cx.P(L.qg)}, {cx.P(L.kg), cx.P(L.kg)}};
   TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.proj, LD, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
