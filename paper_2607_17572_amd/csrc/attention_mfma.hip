@@ -656,11 +656,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
   for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
 
+  // token q of sample b sits at row q + gofs_t (text, q < nt) or q + gofs_i
+  // (image) of dO: branch-free byte offsets (rows and row bytes < 2^24)
+  const int gofs_t = b * a.rm.nt, gofs_i = a.rm.B * a.rm.nt + b * a.rm.ni - a.rm.nt;
+  const int grow = a.ld_do * 2, gcol = hd * DH * 2;
   auto load_tile = [&](char* Qd, char* Gd, float* Ld, float* Dd, int q0) {
     at.load(RQ, Qd, [&](int r) { return (q0 + r) * (DH * 2); });
     at.load(RG, Gd, [&](int r) {
       const int q = q0 + r;
-      return q < N ? (row_of_tok_m(a.rm, b, q) * a.ld_do + hd * DH) * 2 : -1;
+      const int row = q + (q < a.rm.nt ? gofs_t : gofs_i);
+      return q < N ? __mul24(row, grow) + gcol : -1;
     });
     if (w == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(RL, ALDS(Ld), 4, (q0 + lane) * 4, 0, 0, 0);
     if (w == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(RD, ALDS(Dd), 4, (q0 + lane) * 4, 0, 0, 0);
