@@ -300,7 +300,11 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   W.dsh1 = a.f32((size_t)B * m.D);
   W.tmp = a.f32((size_t)B * m.D);
   W.tmp2 = a.f32((size_t)B * m.D);
-  const size_t slp = std::max(small_linear_bwd_part_floats(B, m.D, 6 * m.D), small_linear_bwd_part_floats(B, m.tf, m.D));
+  // partials of every small-linear backward with an input gradient: the
+  // modulations (D -> 6D or 3D or 2D) and the second time-MLP layer (D -> D)
+  const size_t slp = std::max({small_linear_bwd_part_floats(B, m.D, 6 * m.D), small_linear_bwd_part_floats(B, m.D, 3 * m.D),
+                               small_linear_bwd_part_floats(B, m.D, 2 * m.D), small_linear_bwd_part_floats(B, m.D, m.D),
+                               small_linear_bwd_part_floats(B, m.tf, m.D)});
   W.slpart = a.f32(slp);
   W.slpart2 = a.f32(slp);
   W.gact = a.take(rows * m.D * es);

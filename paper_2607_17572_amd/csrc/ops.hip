@@ -112,8 +112,18 @@ constexpr int SL_JT = 64;   // output rows per tile
 constexpr int SL_DT = 256;  // input columns per tile (one per thread)
 constexpr int SL_MAXB = 32;
 
+// Output rows per block of the vector kernel: enough blocks (~1024) to keep
+// every CU streaming W and dW, at most SL_JT; the input-gradient partials
+// grow with the block-row count.
+static int sl_rows(int Din, int Dout) {
+  const long cb = (Din + 1023) / 1024;
+  const long r = cb * Dout / 1024 / 8 * 8;
+  return (int)std::max<long>(8, std::min<long>(SL_JT, r));
+}
+
 size_t small_linear_bwd_part_floats(int B, int Din, int Dout) {
-  return (size_t)((Dout + SL_JT - 1) / SL_JT) * B * Din;
+  const int jt = std::min(SL_JT, sl_rows(Din, Dout));
+  return (size_t)((Dout + jt - 1) / jt) * B * Din;
 }
 
 template <typename TW, typename TG>
@@ -185,16 +195,16 @@ __global__ __launch_bounds__(128) void small_linear_bwd_vec_k(const float* __res
                                                               const float* __restrict__ in, int B, int Din,
                                                               const TW* __restrict__ W, int Dout, TG* __restrict__ dW,
                                                               TG* __restrict__ db, float beta,
-                                                              float* __restrict__ part) {
+                                                              float* __restrict__ part, int JT) {
   __shared__ float sd[BM][SL_JT];
-  const int jt = blockIdx.y, j0 = jt * SL_JT;
-  for (int i = threadIdx.x; i < BM * SL_JT; i += 128) {
-    const int b = i / SL_JT, jj = i % SL_JT;
+  const int jt = blockIdx.y, j0 = jt * JT;
+  for (int i = threadIdx.x; i < BM * JT; i += 128) {
+    const int b = i / JT, jj = i % JT;
     sd[b][jj] = (b < B && j0 + jj < Dout) ? dout[(size_t)b * Dout + j0 + jj] : 0.f;
   }
   __syncthreads();
   if (blockIdx.x == 0 && db) {
-    for (int jj = threadIdx.x; jj < SL_JT; jj += 128) {
+    for (int jj = threadIdx.x; jj < JT; jj += 128) {
       if (j0 + jj >= Dout) continue;
       float sacc = 0.f;
       for (int b = 0; b < B; ++b) sacc += sd[b][jj];
@@ -214,7 +224,7 @@ __global__ __launch_bounds__(128) void small_linear_bwd_vec_k(const float* __res
       acc[b][e] = 0.f;
     }
   }
-  const int jn = min(SL_JT, Dout - j0);
+  const int jn = min(JT, Dout - j0);
   // rows are independent apart from the input-gradient sums: unrolled so that
   // the loads of several rows are in flight together
 #pragma unroll 8
@@ -253,11 +263,12 @@ int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din
   if (act != 0 || B <= 0 || B > SL_MAXB) { set_error("small_linear_bwd: batch must be 1..32"); return 1; }
   const int njt = (Dout + SL_JT - 1) / SL_JT;
   if (B <= 4 && Din % 8 == 0 && al16(in) && al16(W) && al16(dW) && (!din || al16(part))) {
-    dim3 grid((Din + 1023) / 1024, njt);
+    const int jt = sl_rows(Din, Dout), njv = (Dout + jt - 1) / jt;
+    dim3 grid((Din + 1023) / 1024, njv);
     float* p = din ? part : nullptr;
 #define SLV(TW, TG) \
   hipLaunchKernelGGL((small_linear_bwd_vec_k<TW, TG, 4>), grid, dim3(128), 0, s, dout, in, B, Din, (const TW*)W, Dout, \
-                     (TG*)dW, (TG*)db, beta, p)
+                     (TG*)dW, (TG*)db, beta, p, jt)
     if (w_dt == BF16 && g_dt == BF16) SLV(uint16_t, uint16_t);
     else if (w_dt == BF16) SLV(uint16_t, float);
     else if (g_dt == BF16) SLV(float, uint16_t);
@@ -266,7 +277,7 @@ int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din
     LAUNCH_OK("small_linear_bwd_vec");
     if (din) {
       const size_t n = (size_t)B * Din;
-      hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njt, n, din);
+      hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njv, n, din);
       LAUNCH_OK("small_linear_bwd_sum");
     }
     return 0;

@@ -129,6 +129,26 @@ def test_determinism_bitwise():
     assert torch.equal(a, b)
 
 
+def test_two_stream_schedule_equals_single_stream_bitwise():
+    """The double block's text-stream chain runs on a side stream; while a
+    kernel class is timed the library runs on one stream.  Both schedules
+    must give the same bits (disjoint buffers, fixed-order join)."""
+    say("case: two-stream vs single-stream schedule, bf16 block hidden 512, B=2")
+    cs = Case(BLOCK_MID, B=2, W=4)
+    sv = cs.saved_pair()
+    a = cs.new_grad()
+    cs.ctx.group_backward(cs.theta_dev, sv, cs.B, cs.s_dev, cs.t, a)
+    torch.cuda.synchronize()
+    b = cs.new_grad()
+    pk.prof_begin(pk.PROF_AGGREGATE)  # arms timing: one stream
+    try:
+        cs.ctx.group_backward(cs.theta_dev, sv, cs.B, cs.s_dev, cs.t, b)
+    finally:
+        pk.prof_end()
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
 # ------------------------------------------------------------ aggregation
 @pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("n,W", [(1, 4), (77, 4), (4096, 2), (100003, 5), (262144, 8)])
