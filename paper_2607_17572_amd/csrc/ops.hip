@@ -94,9 +94,62 @@ __global__ __launch_bounds__(256) void small_linear_fwd_k(const float* __restric
   }
 }
 
+// Wide rows (Din a multiple of 512): two output rows per wave, each lane
+// reads 8 consecutive weights per 16-byte load (a wave streams 1 KB of W per
+// instruction), the batch's inputs are read as 8-float vectors from cache.
+template <typename TW>
+__global__ __launch_bounds__(256) void small_linear_fwd_vec_k(const float* __restrict__ in, int B, int Din,
+                                                              const TW* __restrict__ W, const TW* __restrict__ bias,
+                                                              float* __restrict__ out, int Dout) {
+  const int lane = threadIdx.x & 63;
+  const int j0 = blockIdx.x * 8 + 2 * (threadIdx.x >> 6);
+  if (j0 >= Dout) return;
+  const bool two = j0 + 1 < Dout;
+  const TW* w0 = W + (size_t)j0 * Din;
+  const TW* w1 = W + (size_t)(two ? j0 + 1 : j0) * Din;
+  for (int b0 = 0; b0 < B; b0 += 4) {
+    float acc[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
+    for (int d = 8 * lane; d < Din; d += 512) {
+      float a[8], c[8];
+      ld8f(w0 + d, a);
+      ld8f(w1 + d, c);
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) {
+        if (b0 + bb >= B) break;
+        float x[8];
+        ld8f(in + (size_t)(b0 + bb) * Din + d, x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          acc[0][bb] = fmaf(a[e], x[e], acc[0][bb]);
+          acc[1][bb] = fmaf(c[e], x[e], acc[1][bb]);
+        }
+      }
+    }
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb) {
+      const float s0 = wave_sum(acc[0][bb]), s1 = wave_sum(acc[1][bb]);
+      if (lane == 0 && b0 + bb < B) {
+        out[(size_t)(b0 + bb) * Dout + j0] = s0 + (bias ? ldf(bias, j0) : 0.f);
+        if (two) out[(size_t)(b0 + bb) * Dout + j0 + 1] = s1 + (bias ? ldf(bias, j0 + 1) : 0.f);
+      }
+    }
+  }
+}
+
 int small_linear_fwd(const float* in, int act, int B, int Din, const void* W, const void* bias, int w_dt,
                      float* out, int Dout, hipStream_t s) {
   if (act != 0 || B <= 0 || B > 64) { set_error("small_linear_fwd: bad batch/act"); return 1; }
+  if (Din % 512 == 0 && al16(in) && al16(W)) {
+    dim3 grid((Dout + 7) / 8);
+    if (w_dt == BF16)
+      hipLaunchKernelGGL(small_linear_fwd_vec_k<uint16_t>, grid, dim3(256), 0, s, in, B, Din, (const uint16_t*)W,
+                         (const uint16_t*)bias, out, Dout);
+    else
+      hipLaunchKernelGGL(small_linear_fwd_vec_k<float>, grid, dim3(256), 0, s, in, B, Din, (const float*)W,
+                         (const float*)bias, out, Dout);
+    LAUNCH_OK("small_linear_fwd_vec");
+    return 0;
+  }
   dim3 grid((Dout + 3) / 4);
   if (w_dt == BF16)
     hipLaunchKernelGGL(small_linear_fwd_k<uint16_t>, grid, dim3(256), 0, s, in, B, Din, (const uint16_t*)W,
