@@ -2,7 +2,8 @@
 Euler step and the PPO-clipped loss) and of its fusion with the composites,
 against oracle.grpo on the same bf16/fp32-rounded inputs.  Clip decisions
 (which steps get a zero gradient) must match exactly: both sides take them in
-fp64.  log pi_j: relative 1e-12, rho_j: 1e-9, loss: 1e-9; s_j and the
+fp64.  log pi_j: relative 1e-12, rho_j and loss: 1e-12 x |log pi_j| (at least
+1e-9, see check_stats); s_j and the
 composites: relative L2 1e-6 (fp32), 8e-3 (bf16, one rounding on store)."""
 import sys
 
@@ -101,10 +102,15 @@ class Window:
 
 
 def check_stats(got, want):
+    """log pi to 1e-12 relative (fp64 sums in a different order); rho = exp(log pi -
+    log pi_old) then carries the ABSOLUTE error of log pi as its relative error:
+    1e-12 x |log pi| (~1e-4 for a 14M-element sample, whose |log pi| ~ 1e8),
+    at least 1e-9; the loss is -A rho / W or a constant."""
     got = got.cpu().numpy()
     assert np.allclose(got[..., 0], want[..., 0], rtol=1e-12, atol=0)
-    assert np.allclose(got[..., 1], want[..., 1], rtol=1e-9, atol=0)
-    assert np.allclose(got[..., 2], want[..., 2], rtol=1e-9, atol=1e-15)
+    rt = max(1e-9, 1e-12 * float(np.max(np.abs(want[..., 0]))))
+    assert np.allclose(got[..., 1], want[..., 1], rtol=rt, atol=0)
+    assert np.allclose(got[..., 2], want[..., 2], rtol=rt, atol=1e-15)
 
 
 @pytest.mark.parametrize("name,B", [("tiny", 2), ("block", 2), ("full", 1)])
