@@ -150,3 +150,48 @@ def test_variant_entry_points_reject_bad_arguments():
         assert L.jagg_grad_compare(h, p, p, 8, 0, out) == 1          # no workspace bound
     finally:
         L.jagg_ctx_destroy(h)
+
+
+def test_grpo_entry_points_reject_bad_arguments():
+    """GRPO Phase-2 calls: window and argument errors are caught on the host."""
+    L = _lib_or_skip()
+    import ctypes
+    from paper_2607_17572_amd.api import _GrpoWindow
+    c = pk.config("tiny").c()
+    h = ctypes.c_void_p()
+    assert L.jagg_ctx_create(ctypes.byref(c), None, ctypes.byref(h)) == 0
+    try:
+        p = 4096
+        W = 4
+        v = (ctypes.c_void_p * W)(*[p] * W)
+        z = (ctypes.c_void_p * (W + 1))(*[p] * (W + 1))
+        t = (ctypes.c_float * (W + 1))(1.0, 0.9, 0.8, 0.7, 0.6)
+        sg = (ctypes.c_float * W)(0.3, 0.3, 0.3, 0.3)
+
+        def win(**kw):
+            d = dict(v_hat=v, z=z, t=t, sigma=sg, logp_old=p, adv=p, clip_eps=0.1, adv_clip=5.0, W=W,
+                     v_batch=None, v_index=None)
+            d.update(kw)
+            return _GrpoWindow(**d)
+
+        out = (ctypes.c_void_p * W)(*[p] * W)
+        ok = win()
+        assert L.jagg_grpo_composites(h, ctypes.byref(ok), 0, p, p, None) == 1          # batch 0
+        assert L.jagg_grpo_composites(h, ctypes.byref(ok), 17, p, p, None) == 1         # batch > 16
+        assert L.jagg_grpo_composites(h, ctypes.byref(win(W=1)), 1, p, p, None) == 1   # W < 2
+        assert L.jagg_grpo_composites(h, ctypes.byref(win(W=17)), 1, p, p, None) == 1  # W > 16
+        bad_sg = (ctypes.c_float * W)(0.3, 0.0, 0.3, 0.3)
+        assert L.jagg_grpo_composites(h, ctypes.byref(win(sigma=bad_sg)), 1, p, p, None) == 1  # sigma <= 0
+        flat = (ctypes.c_float * (W + 1))(0.5, 0.4, 0.3, 0.5, 0.2)
+        assert L.jagg_grpo_composites(h, ctypes.byref(win(t=flat)), 1, p, p, None) == 1  # t_0 == t_{W-1}
+        assert L.jagg_grpo_composites(h, ctypes.byref(win(logp_old=None)), 1, p, p, None) == 1
+        assert L.jagg_grpo_composites(h, ctypes.byref(win(adv_clip=0.0)), 1, p, p, None) == 1
+        vb = (ctypes.c_int * W)(2, 2, 2, 2)
+        vk = (ctypes.c_int * W)(0, 1, 2, 0)  # index 2 of a batch-2 output: out of range
+        assert L.jagg_grpo_composites(h, ctypes.byref(win(v_batch=vb, v_index=vk)), 1, p, p, None) == 1
+        unal = (ctypes.c_void_p * W)(p, p + 4, p, p)
+        assert L.jagg_grpo_upstream(h, ctypes.byref(ok), 1, unal, None) == 1           # unaligned s_j
+        assert L.jagg_grpo_group_backward(h, p, p, 1, ctypes.byref(ok), p, 0.5, None) == 1  # beta
+        assert L.jagg_grpo_composites(h, ctypes.byref(ok), 1, p, p, None) == 1          # no workspace
+    finally:
+        L.jagg_ctx_destroy(h)
