@@ -637,8 +637,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
 }
 
 // --------------------------------------------- direct-to-LDS MFMA GEMM
-// BM x BN workgroup tile (each 192 or 256), 4 waves (2 x 2), 32-deep k tiles
-// through 4 LDS stages, for K a multiple of 32.  Operands go from memory
+// BM x BN workgroup tile (each 192 or 256), WM x WN waves (2 x 2; 2 x 4 for
+// 256 x 256, where a second wave per SIMD keeps the MFMAs busy while the other
+// wave stalls issuing its direct loads: 8% faster on that tile, while 4 x 2
+// on 256 x 192 was slower than 2 x 2), 32-deep k tiles through 4 LDS stages,
+// for K a multiple of 32.  Operands go from memory
 // straight into LDS (buffer loads with the LDS bit: no register staging and no
 // LDS write instructions), three k tiles ahead of the MFMAs.  LDS rows are
 // unpadded and 16-byte chunks are XOR-swizzled by row so that both the 1 KB
@@ -659,18 +662,16 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
 // kernels above.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 #define JG_LDS(p) ((__attribute__((address_space(3))) void*)(p))
-// Workgroup barrier for the direct-loaded stages: this wave's LDS reads done
-// (lgkmcnt 0) and at most NV direct loads still in flight (the loads of the
-// two newest k tiles), then s_barrier.  Unlike __syncthreads there is no
-// release fence, which would wait for every direct load (they are LDS writes)
-// and drain the prefetch; the empty asm statements keep the compiler from
-// moving memory accesses across it.
+// First half of the workgroup barrier for the direct-loaded stages: this
+// wave's LDS reads done (lgkmcnt 0) and at most NV of its direct loads still
+// in flight (the loads of the two newest k tiles); s_barrier follows.  Unlike
+// __syncthreads there is no release fence, which would wait for every direct
+// load (they are LDS writes) and drain the prefetch; the empty asm statements
+// keep the compiler from moving memory accesses across it.
 template <int NV>
-__device__ __forceinline__ void lds_barrier_vm() {
+__device__ __forceinline__ void wait_vm_lds() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt((NV & 15) | ((NV >> 4) << 14) | 0x70);  // vmcnt(NV) expcnt(7) lgkmcnt(0)
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 __device__ __forceinline__ int swz_n(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
@@ -680,13 +681,18 @@ __device__ __forceinline__ int swz_t(int k) {
 }
 
 // One operand of the direct-to-LDS kernel: ROWS x 32 elements = ROWS * 64 B per
-// k tile, NL = ROWS / 64 direct loads of 1 KB per wave.
-template <bool T, int ROWS>
+// k tile = NB direct loads of 1 KB, NL of them by each of the first NLW of the
+// NW waves (the other waves load none of this operand); a wave's MFMAs read WR
+// of the ROWS rows.
+template <bool T, int ROWS, int NW, int WR>
 struct DtlOp {
-  static constexpr int NL = ROWS / 64;
+  static constexpr int NB = ROWS / 16;
+  static constexpr int NL = (NB + NW - 1) / NW;
+  static constexpr int NLW = NB / NL;
+  static_assert(NB % NL == 0, "the loads of a k tile must split evenly over the loading waves");
   static constexpr int RB = ROWS * 2;   // bytes per k row (k-strided layout)
   static constexpr int CPR = ROWS / 8;  // chunks per k row
-  static constexpr int FR = ROWS / 64;  // 32-row fragments per wave (2 waves share the rows)
+  static constexpr int FR = WR / 32;    // 32-row fragments per wave
   int voff[NL];  // per load: byte offset at k = 0
   int kmul;      // bytes per unit of k
   int fo[FR > 2 ? FR : 2];  // fragment read offsets (bytes)
@@ -718,9 +724,12 @@ struct DtlOp {
       }
     }
   }
+  // does this wave load any of the operand (wave-uniform)
+  __device__ static inline bool loads(int wave) { return NLW == NW || wave < NLW; }
   // direct loads of the k tile at k0 into the stage at S (byte pointer)
   __device__ inline void load(__amdgpu_buffer_rsrc_t R, char* S, int k0) const {
     const int wave = threadIdx.x >> 6;
+    if (!loads(wave)) return;
 #pragma unroll
     for (int t = 0; t < NL; ++t)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(R, JG_LDS(S + (wave * NL + t) * 1024), 16, voff[t] + k0 * kmul, 0, 0, 0);
@@ -750,15 +759,15 @@ struct DtlOp {
 // global load its epilogue kind needs (old C, GELU input, bias) is issued
 // before the first use, so the load latency is paid once per row of tiles
 // instead of once per 32x32 tile.  Edge tiles take the checked path.
-template <int BM, int BN, int EK>
-__device__ __forceinline__ void dtl_epilogue(const GemmArgs& g, f32x16 (&acc)[BM / 64][BN / 64], int m0, int n0,
-                                             float* T) {
-  constexpr int FM = BM / 64, FN = BN / 64, ES = 36, TS = 32 * ES;
+template <int BM, int BN, int WM, int WN, int EK>
+__device__ __forceinline__ void dtl_epilogue(const GemmArgs& g, f32x16 (&acc)[BM / (32 * WM)][BN / (32 * WN)],
+                                             int m0, int n0, float* T) {
+  constexpr int FM = BM / (32 * WM), FN = BN / (32 * WN), ES = 36, TS = 32 * ES;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / 2, wn = wave % 2;
+  const int wm = wave / WN, wn = wave % WN;
   const int h = lane >> 5, c32 = lane & 31;
   const int rr = lane & 31, cc = (lane >> 5) * 16;  // read-back: row rr, columns cc .. cc+15
-  const int rbase = m0 + wm * (BM / 2), cbase = n0 + wn * (BN / 2);
+  const int rbase = m0 + wm * (BM / WM), cbase = n0 + wn * (BN / WN);
   const bool vec_ok = (g.N % 8 == 0) && (g.epi.ldc % 8 == 0);
   const bool inner = vec_ok && m0 + BM <= g.M && n0 + BN <= g.N;
   const Epi& e = g.epi;
@@ -858,9 +867,9 @@ __device__ __forceinline__ void dtl_epilogue(const GemmArgs& g, f32x16 (&acc)[BM
   }
 }
 
-template <bool TA, bool TB, int EK, int BM, int BN>
-__global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
-  constexpr int BK = 32, WM = 2, WN = 2, FM = BM / 64, FN = BN / 64;
+template <bool TA, bool TB, int EK, int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_dtl_kernel(GemmArgs g) {
+  constexpr int BK = 32, NW = WM * WN, FM = BM / (32 * WM), FN = BN / (32 * WN);
   constexpr int SB = BM * 64;  // byte offset of the B tile in a stage
   constexpr int STG = 32768;   // bytes per stage (room for 256 + 256 rows)
   // one variable per stage: every LDS access names its stage statically, so
@@ -878,10 +887,12 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
   const int wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
 
-  DtlOp<TA, BM> oa;
-  DtlOp<TB, BN> ob;
-  oa.init(g.lda, m0, wm * (BM / 2));
-  ob.init(g.ldb, n0, wn * (BN / 2));
+  typedef DtlOp<TA, BM, NW, BM / WM> OpA;
+  typedef DtlOp<TB, BN, NW, BN / WN> OpB;
+  OpA oa;
+  OpB ob;
+  oa.init(g.lda, m0, wm * (BM / WM));
+  ob.init(g.ldb, n0, wn * (BN / WN));
   const long ext_a = TA ? ((long)(g.K - 1) * g.lda + g.M) * 2 : ((long)(g.M - 1) * g.lda + g.K) * 2;
   const long ext_b = TB ? ((long)(g.K - 1) * g.ldb + g.N) * 2 : ((long)(g.N - 1) * g.ldb + g.K) * 2;
   const __amdgpu_buffer_rsrc_t RA = make_rsrc(g.A, ext_a), RB = make_rsrc(g.B, ext_b);
@@ -921,12 +932,24 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
   };
 
   // prologue: tiles 0, 1, 2 in flight; wait for tile 0
-  constexpr int NL = DtlOp<TA, BM>::NL + DtlOp<TB, BN>::NL;  // direct loads per wave per k tile
+  constexpr int NL = OpA::NL + OpB::NL;  // direct loads per (fully loading) wave per k tile
+  // Wait until at most two k tiles of this wave's own direct loads are in
+  // flight, then meet the other waves: the waves that load only one operand
+  // (or none) wait for fewer.
+  const bool lda_w = OpA::loads(wave), ldb_w = OpB::loads(wave);
+  auto tile_barrier = [&]() {
+    if (lda_w && ldb_w) wait_vm_lds<2 * NL>();
+    else if (lda_w) wait_vm_lds<2 * OpA::NL>();
+    else if (ldb_w) wait_vm_lds<2 * OpB::NL>();
+    else wait_vm_lds<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
   const int nk = g.K / BK;
   load_tile(st0, 0);
   load_tile(st1, 1);
   load_tile(st2, 2);
-  lds_barrier_vm<2 * NL>();  // tiles 1 and 2 may still fly
+  tile_barrier();  // tiles 1 and 2 may still fly
   ldfrag(st0, 0, 0);
 
   constexpr int RD = (TA ? 2 : 1) * FM + (TB ? 2 : 1) * FN;  // LDS reads per k16 step
@@ -943,7 +966,7 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
     pipe_sched<FM * FN, RD, 0, NL>();
     __builtin_amdgcn_sched_barrier(0);
     // tile kt+1 has landed once at most the loads of tiles kt+2, kt+3 fly
-    lds_barrier_vm<2 * NL>();
+    tile_barrier();
     // step 1, hiding the first fragment reads of tile kt+1
     ldfrag(Sn, 0, 0);
     mfma_step(1);
@@ -964,8 +987,12 @@ __global__ __launch_bounds__(256) void gemm_dtl_kernel(GemmArgs g) {
   // read before the stages are reused as per-wave epilogue staging
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  float* T = (float*)(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
-  dtl_epilogue<BM, BN, EK>(g, acc, m0, n0, T);
+  // per-wave staging: FN 32 x 36 fp32 tiles (at most 18 KB), NW / 4 waves per stage
+  constexpr int TQ = NW / 4, TB_ = STG / TQ;
+  static_assert(FN * 32 * 36 * 4 <= TB_, "epilogue staging exceeds its share of a stage");
+  const int ws = wave / TQ;
+  float* T = (float*)((ws == 0 ? st0 : ws == 1 ? st1 : ws == 2 ? st2 : st3) + (wave % TQ) * TB_);
+  dtl_epilogue<BM, BN, WM, WN, EK>(g, acc, m0, n0, T);
 }
 
 // ---------------------------------------------------------------- VALU GEMM
@@ -1040,17 +1067,17 @@ static int launch_mfma(const GemmArgs& g, hipStream_t s) {
 static int g_tile_cfg = 0;
 void gemm_set_tile_cfg(int c) { g_tile_cfg = c; }
 
-template <bool TA, bool TB, int EK, int BM, int BN>
+template <bool TA, bool TB, int EK, int BM, int BN, int WM = 2, int WN = 2>
 static int launch_dtl(const GemmArgs& g, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_dtl_kernel<TA, TB, EK, BM, BN>), dim3(tiles), dim3(256), 0, s, g);
+  hipLaunchKernelGGL((gemm_dtl_kernel<TA, TB, EK, BM, BN, WM, WN>), dim3(tiles), dim3(64 * WM * WN), 0, s, g);
   JG_CHECK_LAUNCH("gemm_dtl");
   return 0;
 }
 
 // Tile shape of the direct-to-LDS kernel: the one with the least estimated
 // time = whole rounds of 256 workgroups x tile area / relative tile efficiency
-// (smaller tiles re-read more operand bytes per MFMA).  0: 256x256,
+// (smaller tiles re-read more operand bytes per MFMA).  0: 256x256 (8 waves),
 // 1: 256x192, 2: 192x256, 3: 192x192.
 static int dtl_shape(int M, int N) {
   static const int bm[4] = {256, 256, 192, 192}, bn[4] = {256, 192, 256, 192};
@@ -1074,7 +1101,7 @@ struct DtlLaunch {
       case 1: return launch_dtl<TA, TB, EK, 256, 192>(g, s);
       case 2: return launch_dtl<TA, TB, EK, 192, 256>(g, s);
       case 3: return launch_dtl<TA, TB, EK, 192, 192>(g, s);
-      default: return launch_dtl<TA, TB, EK, 256, 256>(g, s);
+      default: return launch_dtl<TA, TB, EK, 256, 256, 2, 4>(g, s);
     }
   }
 };
@@ -1203,10 +1230,10 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
 // (the host-side launch stubs of kernel templates reached only through the
 // shape switch are otherwise not always emitted).
 #define JG_DTL_SHAPES(TA, EK)                                            \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 256>(GemmArgs); \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 192>(GemmArgs); \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 256>(GemmArgs); \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 192>(GemmArgs);
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 256, 2, 4>(GemmArgs); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 192, 2, 2>(GemmArgs); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 256, 2, 2>(GemmArgs); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 192, 2, 2>(GemmArgs);
 #define JG_DTL_KINDS(TA) \
   JG_DTL_SHAPES(TA, 0) JG_DTL_SHAPES(TA, 1) JG_DTL_SHAPES(TA, 2) JG_DTL_SHAPES(TA, 3) JG_DTL_SHAPES(TA, 4) \
   JG_DTL_SHAPES(TA, 5) JG_DTL_SHAPES(TA, 6)
