@@ -946,6 +946,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dtl_kernel(GemmArgs g) {
     asm volatile("" ::: "memory");
   };
   const int nk = g.K / BK;
+  // Every wave loads both operands: A's loads of a k tile go with the first
+  // MFMA step, B's with the second.  A wave stalls while the memory pipeline
+  // cannot take its next direct load, and with one wave per SIMD the MFMAs
+  // stall with it; spread over both steps, the loads cost 3-4% less time in
+  // the weight-gradient products.
+  constexpr bool SPLIT = OpA::NLW == NW && OpB::NLW == NW;
   load_tile(st0, 0);
   load_tile(st1, 1);
   load_tile(st2, 2);
@@ -959,18 +965,29 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dtl_kernel(GemmArgs g) {
     const char* S = stage(std::integral_constant<int, c>());
     const char* Sn = stage(std::integral_constant<int, c + 1>());
     // step 0: fragments of step 1 and the direct loads of tile kt+3 (its stage
-    // was last read before the previous barrier)
+    // was last read before the previous barrier): all of them, or with SPLIT
+    // only A's, B's following in step 1
     ldfrag(S, 1, 1);
-    load_tile(stage(std::integral_constant<int, c + 3>()), kt + 3);
+    char* Sx = stage(std::integral_constant<int, c + 3>());
+    if constexpr (SPLIT) oa.load(RA, Sx, (kt + 3) * BK);
+    else load_tile(Sx, kt + 3);
     mfma_step(0);
-    pipe_sched<FM * FN, RD, 0, NL>();
+    pipe_sched<FM * FN, RD, 0, SPLIT ? OpA::NL : NL>();
     __builtin_amdgcn_sched_barrier(0);
-    // tile kt+1 has landed once at most the loads of tiles kt+2, kt+3 fly
-    tile_barrier();
+    // tile kt+1 has landed once at most the loads of tile kt+2 and those of
+    // tile kt+3 issued so far fly
+    if constexpr (SPLIT) {
+      wait_vm_lds<NL + OpA::NL>();
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    } else {
+      tile_barrier();
+    }
     // step 1, hiding the first fragment reads of tile kt+1
     ldfrag(Sn, 0, 0);
+    if constexpr (SPLIT) ob.load(RB, Sx + SB, (kt + 3) * BK);
     mfma_step(1);
-    pipe_sched<FM * FN, RD, 0, 0>();
+    pipe_sched<FM * FN, RD, 0, SPLIT ? OpB::NL : 0>();
     __builtin_amdgcn_sched_barrier(0);
   };
   int kt = 0;
