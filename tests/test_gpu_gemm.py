@@ -44,8 +44,12 @@ def operands(rows, n_out, n_in, seed):
     return dY, X, W, C0
 
 
-# ragged in every dimension, several tiles, K not a multiple of the k tile
-SHAPES = [(37, 20, 12), (8, 8, 8), (200, 136, 72), (1000, 520, 776), (1032, 3072, 264), (520, 1048, 3080)]
+# ragged in every dimension, several tiles, K not a multiple of the k tile;
+# the last shape gives both products 16 x 16 tiles of 256 x 256 (one round of
+# 256 CUs, against two rounds of the smaller tiles), so they run the 8-wave
+# 256 x 256 direct-to-LDS kernel with a ragged N edge and a ragged k-tile count
+SHAPES = [(37, 20, 12), (8, 8, 8), (200, 136, 72), (1000, 520, 776), (1032, 3072, 264), (520, 1048, 3080),
+          (4000, 4064, 4040)]
 
 
 @pytest.mark.parametrize("rows,n_out,n_in", SHAPES)
