@@ -728,7 +728,8 @@ struct DtlOp {
   __device__ static inline bool loads(int wave) { return NLW == NW || wave < NLW; }
   // direct loads of the k tile at k0 into the stage at S (byte pointer)
   __device__ inline void load(__amdgpu_buffer_rsrc_t R, char* S, int k0) const {
-    const int wave = threadIdx.x >> 6;
+    // wave-uniform: the LDS destination (M0) is then computed on the scalar unit
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (!loads(wave)) return;
 #pragma unroll
     for (int t = 0; t < NL; ++t)
