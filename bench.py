@@ -136,7 +136,8 @@ def main():
                     help="jagg: time the JAGG windows only (for a kernel trace of exactly those launches)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU (every GPU box here has one); --gpus must be 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU (the path has no multi-GPU sharding); "
+                                   "--gpus must be 1"}))
         sys.exit(2)
 
     import torch
