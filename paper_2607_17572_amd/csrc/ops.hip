@@ -1149,10 +1149,41 @@ __global__ void convert_k(const void* x, int dti, void* y, int dto, size_t n) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) st_any(y, dto, i, ld_any(x, dti, i));
 }
+// 8 elements per thread: 16- and 32-byte accesses (the same conversions as
+// convert_k, so the same bits)
+template <typename TI, typename TO>
+__global__ void convert8_k(const TI* __restrict__ x, TO* __restrict__ y, size_t n8) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n8) {
+    float v[8];
+    ld8f(x + 8 * i, v);
+    st8f(y + 8 * i, v);
+  }
+}
 int convert(const void* x, int dt_in, void* y, int dt_out, size_t n, hipStream_t s) {
   if (!n) return 0;
-  hipLaunchKernelGGL(convert_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, dt_in, y, dt_out, n);
-  LAUNCH_OK("convert");
+  size_t done = 0;
+  if (al16(x) && al16(y) && n >= 8) {
+    const size_t n8 = n / 8;
+    const dim3 grid((unsigned)((n8 + 255) / 256));
+    if (dt_in == BF16 && dt_out == F32)
+      hipLaunchKernelGGL((convert8_k<uint16_t, float>), grid, dim3(256), 0, s, (const uint16_t*)x, (float*)y, n8);
+    else if (dt_in == F32 && dt_out == BF16)
+      hipLaunchKernelGGL((convert8_k<float, uint16_t>), grid, dim3(256), 0, s, (const float*)x, (uint16_t*)y, n8);
+    else if (dt_in == BF16)
+      hipLaunchKernelGGL((convert8_k<uint16_t, uint16_t>), grid, dim3(256), 0, s, (const uint16_t*)x, (uint16_t*)y, n8);
+    else
+      hipLaunchKernelGGL((convert8_k<float, float>), grid, dim3(256), 0, s, (const float*)x, (float*)y, n8);
+    LAUNCH_OK("convert");
+    done = n8 * 8;
+  }
+  if (done < n) {
+    const size_t r = n - done;
+    hipLaunchKernelGGL(convert_k, dim3((unsigned)((r + 255) / 256)), dim3(256), 0, s,
+                       (const void*)((const char*)x + done * dsize(dt_in)), dt_in,
+                       (void*)((char*)y + done * dsize(dt_out)), dt_out, r);
+    LAUNCH_OK("convert");
+  }
   return 0;
 }
 
