@@ -606,7 +606,11 @@ int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int
 #define LNB(T, NV)                                                                                             \
   case NV: {                                                                                                   \
     auto k = ln_mod_bwd_vec_k<T, NV>;                                                                          \
-    if (lds > 65536) hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds); \
+    if (lds > 65536 &&                                                                                         \
+        hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) { \
+      set_error("ln_mod_bwd: cannot reserve the row buffers in LDS");                                          \
+      return 3;                                                                                                \
+    }                                                                                                          \
     hipLaunchKernelGGL(k, dim3(nc), dim3(64 * LN_W), lds, s, dA, (const T*)x, ch, c0, mean, rstd, mod_txt, mod_img, \
                        mod_w, sc_off, g, part_scale, part_shift);                                              \
   } break;
@@ -884,7 +888,6 @@ __global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__
     const T* pr = proj + (size_t)r * ld + 2 * p;
     T* dp = dproj + (size_t)r * ld_d + 2 * p;
     const size_t ob = ((size_t)bb * H * N + j) * Dh + 2 * p;  // head h adds h * N * Dh
-#pragma unroll 4
     for (int h = 0; h < H; ++h) {
       const size_t o = ob + (size_t)h * N * Dh;
       float qa = 0, qc = 0, ka = 0, kc = 0, va = 0, vc = 0, x0 = 0, x1 = 0, y0 = 0, y1 = 0;

@@ -10,7 +10,7 @@
 namespace jg {
 
 namespace {
-struct Rec { hipEvent_t a, b; double work; };
+struct Rec { hipEvent_t a, b; double work; bool ok; };
 struct Prof {
   std::mutex mu;
   int cls = PROF_NONE;
@@ -38,9 +38,8 @@ int prof_begin(int cls, hipStream_t s) {
   Prof& p = P();
   if (p.cls == PROF_NONE || cls != p.cls) return -1;
   std::lock_guard<std::mutex> g(p.mu);
-  Rec r{take_event(p), take_event(p), 0.0};
-  if (!r.a || !r.b) return -1;
-  hipEventRecord(r.a, s);
+  Rec r{take_event(p), take_event(p), 0.0, false};
+  if (!r.a || !r.b || hipEventRecord(r.a, s) != hipSuccess) return -1;
   p.recs.push_back(r);
   return (int)p.recs.size() - 1;
 }
@@ -49,7 +48,7 @@ void prof_end(int idx, hipStream_t s, double work) {
   if (idx < 0) return;
   Prof& p = P();
   std::lock_guard<std::mutex> g(p.mu);
-  hipEventRecord(p.recs[idx].b, s);
+  p.recs[idx].ok = hipEventRecord(p.recs[idx].b, s) == hipSuccess;
   p.recs[idx].work = work;
 }
 
@@ -75,12 +74,14 @@ jagg_status jagg_prof_end(long* launches, double* total_ms, double* total_work) 
   std::lock_guard<std::mutex> g(p.mu);
   double ms = 0.0, work = 0.0;
   for (auto& r : p.recs) {
-    if (hipEventSynchronize(r.b) != hipSuccess) {
-      jg::set_error("jagg_prof_end: event synchronisation failed");
+    float t = 0.f;
+    if (!r.ok || hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) {
+      jg::set_error("jagg_prof_end: a launch's timing events failed");
+      p.cls = jg::PROF_NONE;
+      p.recs.clear();
+      p.used = 0;
       return JAGG_EDEVICE;
     }
-    float t = 0.f;
-    hipEventElapsedTime(&t, r.a, r.b);
     ms += t;
     work += r.work;
   }
