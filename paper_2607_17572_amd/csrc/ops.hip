@@ -434,11 +434,75 @@ __global__ __launch_bounds__(256) void ln_mod_fwd_k(const T* __restrict__ x, int
   if (threadIdx.x == 0) { mean[r] = mu; rstd[r] = rs; }
 }
 
+// Hidden sizes that are multiples of 512: one wave per row, 8 consecutive
+// columns per lane and access (lane columns 8 lane + 512 i), the row's mean
+// and variance from wave reductions.
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void ln_mod_fwd_vec_k(const T* __restrict__ x, RowMap rm, int row0, int nrows,
+                                                        const float* __restrict__ mt, const float* __restrict__ mi,
+                                                        int mod_w, int sh_off, int sc_off, T* __restrict__ a,
+                                                        float* __restrict__ mean, float* __restrict__ rstd) {
+  constexpr int D = NV * 512;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int rr = blockIdx.x * 4 + w;
+  if (rr >= nrows) return;
+  const int r = row0 + rr;
+  float v[NV * 8];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) ld8f(x + (size_t)r * D + 8 * lane + 512 * i, v + 8 * i);
+#pragma unroll
+  for (int e = 0; e < NV * 8; ++e) s += v[e];
+  const float mu = wave_sum(s) / D;
+  float s2 = 0.f;
+#pragma unroll
+  for (int e = 0; e < NV * 8; ++e) {
+    const float dlt = v[e] - mu;
+    s2 += dlt * dlt;
+  }
+  const float var = wave_sum(s2) / D;
+  const float rs = rsqrtf(var + 1e-6f);
+  const float* m = (is_txt(rm, r) ? mt : mi) + (size_t)sample_of(rm, r) * mod_w;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = 8 * lane + 512 * i;
+    float sc[8], sf[8], o[8];
+    ld8f(m + sc_off + c, sc);
+    ld8f(m + sh_off + c, sf);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (v[8 * i + e] - mu) * rs * (1.f + sc[e]) + sf[e];
+    st8f(a + (size_t)r * D + c, o);
+  }
+  if (lane == 0) {
+    mean[r] = mu;
+    rstd[r] = rs;
+  }
+}
+
 int ln_mod_fwd(const void* x, int act_dt, int D, RowMap rm, int row0, int nrows, const float* mod_txt,
                const float* mod_img, int mod_w, int sh_off, int sc_off, void* a, float* mean, float* rstd,
                hipStream_t s) {
   if (D > 256 * MAXC) { set_error("ln_mod_fwd: hidden too large"); return 1; }
   if (nrows <= 0) return 0;
+  if (D % 512 == 0 && D <= 3584 && al16(x) && al16(a) && al16(mod_txt) && al16(mod_img) && mod_w % 4 == 0 &&
+      sh_off % 4 == 0 && sc_off % 4 == 0) {
+    const dim3 grid((unsigned)((nrows + 3) / 4));
+#define LNF(T, NV)                                                                                                \
+  case NV:                                                                                                        \
+    hipLaunchKernelGGL((ln_mod_fwd_vec_k<T, NV>), grid, dim3(256), 0, s, (const T*)x, rm, row0, nrows, mod_txt,  \
+                       mod_img, mod_w, sh_off, sc_off, (T*)a, mean, rstd);                                       \
+    break;
+    if (act_dt == BF16) {
+      switch (D / 512) { LNF(uint16_t, 1) LNF(uint16_t, 2) LNF(uint16_t, 3) LNF(uint16_t, 4) LNF(uint16_t, 5)
+                         LNF(uint16_t, 6) LNF(uint16_t, 7) }
+    } else {
+      switch (D / 512) { LNF(float, 1) LNF(float, 2) LNF(float, 3) LNF(float, 4) LNF(float, 5) LNF(float, 6)
+                         LNF(float, 7) }
+    }
+#undef LNF
+    LAUNCH_OK("ln_mod_fwd_vec");
+    return 0;
+  }
   if (act_dt == BF16)
     hipLaunchKernelGGL(ln_mod_fwd_k<uint16_t>, dim3(nrows), dim3(256), 0, s, (const uint16_t*)x, D, rm, row0,
                        mod_txt, mod_img, mod_w, sh_off, sc_off, (uint16_t*)a, mean, rstd);
@@ -649,11 +713,44 @@ __global__ void gated_residual_k(const T* __restrict__ xi, const T* __restrict__
   stf(xo, xidx, ldf(xi, xidx) + gt * ldf(y, (size_t)r * ld_y + c));
 }
 
+// 8 consecutive columns of one row per thread (D a multiple of 8): 16-byte
+// accesses, the same arithmetic per element as gated_residual_k
+template <typename T>
+__global__ void gated_residual8_k(const T* __restrict__ xi, const T* __restrict__ y, int D, int ld_y, RowMap rm,
+                                  int row0, size_t n8, const float* __restrict__ mt, const float* __restrict__ mi,
+                                  int mod_w, int gate_off, T* __restrict__ xo) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n8) return;
+  const size_t e0 = 8 * i;
+  const int r = row0 + (int)(e0 / D), c = (int)(e0 % D);
+  const float* gp = (is_txt(rm, r) ? mt : mi) + (size_t)sample_of(rm, r) * mod_w + gate_off + c;
+  float xv[8], yv[8], gt[8], o[8];
+  ld8f(xi + (size_t)r * D + c, xv);
+  ld8f(y + (size_t)r * ld_y + c, yv);
+  ld8f(gp, gt);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = xv[e] + gt[e] * yv[e];
+  st8f(xo + (size_t)r * D + c, o);
+}
+
 int gated_residual(const void* xi, const void* y, int act_dt, int D, int ld_y, RowMap rm, int row0, int nrows,
                    const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* xo,
                    hipStream_t s) {
   const size_t n = (size_t)nrows * D;
   if (n == 0) return 0;
+  if (D % 8 == 0 && ld_y % 8 == 0 && al16(xi) && al16(y) && al16(xo) && al16(mod_txt) && al16(mod_img) &&
+      mod_w % 4 == 0 && gate_off % 4 == 0) {
+    const size_t n8 = n / 8;
+    const dim3 grid((unsigned)((n8 + 255) / 256));
+    if (act_dt == BF16)
+      hipLaunchKernelGGL(gated_residual8_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)xi,
+                         (const uint16_t*)y, D, ld_y, rm, row0, n8, mod_txt, mod_img, mod_w, gate_off, (uint16_t*)xo);
+    else
+      hipLaunchKernelGGL(gated_residual8_k<float>, grid, dim3(256), 0, s, (const float*)xi, (const float*)y, D, ld_y,
+                         rm, row0, n8, mod_txt, mod_img, mod_w, gate_off, (float*)xo);
+    LAUNCH_OK("gated_residual");
+    return 0;
+  }
   dim3 grid((unsigned)((n + 255) / 256));
   if (act_dt == BF16)
     hipLaunchKernelGGL(gated_residual_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)xi, (const uint16_t*)y,
