@@ -913,9 +913,27 @@ __global__ __launch_bounds__(256) void qk_norm_rope_fwd_k(const T* __restrict__ 
   stf(Vh, o + 1, ldf(pr, 2 * D + h * rp.Dh + 2 * p + 1));
 }
 
+template <typename T>
+__global__ void qk_norm_rope_fwd_row_k(const T* __restrict__ proj, int ld, RowMap rm, Rope rp, Gains gn,
+                                       T* __restrict__ Qh, T* __restrict__ Kh, T* __restrict__ Vh,
+                                       float* __restrict__ rq, float* __restrict__ rk);
+
 int qk_norm_rope_fwd(const void* proj, int ld, int act_dt, RowMap rm, Rope rp, Gains gn,
                      void* Qh, void* Kh, void* Vh, float* rinv_q, float* rinv_k, hipStream_t s) {
   if (rp.Dh > 128 || rp.Dh % 4) { set_error("qk_norm_rope: head_dim must be <= 128 and a multiple of 4"); return 1; }
+  // RoPE pairs as one access each: even leading dimension, 8-byte aligned bases
+  auto al8 = [](const void* p) { return ((uintptr_t)p & 7u) == 0; };
+  if (!(ld & 1) && al8(proj) && al8(Qh) && al8(Kh) && al8(Vh)) {
+    const dim3 grid((unsigned)((rm.rows() + 3) / 4));
+    if (act_dt == BF16)
+      hipLaunchKernelGGL(qk_norm_rope_fwd_row_k<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)proj, ld, rm, rp,
+                         gn, (uint16_t*)Qh, (uint16_t*)Kh, (uint16_t*)Vh, rinv_q, rinv_k);
+    else
+      hipLaunchKernelGGL(qk_norm_rope_fwd_row_k<float>, grid, dim3(256), 0, s, (const float*)proj, ld, rm, rp, gn,
+                         (float*)Qh, (float*)Kh, (float*)Vh, rinv_q, rinv_k);
+    LAUNCH_OK("qk_norm_rope_fwd");
+    return 0;
+  }
   const int nitems = rm.rows() * rp.H;
   dim3 grid((nitems + 3) / 4);
   if (act_dt == BF16)
@@ -947,6 +965,56 @@ __device__ inline void st2f(uint16_t* p, float a, float c) {
   *(uint32_t*)p = (uint32_t)f2bf(a) | ((uint32_t)f2bf(c) << 16);
 }
 __device__ inline void st2f(float* p, float a, float c) { *(float2*)p = make_float2(a, c); }
+
+// Forward, one wave per row: lane p owns RoPE pair p, whose rotation depends
+// only on the token and is computed once per row; the heads are looped over
+// with one pair access per operand.  Per head the arithmetic is that of
+// qk_norm_rope_fwd_k (same lane sums, same products).
+template <typename T>
+__global__ __launch_bounds__(256) void qk_norm_rope_fwd_row_k(const T* __restrict__ proj, int ld, RowMap rm,
+                                                              Rope rp, Gains gn, T* __restrict__ Qh,
+                                                              T* __restrict__ Kh, T* __restrict__ Vh,
+                                                              float* __restrict__ rq, float* __restrict__ rk) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rm.rows()) return;
+  const int lane = threadIdx.x & 63;
+  const int H = rp.H, Dh = rp.Dh, D = H * Dh, N = rm.nt + rm.ni;
+  const bool act = lane < Dh / 2;
+  const int p = act ? lane : 0;
+  const T* pr = proj + (size_t)r * ld + 2 * p;
+  const int st = r < rm.B * rm.nt ? 0 : 1;
+  const T* qg = (const T*)gn.q[st];
+  const T* kg = (const T*)gn.k[st];
+  const float qga = act ? ldf(qg, 2 * p) : 0.f, qgb = act ? ldf(qg, 2 * p + 1) : 0.f;
+  const float kga = act ? ldf(kg, 2 * p) : 0.f, kgb = act ? ldf(kg, 2 * p + 1) : 0.f;
+  int b, j;
+  tok_of_row(rm, r, b, j);
+  float sn = 0.f, cs = 1.f;
+  if (act) sincosf(rope_angle(rp, j, p), &sn, &cs);
+  const size_t ob = ((size_t)b * H * N + j) * Dh + 2 * p;  // head h adds h * N * Dh
+  for (int h = 0; h < H; ++h) {
+    float q0 = 0.f, q1 = 0.f, k0 = 0.f, k1 = 0.f, v0 = 0.f, v1 = 0.f;
+    if (act) {
+      ld2f(pr + h * Dh, q0, q1);
+      ld2f(pr + D + h * Dh, k0, k1);
+      ld2f(pr + 2 * D + h * Dh, v0, v1);
+    }
+    const float riq = rsqrtf(wave_sum(q0 * q0 + q1 * q1) / Dh + 1e-6f);
+    const float rik = rsqrtf(wave_sum(k0 * k0 + k1 * k1) / Dh + 1e-6f);
+    if (lane == 0) {
+      rq[(size_t)r * H + h] = riq;
+      rk[(size_t)r * H + h] = rik;
+    }
+    if (act) {
+      const float qa = q0 * riq * qga, qb = q1 * riq * qgb;
+      const float ka = k0 * rik * kga, kb = k1 * rik * kgb;
+      const size_t o = ob + (size_t)h * N * Dh;
+      st2f(Qh + o, qa * cs - qb * sn, qa * sn + qb * cs);
+      st2f(Kh + o, ka * cs - kb * sn, ka * sn + kb * cs);
+      st2f(Vh + o, v0, v1);
+    }
+  }
+}
 
 // One wave per row (the rows of the sub-chunk dealt to the 4 waves), looping
 // over the heads; lane p owns RoPE pair p, whose rotation depends only on the
