@@ -41,7 +41,7 @@ HBM_PEAK = 8.0e12
 # workload, from two rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by
 # the same counters on a 1 GiB device copy; valid only for the GEMM source
 # it was measured on (sha256 of gemm.hip, first 16 hex digits).
-WGRAD_TRAFFIC = {"gemm_src": "23e61b859234a6d6", "bytes_per_launch": 708.30e6}
+WGRAD_TRAFFIC = {"gemm_src": "ee046861998b99f4", "bytes_per_launch": 710.12e6}
 
 
 def block_flops(D, F, N, B):

@@ -647,8 +647,13 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
 // unpadded and 16-byte chunks are XOR-swizzled by row so that both the 1 KB
 // contiguous direct loads and the fragment reads are free of bank conflicts:
 //   k-contiguous operand, tile [rows][32 k] (64 B rows):
-//     chunk' = chunk ^ (((row >> 1) ^ (row >> 3)) & 3),
-//     fragments are single 16-byte reads;
+//     chunk' = chunk ^ s(row), s = 2 row_1 ^ 3 row_2 ^ row_3 (row_i: bit i),
+//     fragments are single 16-byte reads.  A 16-byte read is served in
+//     groups of lanes such as {0-3, 32-35} (rows r..r+3, both halves of the
+//     16-deep step); s keeps those groups, and groups of 8 or 16 consecutive
+//     lanes, on distinct banks (SQ_LDS_BANK_CONFLICT reads 0; the earlier
+//     s = (row_1 row_2) ^ (row_3 row_4) held only for consecutive lanes and
+//     cost 1.6-1.9 conflict cycles per LDS instruction);
 //   k-strided operand, tile [32 k][rows] (2 * rows bytes per k row):
 //     chunk' = chunk ^ (((k & 3) << 1) | ((k & 1) << 3))  (256 rows),
 //     chunk' = chunk ^ ((k & 3) << 1)                      (192 rows: the XOR
@@ -674,7 +679,7 @@ __device__ __forceinline__ void wait_vm_lds() {
   __builtin_amdgcn_s_waitcnt((NV & 15) | ((NV >> 4) << 14) | 0x70);  // vmcnt(NV) expcnt(7) lgkmcnt(0)
 }
 
-__device__ __forceinline__ int swz_n(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+__device__ __forceinline__ int swz_n(int row) { return (((row >> 1) & 1) * 2) ^ (((row >> 2) & 1) * 3) ^ ((row >> 3) & 1); }
 template <int ROWS>
 __device__ __forceinline__ int swz_t(int k) {
   return ROWS == 256 ? (((k & 3) << 1) | ((k & 1) << 3)) : ((k & 3) << 1);
