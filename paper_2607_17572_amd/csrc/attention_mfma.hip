@@ -566,14 +566,19 @@ struct ATile {
     const int rr = lane & 31, h = lane >> 5;
 #pragma unroll
     for (int kb = 0; kb < 8; ++kb) roff[kb] = rr * 256 + (((2 * kb + h) ^ asw(rr)) << 4);
-    const int g = lane >> 4, j = lane & 15;
-    const int q1 = 4 * (g >> 1) + (j >> 2), q2 = q1 + 8;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      const int ch = 4 * dt + 2 * (g & 1) + ((j & 3) >> 1);
-      t1[dt] = q1 * 256 + ((ch ^ asw(q1)) << 4) + (j & 1) * 8;
-      t2[dt] = q2 * 256 + ((ch ^ asw(q2)) << 4) + (j & 1) * 8;
+      const int2 o = tr_off(lane, dt);
+      t1[dt] = o.x;
+      t2[dt] = o.y;
     }
+  }
+  // byte offsets of the two transposing reads of column block dt for this lane
+  static __device__ inline int2 tr_off(int lane, int dt) {
+    const int g = lane >> 4, j = lane & 15;
+    const int q1 = 4 * (g >> 1) + (j >> 2), q2 = q1 + 8;
+    const int ch = 4 * dt + 2 * (g & 1) + ((j & 3) >> 1);
+    return {q1 * 256 + ((ch ^ asw(q1)) << 4) + (j & 1) * 8, q2 * 256 + ((ch ^ asw(q2)) << 4) + (j & 1) * 8};
   }
   // 16 direct loads of 1 KB (4 rows each), 4 per wave; rowoff(r) = byte offset
   // of tile row r in the resource, or a negative value for a padding row
@@ -597,6 +602,16 @@ struct ATile {
   __device__ inline bf16x8 tr(const char* S, int c, int dt) const {
     const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + t1[dt] + c * 4096));
     const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + t2[dt] + c * 4096));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+  }
+  // The two read offsets of column block dt, for a dt known only at run time:
+  // recomputed rather than indexed, so that t1/t2 stay in registers (a dynamic
+  // index moves the arrays to LDS and costs a strided LDS read per use)
+  __device__ inline int2 tr_sel(int dt) const { return tr_off(threadIdx.x & 63, dt); }
+  __device__ inline bf16x8 tr(const char* S, int c, int2 o) const {
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + o.x + c * 4096));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + o.y + c * 4096));
     const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     return __builtin_bit_cast(bf16x8, v);
   }
@@ -953,6 +968,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       arsrc((const uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds, (long)a.nk_pad * a.ld_ds * 2);
   ATile at;
   at.init();
+  const int2 wsel = at.tr_sel(w);  // this wave's 32 query columns of the dS^T tile
   f32x16 dq[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) dq[i] = zero16();
@@ -985,14 +1001,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     bf16x8 tk[2][4], ts[2];
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) tk[0][dt] = at.tr(Kc, 0, dt);
-    ts[0] = at.tr(Sc, 0, w);
+    ts[0] = at.tr(Sc, 0, wsel);
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
       const int cur = cb & 1, nxt = cur ^ 1;
       if (cb + 1 < 4) {
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) tk[nxt][dt] = at.tr(Kc, cb + 1, dt);
-        ts[nxt] = at.tr(Sc, cb + 1, w);
+        ts[nxt] = at.tr(Sc, cb + 1, wsel);
       }
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(tk[cur][dt], ts[cur], dq[dt]);
