@@ -71,21 +71,22 @@ __device__ inline float block_sum(float v, float* sh) {
   return r;
 }
 
-// tanh(u) = 1 - 2 / (exp(2u) + 1): one exp and one hardware reciprocal
-// (v_rcp_f32, 1 ulp) instead of an IEEE division sequence; exact limits at
-// +-inf (rcp(inf) = 0, rcp(1) = 1), absolute error a few ulp of 1
-__device__ __forceinline__ float tanh_exp(float u) {
-  return 1.f - 2.f * __builtin_amdgcn_rcpf(__expf(2.f * u) + 1.f);
+// GELU, tanh form: u = c (x + a x^3), tanh(u) = 1 - 2r with
+// r = 1 / (exp(2u) + 1) (one exp2 and one hardware reciprocal, v_rcp_f32, 1
+// ulp; exact limits at +-inf: rcp(inf) = 0, rcp(1) = 1).  Then 1 + tanh = 2(1 - r)
+// and 1 - tanh^2 = 4 r (1 - r), so
+//   gelu(x)  = x (1 - r)
+//   gelu'(x) = (1 - r) (1 + 2 x r u'(x)),  u'(x) = c (1 + 3 a x^2).
+constexpr float GELU_C = 0.7978845608028654f, GELU_A = 0.044715f;
+__device__ __forceinline__ float gelu_r(float x, float x2) {
+  // 2u log2(e) = x (2c log2(e) + 2ca log2(e) x^2)
+  const float kc = 2.f * GELU_C * 1.4426950408889634f, ka = kc * GELU_A;
+  return __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f(x * fmaf(ka, x2, kc)) + 1.f);
 }
-__device__ __forceinline__ float gelu_tanh(float x) {
-  const float c = 0.7978845608028654f;
-  const float th = tanh_exp(c * (x + 0.044715f * x * x * x));
-  return 0.5f * x * (1.f + th);
-}
+__device__ __forceinline__ float gelu_tanh(float x) { return x * (1.f - gelu_r(x, x * x)); }
 __device__ __forceinline__ float gelu_tanh_grad(float x) {
-  const float c = 0.7978845608028654f;
-  const float th = tanh_exp(c * (x + 0.044715f * x * x * x));
-  return 0.5f * (1.f + th) + 0.5f * x * (1.f - th * th) * c * (1.f + 3.f * 0.044715f * x * x);
+  const float x2 = x * x, r = gelu_r(x, x2);
+  return (1.f - r) * fmaf(x * r, fmaf(6.f * GELU_A * GELU_C, x2, 2.f * GELU_C), 1.f);
 }
 __device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
 __device__ inline float silu_grad(float x) {
