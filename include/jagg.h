@@ -80,9 +80,13 @@ typedef struct jagg_ctx jagg_ctx;
 /* Thread-local message describing the last failure of any call (never NULL). */
 const char* jagg_last_error(void);
 
-/* Parameter layout.  *n_tensors receives the tensor count, *n_elems the flat
- * length (padding between tensors is never read or written).  If out != NULL
- * it receives min(cap, count) descriptors.  Host only; no device needed. */
+/* Parameter layout of theta, the parameters of the velocity network
+ * v_theta(z, t) whose gradient the method computes (problem statement of the
+ * Method section; the block structure is the MMDiT described above).
+ * *n_tensors receives the tensor count, *n_elems the flat length (padding
+ * between tensors is never read or written).  If out != NULL it receives
+ * min(cap, count) descriptors.  Host only; no device needed.  EINVAL on a null
+ * pointer or an invalid config. */
 jagg_status dit_param_layout(const dit_config* cfg, size_t* n_tensors, size_t* n_elems, jagg_tensor_desc* out,
                              size_t cap);
 
@@ -99,7 +103,7 @@ jagg_status dit_workspace_bytes(const jagg_ctx* ctx, int batch, size_t* bytes);
  * destroyed; the caller frees it).  Calls check that it is large enough. */
 jagg_status jagg_ctx_set_workspace(jagg_ctx* ctx, void* ws, size_t bytes);
 
-/* Forward v = v_theta(z, t) for `batch` samples (1 <= batch <= 64).
+/* Forward v = v_theta(z, t) for `batch` samples (1 <= batch <= 32).
  *   theta : device, flat parameters (act dtype)
  *   z     : device, latent (batch, in_ch, lat_h, lat_w); block-only: token rows
  *   t     : host, `batch` network-input timesteps
@@ -120,22 +124,29 @@ jagg_status dit_vjp(jagg_ctx* ctx, const void* theta, const void* saved, int bat
 
 /* Eq. alpha on the host: alpha_j = (t_0 - t_j)/(t_0 - t_{W-1}) computed in fp64
  * and rounded to fp32 (alpha_0 = 0 and alpha_{W-1} = 1 exactly).  EINVAL if
- * W < 2, a pointer is NULL or t_0 == t_{W-1}. */
+ * W < 2, a pointer is NULL or t is not strictly decreasing (a window's steps
+ * run from high to low noise; this includes t_0 == t_{W-1}). */
 jagg_status jagg_alpha(const float* t, int W, float* alpha_out);
 
 /* Eq. s_base / s_corr on the device: s_base = sum_j (1 - alpha_j) s_j,
  * s_corr = sum_j alpha_j s_j over n elements; fp32 accumulation in j order,
  * one rounding on store.  s: host array of W device pointers; t: host W
- * timesteps (the weights come from jagg_alpha).  s_base/s_corr: device, n
- * elements of `dtype` (same as the inputs).  1 <= W <= 64. */
+ * timesteps, strictly decreasing (the weights come from jagg_alpha).
+ * s_base/s_corr: device, n elements of `dtype` (same as the inputs).
+ * 2 <= W <= 64. */
 jagg_status jagg_aggregate(jagg_ctx* ctx, const void* const* s, const float* t, int W, size_t n, int dtype,
                            void* s_base, void* s_corr);
 
-/* Routing score of one window: the mean over the W(W-1)/2 pairs (i < j) of the
- * cosine similarity of the per-step vectors h_i, h_j (n elements each, `dtype`),
- * accumulated in fp64.  h: host array of W device pointers, 2 <= W <= 8.
+/* Routing score of one window (high-noise vs low-noise scheduling: a window is
+ * routed to JAGG while its score passes the cosine rule of the
+ * gradient-quality appendix, cos >= 0.5).  The paper's cosine compares
+ * gradients; this call scores any W per-step vectors the caller supplies
+ * (per-step gradients, hidden states): the mean over the W(W-1)/2 pairs
+ * (i < j) of cos(h_i, h_j) (n elements each, `dtype`), accumulated in fp64 in
+ * a fixed order.  h: host array of W device pointers, 2 <= W <= 8.
  * score_out: host, receives the score (the call synchronises the stream).
- * Uses the bound workspace. */
+ * Uses the head of the bound workspace; EINVAL if it is not bound or too
+ * small, on a null pointer, n = 0 or an unknown dtype. */
 jagg_status jagg_group_scores(jagg_ctx* ctx, const void* const* h, size_t n, int W, int dtype, double* score_out);
 
 /* Routing (high-noise vs low-noise scheduling; gradient-quality appendix).
@@ -173,13 +184,32 @@ jagg_status jagg_endpoint_backward(jagg_ctx* ctx, const void* theta, const void*
                                    const float* t, int W, int endpoint, void* dtheta, float beta);
 
 /* Gradient quality (gradient-quality appendix: cos(g_jagg, g_exact) and the
- * norm ratio rho = |g_jagg| / |g_exact|): the fp64 sums a.b, a.a and b.b over n
- * elements of two device vectors of `dtype` (16-byte aligned), returned in
- * out[0..2] (host).  cos = out[0] / sqrt(out[1] out[2]), rho = sqrt(out[1] /
- * out[2]).  Every element of the n is included: flat gradient buffers must
- * hold zeros in their padding.  Deterministic (fixed block order).  Uses the
- * bound workspace; synchronises the context's stream. */
+ * norm ratio rho = |g_jagg| / |g_exact|) of two device vectors a, b of n
+ * elements of `dtype` (16-byte aligned).  out (host, 5 doubles): out[0..2] the
+ * fp64 sums a.b, a.a, b.b; out[3] = cos = a.b / sqrt(a.a b.b); out[4] = rho =
+ * sqrt(a.a / b.b) (NaN where a norm is zero).  Every element of the n is
+ * included: flat gradient buffers must hold zeros in their padding.
+ * Deterministic (fixed block order).  Uses the head of the bound workspace;
+ * synchronises the context's stream. */
 jagg_status jagg_grad_compare(jagg_ctx* ctx, const void* a, const void* b, size_t n, int dtype, double* out);
+
+/* Gradient quality of one window (gradient-quality appendix, per-group
+ * cos(g_jagg, g_exact) and rho; the endpoint-only ablation of the
+ * experiments): runs the JAGG group backward into g_jagg, the per-step
+ * backward into g_exact and the ablation J_0^T s_0 + J_{W-1}^T s_{W-1} (the
+ * JAGG pass with the endpoint signals alone, weight one each) into g_ablate,
+ * then compares them.  out (host, 4 doubles): cos(g_jagg, g_exact),
+ * rho_jagg = |g_jagg| / |g_exact|, cos(g_ablate, g_exact), rho_ablate.
+ *   saved_pair: batch-2B forward of the window's endpoint pair; saved_steps:
+ *   host array of W device pointers, the batch-B forward of each step; s: host
+ *   array of W device pointers; t: host, W timesteps (strictly decreasing);
+ *   g_jagg, g_exact, g_ablate: device, dtheta-sized buffers of cfg.grad_dtype
+ *   (16-byte aligned; their padding is never written and must hold zeros, so
+ *   zero them once before the first call).
+ * Workspace: dit_workspace_bytes(2 * batch).  Synchronises the stream. */
+jagg_status jagg_window_quality(jagg_ctx* ctx, const void* theta, const void* saved_pair,
+                                const void* const* saved_steps, int batch, const void* const* s, const float* t, int W,
+                                void* g_jagg, void* g_exact, void* g_ablate, double* out);
 
 /* Phase 2 of JAGG for a GRPO window on rectified flow (GRPO section: Eq.
  * grpo_loss, Eq. logprob and the Euler-step mean; hyperparameter appendix:
@@ -194,7 +224,8 @@ jagg_status jagg_grad_compare(jagg_ctx* ctx, const void* a, const void* b, size_
  *         term is strictly the larger (the PPO-clip remark's zero gradient)
  *         and -A/W otherwise.
  * The squared norms are accumulated in fp64 and the clip decision is taken
- * in fp64; the gradients are formed in fp32.  All arrays use the batch-B
+ * in fp64; the gradients are formed in fp32.  t_0 .. t_W must be strictly
+ * decreasing.  All arrays use the batch-B
  * output layout of the model (block-only: stream-major token rows); every
  * per-sample segment must be a multiple of 8 elements. */
 typedef struct {
@@ -237,6 +268,34 @@ jagg_status jagg_grpo_group_backward(jagg_ctx* ctx, const void* theta, const voi
  * pointers, each a batch-B forward. */
 jagg_status perstep_group_backward(jagg_ctx* ctx, const void* theta, const void* const* saved, int batch,
                                    const void* const* s, int W, void* dtheta, float beta);
+
+/* Whole-trajectory gradient (high-noise vs low-noise scheduling; gradient
+ * accumulation over groups).  The T steps, in sampling order (t strictly
+ * decreasing: high noise first), form n = floor(T / W) full windows (window g
+ * = steps gW .. gW + W - 1) and a tail of T mod W steps.  Window g takes the
+ * JAGG backward (as jagg_group_backward) when use_jagg[g] = 1 and the per-step
+ * backward (as perstep_group_backward) when it is 0; the tail always takes the
+ * per-step backward.  dtheta = beta * dtheta + the sum of all windows'
+ * gradients.
+ *   saved_pairs: host array of n device pointers; entry g is the batch-2B
+ *                forward of window g's endpoint pair (read only where
+ *                use_jagg[g] = 1; may be NULL elsewhere, or the array NULL
+ *                if no window takes JAGG)
+ *   saved_steps: host array of T device pointers; entry k is the batch-B
+ *                forward of step k (read only for the steps of per-step
+ *                windows and of the tail; may be NULL for the others)
+ *   s:           host array of T device pointers, batch-B outputs s_k
+ *   t:           host, T timesteps
+ *   use_jagg:    host, n bytes 0/1 (e.g. from jagg_route); may be NULL if n = 0
+ * Workspace: dit_workspace_bytes(2 * batch) if any window takes JAGG, else
+ * dit_workspace_bytes(batch).  2 <= W <= 64, T >= 1, batch 1..16 (1..32 if no
+ * window takes JAGG).  EINVAL before any launch on a null pointer that would
+ * be read, a mask byte other than 0/1, t not strictly decreasing or a size out
+ * of range. */
+jagg_status jagg_trajectory_backward(jagg_ctx* ctx, const void* theta, int T, int W, int batch,
+                                     const void* const* saved_pairs, const void* const* saved_steps,
+                                     const void* const* s, const float* t, const unsigned char* use_jagg,
+                                     void* dtheta, float beta);
 
 /* One product of a linear layer's backward, the kernel the VJP issues for every
  * projection of a block (backward-cost appendix: the backward of a linear map

@@ -12,7 +12,9 @@ paper's steps in its order and notation:
   Phase 2 remark and the gradient-quality appendix)
 * routing: groups ordered from high to low noise; the first fraction use JAGG
   (high-noise vs low-noise scheduling); calibrated by cos >= 0.5
-  (gradient-quality appendix).
+  (gradient-quality appendix);
+* trajectory: the routed windows take g_jagg, the others and the T mod W tail
+  take g_exact, summed over the trajectory (gradient accumulation over groups).
 """
 from __future__ import annotations
 
@@ -25,14 +27,18 @@ from . import mmdit
 def alpha(t) -> np.ndarray:
     """Interpolation coefficients of one window, in fp64.
 
-    Raises ValueError when W < 2 or t_0 == t_{W-1} (the weights are undefined)."""
+    A window is W consecutive denoising steps, which run from high noise to low
+    noise, so its timesteps are strictly decreasing (reading of the problem
+    statement: sampling integrates from t = 1 towards t = 0).  Raises
+    ValueError when W < 2 or t is not strictly decreasing (which includes
+    t_0 == t_{W-1}, where the weights are undefined)."""
     t = np.asarray(t, dtype=np.float64)
     W = t.shape[0]
     if W < 2:
         raise ValueError("a window needs at least two timesteps")
+    if not np.all(t[1:] < t[:-1]):
+        raise ValueError("the timesteps of a window must be strictly decreasing")
     den = t[0] - t[W - 1]
-    if den == 0.0:
-        raise ValueError("t_0 == t_{W-1}: interpolation weights undefined")
     return (t[0] - t) / den
 
 
@@ -149,6 +155,51 @@ def windows(T: int, W: int):
     return full, tail
 
 
+# ------------------------------------------------------------- trajectory
+def trajectory_plan(T: int, W: int, mask):
+    """The backward passes of a whole trajectory of T steps (high-noise vs
+    low-noise scheduling): steps are taken in sampling order, i.e. from high to
+    low noise; they form floor(T / W) full windows, window g takes the JAGG
+    backward when mask[g] is 1 and the per-step backward otherwise, and the
+    last T mod W steps (a tail the paper avoids by choosing T divisible by W)
+    always take the per-step backward.  Returns [(step indices, use_jagg)]."""
+    if W < 2 or T < 1:
+        raise ValueError("need W >= 2 and T >= 1")
+    full, tail = windows(T, W)
+    mask = np.asarray(mask, dtype=np.uint8).reshape(-1)
+    if mask.shape[0] != len(full) or np.any(mask > 1):
+        raise ValueError("the mask needs one 0/1 entry per full window")
+    plan = [(idx, bool(m)) for idx, m in zip(full, mask)]
+    if tail:
+        plan.append((tail, False))
+    return plan
+
+
+def trajectory(cfg, P, inputs, s_list, t, W, mask=None, frac=None, scores=None, tau: float = 0.5):
+    """Gradient of a whole trajectory of T = len(inputs) steps: the sum over
+    its windows of the JAGG group gradient (routed windows) or the per-step
+    gradient (the rest and the tail), as gradient accumulation over groups
+    does.  The mask comes from ``route`` (static frac or per-window scores)
+    unless given.  t: the T timesteps, strictly decreasing.  Returns
+    (mask, {name: grad})."""
+    T = len(inputs)
+    t = np.asarray(t, dtype=np.float64)
+    if t.shape[0] != T or len(s_list) != T:
+        raise ValueError("one timestep and one upstream gradient per step")
+    if not np.all(t[1:] < t[:-1]):
+        raise ValueError("a trajectory's timesteps must be strictly decreasing")
+    n_full = T // W
+    if mask is None:
+        mask = route(n_full, frac=frac, scores=scores, tau=tau)[0] if n_full else np.zeros(0, np.uint8)
+    total = None
+    for idx, use_jagg in trajectory_plan(T, W, mask):
+        ins = [inputs[k] for k in idx]
+        ss = [s_list[k] for k in idx]
+        G = g_jagg(cfg, P, ins, ss, t[idx]) if use_jagg else g_exact(cfg, P, ins, ss)
+        total = G if total is None else {k: total[k] + G[k] for k in total}
+    return np.asarray(mask, dtype=np.uint8), total
+
+
 # ----------------------------------------------------- Theorem 1 linear toy
 class LinearToy:
     """v_theta(z, t) = A z + b t + c, theta = (A, b, c): linear in (z, t)."""
@@ -177,3 +228,13 @@ class LinearToy:
         g0 = self.vjp(zs[0], ts[0], sb)
         g1 = self.vjp(zs[W - 1], ts[W - 1], sc)
         return [x + y for x, y in zip(g0, g1)]
+
+    def trajectory(self, zs, ts, ss, W, mask):
+        """Whole-trajectory gradient under ``trajectory_plan`` (same windows,
+        routing and tail as the MMDiT trajectory)."""
+        out = [np.zeros_like(self.A), np.zeros_like(self.b), np.zeros_like(self.c)]
+        for idx, use_jagg in trajectory_plan(len(zs), W, mask):
+            args = ([zs[k] for k in idx], [ts[k] for k in idx], [ss[k] for k in idx])
+            g = self.g_jagg(*args) if use_jagg else self.g_exact(*args)
+            out = [a + b for a, b in zip(out, g)]
+        return out

@@ -64,9 +64,13 @@ def lib() -> ctypes.CDLL:
             "jagg_route": [ctypes.POINTER(d), i, d, d, ctypes.POINTER(ctypes.c_ubyte), ctypes.POINTER(d)],
             "jagg_group_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, vp, f],
             "perstep_group_backward": [vp, vp, ctypes.POINTER(vp), i, ctypes.POINTER(vp), i, vp, f],
+            "jagg_trajectory_backward": [vp, vp, i, i, i, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                         ctypes.POINTER(f), ctypes.POINTER(ctypes.c_ubyte), vp, f],
             "jagg_linear_grad": [vp, i, vp, vp, vp, i, i, i, vp, i, f],
             "jagg_endpoint_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, i, vp, f],
             "jagg_grad_compare": [vp, vp, vp, sz, i, ctypes.POINTER(d)],
+            "jagg_window_quality": [vp, vp, vp, ctypes.POINTER(vp), i, ctypes.POINTER(vp), ctypes.POINTER(f), i, vp, vp,
+                                    vp, ctypes.POINTER(d)],
             "jagg_grpo_composites": [vp, ctypes.POINTER(_GrpoWindow), i, vp, vp, vp],
             "jagg_grpo_upstream": [vp, ctypes.POINTER(_GrpoWindow), i, ctypes.POINTER(vp), vp],
             "jagg_grpo_group_backward": [vp, vp, vp, i, ctypes.POINTER(_GrpoWindow), vp, f, vp],
@@ -292,13 +296,26 @@ class Context:
         return dtheta
 
     def grad_compare(self, a, b):
-        """(a.b, a.a, b.b) in fp64 over every element of two equal-size device tensors."""
+        """(a.b, a.a, b.b, cos, rho) over every element of two equal-size device
+        tensors: the fp64 sums and the quality figures the library forms from them."""
         self.ensure_workspace(1)
-        out = (ctypes.c_double * 3)()
+        out = (ctypes.c_double * 5)()
         dt = BF16 if a.dtype == _torch().bfloat16 else F32
         assert a.numel() == b.numel() and a.dtype == b.dtype
         _check(lib().jagg_grad_compare(self._h, a.data_ptr(), b.data_ptr(), a.numel(), dt, out))
-        return out[0], out[1], out[2]
+        return tuple(out)
+
+    def window_quality(self, theta, saved_pair, saved_steps, batch: int, s_list, t, g_jagg, g_exact, g_ablate):
+        """(cos_jagg, rho_jagg, cos_ablate, rho_ablate) of one window; the three
+        group gradients are left in the given (zero-padded) buffers."""
+        W = len(s_list)
+        self.ensure_workspace(2 * batch)
+        tt = (ctypes.c_float * W)(*[float(x) for x in t])
+        out = (ctypes.c_double * 4)()
+        _check(lib().jagg_window_quality(self._h, theta.data_ptr(), saved_pair.data_ptr(), _ptrs(saved_steps), batch,
+                                         _ptrs(s_list), tt, W, g_jagg.data_ptr(), g_exact.data_ptr(),
+                                         g_ablate.data_ptr(), out))
+        return tuple(out)
 
     @staticmethod
     def _grpo_window(v_list, z_list, t, sigma, logp_old, adv, clip_eps, adv_clip):
@@ -359,6 +376,25 @@ class Context:
                                       None if pre is None else pre.data_ptr(), rows, n_out, n_in, result.data_ptr(),
                                       rdt, float(beta)))
         return result
+
+    def trajectory_backward(self, theta, W: int, batch: int, saved_pairs, saved_steps, s_list, t, use_jagg, dtheta,
+                            beta: float = 0.0):
+        """Whole trajectory: JAGG for the windows use_jagg marks, per step for
+        the rest and the T mod W tail.  saved_pairs: one entry per full window
+        (None where it takes the per-step backward); saved_steps: one per step
+        (None for steps of JAGG windows)."""
+        T = len(s_list)
+        n = T // W
+        any_jagg = any(int(u) for u in use_jagg)
+        self.ensure_workspace(2 * batch if any_jagg else batch)
+        vp = ctypes.c_void_p
+        pairs = (vp * max(n, 1))(*[None if x is None else x.data_ptr() for x in saved_pairs])
+        steps = (vp * T)(*[None if x is None else x.data_ptr() for x in saved_steps])
+        tt = (ctypes.c_float * T)(*[float(x) for x in t])
+        mk = (ctypes.c_ubyte * max(n, 1))(*[int(u) for u in use_jagg])
+        _check(lib().jagg_trajectory_backward(self._h, theta.data_ptr(), T, W, batch, pairs, steps, _ptrs(s_list), tt,
+                                              mk, dtheta.data_ptr(), float(beta)))
+        return dtheta
 
     def perstep_group_backward(self, theta, saved_list, batch: int, s_list, dtheta, beta: float = 0.0):
         self.ensure_workspace(batch)

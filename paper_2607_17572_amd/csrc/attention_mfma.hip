@@ -1046,9 +1046,9 @@ int attention_fwd_mfma(const AttnFwd& a, hipStream_t s) {
   if (!mfma_ok(a.Dh, a.dt, a.O, a.ld_o)) return -1;
   dim3 grid((a.N + F_QB - 1) / F_QB, a.B * a.H);
   const double nn = (double)a.B * a.H * a.N * (double)a.N * DH;
-  const int pi = prof_begin(PROF_ATTN_FWD, s);
-  hipLaunchKernelGGL(attn_fwd_mfma_k, grid, dim3(256), 0, s, a);
-  prof_end(pi, s, 4.0 * nn);
+  const int pi = prof_begin(PROF_ATTN_FWD);
+  launch(attn_fwd_mfma_k, grid, dim3(256), 0u, s, a);
+  prof_end(pi, 4.0 * nn);
   JG_CHECK_LAUNCH("attention_fwd_mfma");
   return 0;
 }
@@ -1065,16 +1065,16 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
                   (double)a.nk_pad * a.ld_ds * 2.0 < 2147483000.0 && (uintptr_t)a.dS % 16 == 0;
   AttnBwd ak = a;
   if (!ds) ak.dS = nullptr;
-  int pi = prof_begin(PROF_ATTN_BWD_KV, s);
-  if (v2) hipLaunchKernelGGL(attn_bwd_kv2_k, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0, s, ak);
-  else hipLaunchKernelGGL(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0, s, a);
-  prof_end(pi, s, 6.0 * nn);
+  int pi = prof_begin(PROF_ATTN_BWD_KV);
+  if (v2) launch(attn_bwd_kv2_k, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0u, s, ak);
+  else launch(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0u, s, a);
+  prof_end(pi, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
-  pi = prof_begin(PROF_ATTN_BWD_Q, s);
-  if (v2 && ds) hipLaunchKernelGGL(attn_bwd_q3_k, dim3((a.N + Q3_QB - 1) / Q3_QB, a.B * a.H), dim3(256), 0, s, a);
-  else if (v2) hipLaunchKernelGGL(attn_bwd_q2_k, dim3((a.N + Q2_QB - 1) / Q2_QB, a.B * a.H), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0, s, a);
-  prof_end(pi, s, 2.0 * nn);
+  pi = prof_begin(PROF_ATTN_BWD_Q);
+  if (v2 && ds) launch(attn_bwd_q3_k, dim3((a.N + Q3_QB - 1) / Q3_QB, a.B * a.H), dim3(256), 0u, s, a);
+  else if (v2) launch(attn_bwd_q2_k, dim3((a.N + Q2_QB - 1) / Q2_QB, a.B * a.H), dim3(256), 0u, s, a);
+  else launch(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0u, s, a);
+  prof_end(pi, 2.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_q_mfma");
   return 0;
 }

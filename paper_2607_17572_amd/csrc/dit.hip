@@ -805,6 +805,36 @@ jagg_status to_status(int rc) {
   return (jagg_status)rc;
 }
 
+// A window's (or trajectory's) timesteps run from high to low noise: strictly
+// decreasing (NaN fails the comparison too).
+bool decreasing(const float* t, int n) {
+  for (int j = 0; j + 1 < n; ++j)
+    if (!(t[j + 1] < t[j])) return false;
+  return true;
+}
+
+// Gradient quality from the fp64 sums (a.b, a.a, b.b) in out[0..2]: out[3] =
+// cos(a, b) = a.b / sqrt(a.a b.b), out[4] = rho = |a| / |b| (gradient-quality
+// appendix); NaN where a norm is zero.
+void quality_from_sums(double* out) {
+  const double ab = out[0], aa = out[1], bb = out[2];
+  out[3] = (aa > 0.0 && bb > 0.0) ? ab / std::sqrt(aa * bb) : std::nan("");
+  out[4] = bb > 0.0 ? std::sqrt(aa / bb) : std::nan("");
+}
+
+// The batch-independent head of the workspace (reduction partials, the score
+// slot, the GRPO coefficients) is all the scoring, comparison and GRPO calls
+// use; it must lie inside the bound workspace.
+jagg_status need_head_ws(const jagg_ctx* ctx, jg::Ws& W0, const char* who) {
+  if (!ctx->ws) return fail(JAGG_EINVAL, std::string(who) + ": workspace not bound");
+  jg::plan_ws(ctx->m, 1, ctx->ws, W0);
+  const char* end = (const char*)W0.gcoef + (size_t)jg::GRPO_MAX_W * 32 * sizeof(float);
+  if (end > (const char*)ctx->ws + ctx->ws_bytes)
+    return fail(JAGG_EINVAL, std::string(who) + ": workspace smaller than its " +
+                                 std::to_string(end - (const char*)ctx->ws) + "-byte head");
+  return JAGG_OK;
+}
+
 jagg_status need_ws(const jagg_ctx* ctx, int batch) {
   jg::Ws W;
   const size_t need = jg::plan_ws(ctx->m, batch, nullptr, W);
@@ -895,16 +925,16 @@ jagg_status dit_vjp(jagg_ctx* ctx, const void* theta, const void* saved, int bat
 jagg_status jagg_alpha(const float* t, int W, float* alpha_out) {
   if (!t || !alpha_out) return fail(JAGG_EINVAL, "jagg_alpha: null argument");
   if (W < 2) return fail(JAGG_EINVAL, "jagg_alpha: W must be >= 2");
+  if (!decreasing(t, W)) return fail(JAGG_EINVAL, "jagg_alpha: t must be strictly decreasing");
   const double t0 = t[0], den = (double)t[0] - (double)t[W - 1];
-  if (den == 0.0) return fail(JAGG_EINVAL, "jagg_alpha: t_0 == t_{W-1}");
   for (int j = 0; j < W; ++j) alpha_out[j] = (float)((t0 - (double)t[j]) / den);
   return JAGG_OK;
 }
 
 static jagg_status agg_weights(const float* t, int W, jg::AggArgs& a) {
   if (W < 2 || W > 64) return fail(JAGG_EINVAL, "aggregation: W must be 2..64");
+  if (!decreasing(t, W)) return fail(JAGG_EINVAL, "aggregation: t must be strictly decreasing");
   const double t0 = t[0], den = (double)t[0] - (double)t[W - 1];
-  if (den == 0.0) return fail(JAGG_EINVAL, "aggregation: t_0 == t_{W-1}");
   for (int j = 0; j < W; ++j) {
     const double al = (t0 - (double)t[j]) / den;
     a.wb[j] = (float)(1.0 - al);
@@ -940,9 +970,8 @@ jagg_status jagg_group_scores(jagg_ctx* ctx, const void* const* h, size_t n, int
   if (n == 0) return fail(JAGG_EINVAL, "jagg_group_scores: empty vectors");
   if (dtype != JAGG_F32 && dtype != JAGG_BF16) return fail(JAGG_EINVAL, "jagg_group_scores: unknown dtype");
   jg::Ws W0;
-  jg::plan_ws(ctx->m, 1, ctx->ws, W0);
-  const size_t need = jg::score_part_doubles(8) * sizeof(double) + 256;
-  if (!ctx->ws || ctx->ws_bytes < need) return fail(JAGG_EINVAL, "jagg_group_scores: workspace not bound");
+  jagg_status st = need_head_ws(ctx, W0, "jagg_group_scores");
+  if (st) return st;
   jg::ScoreArgs a;
   std::memset(&a, 0, sizeof(a));
   for (int j = 0; j < W; ++j) {
@@ -1089,15 +1118,53 @@ jagg_status jagg_grad_compare(jagg_ctx* ctx, const void* a, const void* b, size_
   if (dtype != JAGG_F32 && dtype != JAGG_BF16) return fail(JAGG_EINVAL, "jagg_grad_compare: unknown dtype");
   if (((uintptr_t)a | (uintptr_t)b) % 16) return fail(JAGG_EINVAL, "jagg_grad_compare: vectors must be 16-byte aligned");
   jg::Ws W0;
-  jg::plan_ws(ctx->m, 1, ctx->ws, W0);
-  static_assert(jg::CMP_BLOCKS * 3 <= 512 * 36, "compare partials must fit the score partial buffer");
-  const size_t need = jg::score_part_doubles(8) * sizeof(double) + 256;
-  if (!ctx->ws || ctx->ws_bytes < need) return fail(JAGG_EINVAL, "jagg_grad_compare: workspace not bound");
+  jagg_status st = need_head_ws(ctx, W0, "jagg_grad_compare");
+  if (st) return st;
   int rc = jg::grad_compare(a, b, n, dtype, W0.spart, W0.score, ctx->stream);
   if (rc) return (jagg_status)rc;
   if (hipMemcpyAsync(out, W0.score, 3 * sizeof(double), hipMemcpyDeviceToHost, ctx->stream) != hipSuccess ||
       hipStreamSynchronize(ctx->stream) != hipSuccess)
     return fail(JAGG_EDEVICE, "jagg_grad_compare: copy of the sums failed");
+  quality_from_sums(out);
+  return JAGG_OK;
+}
+
+jagg_status jagg_window_quality(jagg_ctx* ctx, const void* theta, const void* saved_pair,
+                                const void* const* saved_steps, int batch, const void* const* s, const float* t, int W,
+                                void* g_jagg, void* g_exact, void* g_ablate, double* out) {
+  const char* f = "jagg_window_quality";
+  if (!ctx || !theta || !saved_pair || !saved_steps || !s || !t || !g_jagg || !g_exact || !g_ablate || !out)
+    return fail(JAGG_EINVAL, std::string(f) + ": null argument");
+  if (W < 2 || W > 64) return fail(JAGG_EINVAL, std::string(f) + ": W must be 2..64");
+  if (((uintptr_t)g_jagg | (uintptr_t)g_exact | (uintptr_t)g_ablate) % 16)
+    return fail(JAGG_EINVAL, std::string(f) + ": gradient buffers must be 16-byte aligned");
+  for (int j = 0; j < W; ++j)
+    if (!saved_steps[j] || !s[j]) return fail(JAGG_EINVAL, std::string(f) + ": null saved_j or s_j");
+  if (!decreasing(t, W)) return fail(JAGG_EINVAL, std::string(f) + ": t must be strictly decreasing");
+  jg::Ws W0;
+  jagg_status st = need_head_ws(ctx, W0, f);
+  if (st) return st;
+  const int gdt = ctx->m.grad;
+  const size_t n = ctx->m.total;
+  // the three group gradients of the window
+  st = jagg_group_backward(ctx, theta, saved_pair, batch, s, t, W, g_jagg, 0.f);
+  if (st) return st;
+  st = perstep_group_backward(ctx, theta, saved_steps, batch, s, W, g_exact, 0.f);
+  if (st) return st;
+  // ablation: the endpoint signals alone, weight one each (alpha = (0, 1))
+  const void* s2[2] = {s[0], s[W - 1]};
+  const float t2[2] = {t[0], t[W - 1]};
+  st = jagg_group_backward(ctx, theta, saved_pair, batch, s2, t2, 2, g_ablate, 0.f);
+  if (st) return st;
+  double q[5];
+  st = jagg_grad_compare(ctx, g_jagg, g_exact, n, gdt, q);
+  if (st) return st;
+  out[0] = q[3];
+  out[1] = q[4];
+  st = jagg_grad_compare(ctx, g_ablate, g_exact, n, gdt, q);
+  if (st) return st;
+  out[2] = q[3];
+  out[3] = q[4];
   return JAGG_OK;
 }
 
@@ -1113,8 +1180,8 @@ static jagg_status grpo_args(const jagg_ctx* ctx, const jagg_grpo_window* w, int
   if (W < 2 || W > jg::GRPO_MAX_W) return fail(JAGG_EINVAL, f + ": W must be 2..16");
   if (!(w->clip_eps >= 0.f) || !(w->adv_clip > 0.f)) return fail(JAGG_EINVAL, f + ": bad clip range or advantage clamp");
   std::memset(&a, 0, sizeof(a));
+  if (!decreasing(w->t, W + 1)) return fail(JAGG_EINVAL, f + ": t_0 .. t_W must be strictly decreasing");
   const double t0 = w->t[0], den = (double)w->t[0] - (double)w->t[W - 1];
-  if (den == 0.0) return fail(JAGG_EINVAL, f + ": t_0 == t_{W-1}");
   for (int j = 0; j < W; ++j) {
     if (!(w->sigma[j] > 0.f)) return fail(JAGG_EINVAL, f + ": sigma_j must be positive");
     if (!w->v_hat[j] || (uintptr_t)w->v_hat[j] % 16) return fail(JAGG_EINVAL, f + ": null or unaligned v_j");
@@ -1155,11 +1222,9 @@ static jagg_status grpo_args(const jagg_ctx* ctx, const jagg_grpo_window* w, int
 }
 
 static jagg_status grpo_run(jagg_ctx* ctx, jg::GrpoArgs& a, double* stats) {
-  if (!ctx->ws) return fail(JAGG_EINVAL, "GRPO window: workspace not bound");
   jg::Ws W0;
-  jg::plan_ws(ctx->m, 1, ctx->ws, W0);
-  if ((char*)W0.gcoef + (size_t)jg::GRPO_MAX_W * 32 * sizeof(float) > (char*)ctx->ws + ctx->ws_bytes)
-    return fail(JAGG_EINVAL, "GRPO window: workspace too small");
+  jagg_status st = need_head_ws(ctx, W0, "GRPO window");
+  if (st) return st;
   return to_status(jg::grpo_window(a, W0.spart, W0.gcoef, stats, ctx->stream));
 }
 
@@ -1229,9 +1294,57 @@ jagg_status perstep_group_backward(jagg_ctx* ctx, const void* theta, const void*
                                    const void* const* s, int W, void* dtheta, float beta) {
   if (!ctx || !theta || !saved || !s || !dtheta) return fail(JAGG_EINVAL, "perstep_group_backward: null argument");
   if (W < 1 || W > 64) return fail(JAGG_EINVAL, "perstep_group_backward: W must be 1..64");
+  for (int j = 0; j < W; ++j)
+    if (!saved[j] || !s[j]) return fail(JAGG_EINVAL, "perstep_group_backward: null saved_j or s_j");
   for (int j = 0; j < W; ++j) {
     jagg_status st = dit_vjp(ctx, theta, saved[j], batch, s[j], dtheta, j == 0 ? beta : 1.f);
     if (st) return st;
+  }
+  return JAGG_OK;
+}
+
+jagg_status jagg_trajectory_backward(jagg_ctx* ctx, const void* theta, int T, int W, int batch,
+                                     const void* const* saved_pairs, const void* const* saved_steps,
+                                     const void* const* s, const float* t, const unsigned char* use_jagg,
+                                     void* dtheta, float beta) {
+  const char* f = "jagg_trajectory_backward";
+  if (!ctx || !theta || !s || !t || !dtheta) return fail(JAGG_EINVAL, std::string(f) + ": null argument");
+  if (W < 2 || W > 64 || T < 1) return fail(JAGG_EINVAL, std::string(f) + ": need 2 <= W <= 64 and T >= 1");
+  if (beta != 0.f && beta != 1.f) return fail(JAGG_EINVAL, std::string(f) + ": beta must be 0 or 1");
+  if (!decreasing(t, T)) return fail(JAGG_EINVAL, std::string(f) + ": t must be strictly decreasing");
+  const int n_full = T / W;
+  if (n_full > 0 && !use_jagg) return fail(JAGG_EINVAL, std::string(f) + ": use_jagg is required");
+  bool any_jagg = false;
+  // every pointer a pass will read, checked before the first launch
+  for (int g = 0; g <= n_full; ++g) {
+    const int k0 = g * W, k1 = g < n_full ? k0 + W : T;
+    if (k0 >= k1) continue;
+    const bool j = g < n_full && use_jagg[g] == 1;
+    if (g < n_full && use_jagg[g] > 1) return fail(JAGG_EINVAL, std::string(f) + ": use_jagg entries must be 0 or 1");
+    if (j) {
+      if (!saved_pairs || !saved_pairs[g]) return fail(JAGG_EINVAL, std::string(f) + ": null saved pair of a JAGG window");
+      if (batch < 1 || 2 * batch > MAX_BATCH) return fail(JAGG_EINVAL, std::string(f) + ": batch must be 1..16");
+      any_jagg = true;
+    }
+    for (int k = k0; k < k1; ++k) {
+      if (!s[k] || (uintptr_t)s[k] % 16) return fail(JAGG_EINVAL, std::string(f) + ": null or unaligned s_k");
+      if (!j && (!saved_steps || !saved_steps[k]))
+        return fail(JAGG_EINVAL, std::string(f) + ": null saved forward of a per-step step");
+    }
+  }
+  if (batch < 1 || batch > MAX_BATCH) return fail(JAGG_EINVAL, std::string(f) + ": batch must be 1..32");
+  jagg_status st = need_ws(ctx, any_jagg ? 2 * batch : batch);
+  if (st) return st;
+  float b = beta;
+  for (int g = 0; g <= n_full; ++g) {
+    const int k0 = g * W, k1 = g < n_full ? k0 + W : T;
+    if (k0 >= k1) continue;
+    if (g < n_full && use_jagg[g])
+      st = jagg_group_backward(ctx, theta, saved_pairs[g], batch, s + k0, t + k0, W, dtheta, b);
+    else
+      st = perstep_group_backward(ctx, theta, saved_steps + k0, batch, s + k0, k1 - k0, dtheta, b);
+    if (st) return st;
+    b = 1.f;
   }
   return JAGG_OK;
 }

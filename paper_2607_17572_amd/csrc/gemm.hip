@@ -16,6 +16,7 @@
 //
 // Anything else (fp32 operands, contiguous dims not multiple of 8) takes a
 // plain LDS-tiled VALU kernel with fp32 accumulation.
+#include <atomic>
 #include "gemm.h"
 #include <type_traits>
 #include "prof.h"
@@ -1073,27 +1074,30 @@ static int launch_mfma(const GemmArgs& g, hipStream_t s) {
   void (*kern)(GemmArgs);
   if constexpr (PIPE) kern = gemm_pipe_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
   else kern = gemm_mfma_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
-  static bool attr = false;
-  if (!attr) {
+  // the dynamic-LDS limit is a per-device attribute of the kernel: set once
+  // per device (bit d of `attr`), safe to race (the call is idempotent)
+  static std::atomic<unsigned long long> attr{0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev > 63) {
+    set_error("gemm_mfma: no current device");
+    return 3;
+  }
+  if (!(attr.load(std::memory_order_acquire) & (1ull << dev))) {
     if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
       set_error("gemm_mfma: cannot reserve the LDS tile stages");
       return 3;
     }
-    attr = true;
+    attr.fetch_or(1ull << dev, std::memory_order_acq_rel);
   }
-  hipLaunchKernelGGL(kern, dim3(tiles), dim3(WM * WN * 64), lds, s, g);
+  launch(kern, dim3(tiles), dim3(WM * WN * 64), (uint32_t)lds, s, g);
   JG_CHECK_LAUNCH("gemm_mfma");
   return 0;
 }
 
-// Tile configuration override for tuning: 0 = default choice.
-static int g_tile_cfg = 0;
-void gemm_set_tile_cfg(int c) { g_tile_cfg = c; }
-
 template <bool TA, bool TB, int EK, int BM, int BN, int WM = 2, int WN = 2>
 static int launch_dtl(const GemmArgs& g, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_dtl_kernel<TA, TB, EK, BM, BN, WM, WN>), dim3(tiles), dim3(64 * WM * WN), 0, s, g);
+  launch(gemm_dtl_kernel<TA, TB, EK, BM, BN, WM, WN>, dim3(tiles), dim3(64 * WM * WN), 0u, s, g);
   JG_CHECK_LAUNCH("gemm_dtl");
   return 0;
 }
@@ -1197,9 +1201,9 @@ static int prof_class(const GemmArgs& g) {
 static int gemm_launch(const GemmArgs& g, hipStream_t s);
 
 int gemm(const GemmArgs& g, hipStream_t s) {
-  const int pi = prof_begin(prof_class(g), s);
+  const int pi = prof_begin(prof_class(g));
   const int rc = gemm_launch(g, s);
-  prof_end(pi, s, 2.0 * g.M * g.N * (double)g.K);
+  prof_end(pi, 2.0 * g.M * g.N * (double)g.K);
   return rc;
 }
 
@@ -1227,24 +1231,21 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
     // fills whole rounds of 256 CUs; the forward product takes the 8-wave
     // register-staged 256x256 kernel, or 128x128 for grids too small to
     // cover a quarter of the chip
-    int cfg = g_tile_cfg;
-    if (cfg == 0) {
-      const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-      if (g.tb && dtl_fits(g)) cfg = 8;
-      else if (t256 < 64) cfg = 1;
-      else if (!g.ta && !g.tb) cfg = 6;
-      else cfg = 4;
-    }
+    const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
+    int cfg;
+    if (g.tb && dtl_fits(g)) cfg = 8;
+    else if (t256 < 64) cfg = 1;
+    else if (!g.ta && !g.tb) cfg = 6;
+    else cfg = 4;
     if (!g.ta && !g.tb) return launch_kind<false, false>(g, s, cfg, ek);
     if (!g.ta && g.tb) return launch_kind<false, true>(g, s, cfg, ek);
     if (g.ta && g.tb) return launch_kind<true, true>(g, s, cfg, ek);
     return launch_kind<true, false>(g, s, cfg, ek);
   }
+  // the VALU kernel also covers an empty contraction (K = 0): it still
+  // applies the epilogue (bias, beta)
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
-  if (g.K == 0) {
-    // an empty contraction still applies the epilogue (bias, beta)
-  }
-  hipLaunchKernelGGL(gemm_valu_kernel, grid, dim3(256), 0, s, g);
+  launch(gemm_valu_kernel, grid, dim3(256), 0u, s, g);
   JG_CHECK_LAUNCH("gemm_valu");
   return 0;
 }

@@ -1409,25 +1409,28 @@ __global__ __launch_bounds__(256) void aggregate_k(AggArgs a) {
       for (int e = 0; e < 8; ++e) { sb[e] = fmaf(wb, x[e], sb[e]); sc[e] = fmaf(wc, x[e], sc[e]); }
     }
     const size_t e0 = v * 8;
-    TO* db;
-    TO* dc;
-    if (e0 < a.split) { db = (TO*)a.base0 + e0; dc = (TO*)a.corr0 + e0; }
-    else { db = (TO*)a.base1 + (e0 - a.split); dc = (TO*)a.corr1 + (e0 - a.split); }
-    // a null destination skips that composite (one endpoint of the sequential variant)
+    // the destinations of this element's segment; a null destination skips
+    // that composite (one endpoint of the sequential variant)
+    const bool lo = e0 < a.split;
+    TO* const db0 = (TO*)(lo ? a.base0 : a.base1);
+    TO* const dc0 = (TO*)(lo ? a.corr0 : a.corr1);
+    const size_t off = lo ? e0 : e0 - a.split;
+    TO* const db = db0 ? db0 + off : nullptr;
+    TO* const dc = dc0 ? dc0 + off : nullptr;
     if constexpr (sizeof(TO) == 2) {
       uint4 ub, uc;
       ub.x = f2bf(sb[0]) | ((uint32_t)f2bf(sb[1]) << 16); ub.y = f2bf(sb[2]) | ((uint32_t)f2bf(sb[3]) << 16);
       ub.z = f2bf(sb[4]) | ((uint32_t)f2bf(sb[5]) << 16); ub.w = f2bf(sb[6]) | ((uint32_t)f2bf(sb[7]) << 16);
       uc.x = f2bf(sc[0]) | ((uint32_t)f2bf(sc[1]) << 16); uc.y = f2bf(sc[2]) | ((uint32_t)f2bf(sc[3]) << 16);
       uc.z = f2bf(sc[4]) | ((uint32_t)f2bf(sc[5]) << 16); uc.w = f2bf(sc[6]) | ((uint32_t)f2bf(sc[7]) << 16);
-      if (a.base0) *(uint4*)db = ub;
-      if (a.corr0) *(uint4*)dc = uc;
+      if (db) *(uint4*)db = ub;
+      if (dc) *(uint4*)dc = uc;
     } else {
-      if (a.base0) {
+      if (db) {
         *(float4*)db = make_float4(sb[0], sb[1], sb[2], sb[3]);
         *(float4*)(db + 4) = make_float4(sb[4], sb[5], sb[6], sb[7]);
       }
-      if (a.corr0) {
+      if (dc) {
         *(float4*)dc = make_float4(sc[0], sc[1], sc[2], sc[3]);
         *(float4*)(dc + 4) = make_float4(sc[4], sc[5], sc[6], sc[7]);
       }
@@ -1462,11 +1465,11 @@ int aggregate(const AggArgs& a, hipStream_t s) {
   const uintptr_t al = (uintptr_t)a.base0 | (uintptr_t)a.base1 | (uintptr_t)a.corr0 | (uintptr_t)a.corr1;
   vec = vec && (al % 16 == 0);
   for (int j = 0; j < a.W; ++j) vec = vec && ((uintptr_t)a.s[j] % 16 == 0);
-  const int pi = prof_begin(PROF_AGGREGATE, s);
+  const int pi = prof_begin(PROF_AGGREGATE);
   if (vec) {
     const size_t nv = a.n / 8;
     const unsigned grid = (unsigned)std::min<size_t>((nv + 255) / 256, 256 * 16);
-#define AGG(TI, TO) hipLaunchKernelGGL((aggregate_k<TI, TO>), dim3(grid), dim3(256), 0, s, a)
+#define AGG(TI, TO) launch(aggregate_k<TI, TO>, dim3(grid), dim3(256), 0u, s, a)
     if (a.in_dt == BF16 && a.out_dt == BF16) AGG(uint16_t, uint16_t);
     else if (a.in_dt == BF16) AGG(uint16_t, float);
     else if (a.out_dt == BF16) AGG(float, uint16_t);
@@ -1474,9 +1477,9 @@ int aggregate(const AggArgs& a, hipStream_t s) {
 #undef AGG
   } else {
     const unsigned grid = (unsigned)std::min<size_t>((a.n + 255) / 256, 256 * 16);
-    hipLaunchKernelGGL(aggregate_scalar_k, dim3(grid), dim3(256), 0, s, a, (size_t)0);
+    launch(aggregate_scalar_k, dim3(grid), dim3(256), 0u, s, a, (size_t)0);
   }
-  prof_end(pi, s, (double)a.n * ((double)a.W * dsize(a.in_dt) + 2.0 * dsize(a.out_dt)));
+  prof_end(pi, (double)a.n * ((double)a.W * dsize(a.in_dt) + 2.0 * dsize(a.out_dt)));
   LAUNCH_OK("aggregate");
   return 0;
 }
@@ -1627,11 +1630,11 @@ int grad_compare(const void* a, const void* b, size_t n, int dt, double* part, d
   if ((((uintptr_t)a | (uintptr_t)b) & 15) != 0) { set_error("grad_compare: vectors must be 16-byte aligned"); return 1; }
   const size_t nv = n / 8;
   const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nv + 255) / 256, CMP_BLOCKS));
-  const int pi = prof_begin(PROF_COMPARE, s);
-  if (dt == BF16) hipLaunchKernelGGL(compare_pass1_k<uint16_t>, dim3(grid), dim3(256), 0, s, (const uint16_t*)a,
-                                     (const uint16_t*)b, n, part);
-  else hipLaunchKernelGGL(compare_pass1_k<float>, dim3(grid), dim3(256), 0, s, (const float*)a, (const float*)b, n, part);
-  prof_end(pi, s, 2.0 * (double)n * dsize(dt));
+  const int pi = prof_begin(PROF_COMPARE);
+  if (dt == BF16) launch(compare_pass1_k<uint16_t>, dim3(grid), dim3(256), 0u, s, (const uint16_t*)a, (const uint16_t*)b, n,
+                         part);
+  else launch(compare_pass1_k<float>, dim3(grid), dim3(256), 0u, s, (const float*)a, (const float*)b, n, part);
+  prof_end(pi, 2.0 * (double)n * dsize(dt));
   LAUNCH_OK("grad_compare_pass1");
   hipLaunchKernelGGL(compare_pass2_k, dim3(1), dim3(64), 0, s, part, (int)grid, out_dev);
   LAUNCH_OK("grad_compare_pass2");
@@ -1788,14 +1791,24 @@ __global__ __launch_bounds__(256) void grpo_out_k(GrpoArgs a, const float* coef)
   }
 }
 
+// The three kernels of a window; under timing each is its own record (work in
+// bytes: pass 1 reads z_0..z_W and the v_j, the closed-form scalars move
+// nothing of size, pass 2 reads them again and writes the composites or s_j).
 template <typename T, int W>
 static void grpo_launch(const GrpoArgs& a, double* part, float* coef, double* stats, hipStream_t s) {
   const int ch = grpo_blocks(a.W, a.B);
-  hipLaunchKernelGGL((grpo_sq_k<T, W>), dim3(ch, a.B), dim3(256), 0, s, a, part);
-  hipLaunchKernelGGL(grpo_coef_k, dim3(a.W * a.B), dim3(256), 0, s, a, part, ch, coef, stats);
+  const double es = dsize(a.dt), pass = (double)a.n * es * (2 * a.W + 1);
+  int pi = prof_begin(PROF_UPSTREAM);
+  launch(grpo_sq_k<T, W>, dim3(ch, a.B), dim3(256), 0u, s, a, part);
+  prof_end(pi, pass);
+  pi = prof_begin(PROF_UPSTREAM);
+  launch(grpo_coef_k, dim3(a.W * a.B), dim3(256), 0u, s, a, part, ch, coef, stats);
+  prof_end(pi, 0.0);
   const size_t nv = a.n / 8;
   const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nv + 255) / 256, 256 * 16));
-  hipLaunchKernelGGL((grpo_out_k<T, W>), dim3(grid), dim3(256), 0, s, a, coef);
+  pi = prof_begin(PROF_UPSTREAM);
+  launch(grpo_out_k<T, W>, dim3(grid), dim3(256), 0u, s, a, coef);
+  prof_end(pi, pass + (double)a.n * es * (a.mode == 1 ? a.W : 2));
 }
 
 int grpo_window(const GrpoArgs& a, double* part, float* coef, double* stats, hipStream_t s) {
@@ -1804,7 +1817,6 @@ int grpo_window(const GrpoArgs& a, double* part, float* coef, double* stats, hip
     set_error("grpo_window: per-sample segments must be multiples of 8 elements");
     return 4;
   }
-  const int pi = prof_begin(PROF_UPSTREAM, s);
 #define GRPO_W(T, w) case w: grpo_launch<T, w>(a, part, coef, stats, s); break;
   if (a.dt == BF16) {
     switch (a.W) { GRPO_W(uint16_t, 2) GRPO_W(uint16_t, 3) GRPO_W(uint16_t, 4) GRPO_W(uint16_t, 5) GRPO_W(uint16_t, 6)
@@ -1817,8 +1829,6 @@ int grpo_window(const GrpoArgs& a, double* part, float* coef, double* stats, hip
       default: set_error("grpo_window: W must be one of 2..8, 10, 12, 16"); return 4; }
   }
 #undef GRPO_W
-  const double es = dsize(a.dt);
-  prof_end(pi, s, (double)a.n * es * (2.0 * (2 * a.W + 1) + (a.mode == 1 ? a.W : 2)));
   LAUNCH_OK("grpo_window");
   return 0;
 }

@@ -71,6 +71,10 @@ def test_alpha_host_matches_oracle():
         pk.alpha([0.5])
     with pytest.raises(pk.JaggError):
         pk.alpha([0.5, 0.2, 0.5])
+    with pytest.raises(pk.JaggError):
+        pk.alpha([0.3, 0.5])            # increasing: not a denoising window
+    with pytest.raises(pk.JaggError):
+        pk.alpha([0.9, 0.95, 0.3])      # not monotone
 
 
 def test_route_host_bit_exact_against_oracle():
@@ -143,7 +147,7 @@ def test_variant_entry_points_reject_bad_arguments():
         assert L.jagg_endpoint_backward(h, p, p, 1, s2, t2, 2, 0, p, 0.5) == 1
         assert L.jagg_endpoint_backward(h, p, p, 0, s2, t2, 2, 0, p, 0.0) == 1
         assert L.jagg_endpoint_backward(h, p, None, 1, s2, t2, 2, 0, p, 0.0) == 1
-        out = (ctypes.c_double * 3)()
+        out = (ctypes.c_double * 5)()
         assert L.jagg_grad_compare(h, p, p, 0, 0, out) == 1          # empty
         assert L.jagg_grad_compare(h, p, p + 4, 8, 0, out) == 1      # unaligned
         assert L.jagg_grad_compare(h, p, p, 8, 5, out) == 1          # dtype
@@ -193,5 +197,87 @@ def test_grpo_entry_points_reject_bad_arguments():
         assert L.jagg_grpo_upstream(h, ctypes.byref(ok), 1, unal, None) == 1           # unaligned s_j
         assert L.jagg_grpo_group_backward(h, p, p, 1, ctypes.byref(ok), p, 0.5, None) == 1  # beta
         assert L.jagg_grpo_composites(h, ctypes.byref(ok), 1, p, p, None) == 1          # no workspace
+    finally:
+        L.jagg_ctx_destroy(h)
+
+
+def test_workspace_head_too_small_is_rejected_before_any_launch():
+    """The scoring, comparison and GRPO calls use the batch-independent head of
+    the workspace (partial sums, score slot, GRPO coefficients); a bound
+    workspace shorter than that head is an argument error, whatever its size
+    relative to the scoring partials alone."""
+    L = _lib_or_skip()
+    import ctypes
+    c = pk.config("tiny").c()
+    h = ctypes.c_void_p()
+    assert L.jagg_ctx_create(ctypes.byref(c), None, ctypes.byref(h)) == 0
+    try:
+        p = 1 << 20  # a fake, aligned device address: never dereferenced
+        score = ctypes.c_double()
+        hs = (ctypes.c_void_p * 4)(*[p] * 4)
+        out = (ctypes.c_double * 5)()
+        for nbytes in (147712, 200000, 262144):
+            assert L.jagg_ctx_set_workspace(h, ctypes.c_void_p(p), nbytes) == 0
+            assert L.jagg_group_scores(h, hs, 1024, 4, 0, ctypes.byref(score)) == 1
+            assert b"head" in L.jagg_last_error()
+            assert L.jagg_grad_compare(h, p, p, 1024, 0, out) == 1
+    finally:
+        L.jagg_ctx_destroy(h)
+
+
+def test_trajectory_and_quality_reject_bad_arguments():
+    """Trajectory backward and window quality: every argument error is found
+    on the host before the first launch (no workspace is bound, so a call that
+    passed validation would fail on that instead)."""
+    L = _lib_or_skip()
+    import ctypes
+    c = pk.config("tiny").c()
+    h = ctypes.c_void_p()
+    assert L.jagg_ctx_create(ctypes.byref(c), None, ctypes.byref(h)) == 0
+    try:
+        p = 1 << 20
+        T, W = 10, 4
+        vp = ctypes.c_void_p
+        steps = (vp * T)(*[p] * T)
+        pairs = (vp * 2)(p, p)
+        s = (vp * T)(*[p] * T)
+        t = (ctypes.c_float * T)(*[1.0 - k / T for k in range(T)])
+        mask = (ctypes.c_ubyte * 2)(1, 0)
+
+        def call(**kw):
+            a = dict(T=T, W=W, batch=1, pairs=pairs, steps=steps, s=s, t=t, mask=mask, beta=0.0)
+            a.update(kw)
+            r = L.jagg_trajectory_backward(h, p, a["T"], a["W"], a["batch"], a["pairs"], a["steps"], a["s"], a["t"],
+                                           a["mask"], p, a["beta"])
+            return r, L.jagg_last_error()
+
+        r, e = call()
+        assert r == 1 and b"workspace" in e                      # valid arguments: stops at the workspace
+        t_up = (ctypes.c_float * T)(*[0.1 + k / T for k in range(T)])
+        assert call(t=t_up)[0] == 1                              # t increasing
+        assert call(mask=(ctypes.c_ubyte * 2)(2, 0))[0] == 1     # mask byte not 0/1
+        assert call(W=1)[0] == 1
+        assert call(T=0)[0] == 1
+        assert call(beta=0.5)[0] == 1
+        assert call(pairs=(vp * 2)(None, p))[0] == 1             # JAGG window without its pair
+        r, e = call(pairs=(vp * 2)(p, None))                     # per-step window needs no pair
+        assert r == 1 and b"workspace" in e
+        st = (vp * T)(*([p] * 4 + [None] + [p] * 5))
+        assert call(steps=st)[0] == 1                            # per-step step 4 without its forward
+        st = (vp * T)(*([None] + [p] * 9))
+        r, e = call(steps=st)                                    # step 0 is in a JAGG window
+        assert r == 1 and b"workspace" in e
+        assert call(s=(vp * T)(*([p] * 9 + [p + 4])))[0] == 1   # unaligned s_k
+        assert call(batch=17)[0] == 1                            # a JAGG window's pair would exceed 32
+        r, e = call(mask=None, T=3)                              # no full window: no mask needed
+        assert r == 1 and b"workspace" in e
+        out = (ctypes.c_double * 4)()
+        st4 = (vp * 4)(*[p] * 4)
+        t4 = (ctypes.c_float * 4)(1.0, 0.9, 0.8, 0.7)
+        assert L.jagg_window_quality(h, p, p, st4, 1, st4, t4, 1, p, p, p, out) == 1    # W < 2
+        assert L.jagg_window_quality(h, p, p, st4, 1, st4, t4, 4, p, p + 8, p, out) == 1  # unaligned
+        t4b = (ctypes.c_float * 4)(1.0, 0.9, 0.95, 0.7)
+        assert L.jagg_window_quality(h, p, p, st4, 1, st4, t4b, 4, p, p, p, out) == 1  # t not decreasing
+        assert L.jagg_window_quality(h, p, None, st4, 1, st4, t4, 4, p, p, p, out) == 1
     finally:
         L.jagg_ctx_destroy(h)

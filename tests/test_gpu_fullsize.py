@@ -68,3 +68,45 @@ def test_fullsize_grpo_composites_match_oracle():
     eb, ec = rel_l2(sb.double().cpu().numpy(), wb), rel_l2(sc.double().cpu().numpy(), wc)
     print(f"full-size GRPO composites rel L2 {eb:.2e} {ec:.2e}", flush=True)
     assert eb <= 8e-3 and ec <= 8e-3
+
+
+# Full-width slice: one double-stream and one single-stream block at the
+# model width of the Flux-like workloads (hidden 3072, 24 x 128 heads, MLP
+# 12288, text width 4096, 16 latent channels, 2x2 patches), with the full
+# embeddings and final layer, at token counts the oracle runs in seconds.
+WIDE = dict(n_double=1, n_single=1, hidden=3072, heads=24, head_dim=128, mlp_hidden=12288, in_ch=16, patch=2,
+            txt_dim=4096, t_freq_dim=256, act_dtype=pk.BF16)
+
+
+@pytest.mark.parametrize("B,lat,n_txt", [(2, 32, 64), (8, 16, 32)], ids=["batch2_256+64", "batch8_64+32"])
+def test_fullwidth_slice_matches_oracle(B, lat, n_txt):
+    """JAGG group backward (W = 4, batch-2B endpoint pair) of the full-width
+    slice against the fp32 oracle on the same bf16-rounded values, with fp32
+    and with bf16 parameter gradients; raw per-tensor and global relative L2
+    <= 2e-2.  The batch-8 case also runs the per-step baseline into a bf16
+    gradient (four accumulating VJPs, the bf16 accumulate epilogue)."""
+    import dataclasses
+    print(f"case: full-width slice 1d+1s, batch {B}, {lat // 2}^2 image + {n_txt} text tokens", flush=True)
+    cfg = pk.Config(**WIDE, lat_h=lat, lat_w=lat, n_txt=n_txt, grad_dtype=pk.F32)
+    cs = Case(cfg, B=B, W=4, T=16)
+    got32 = cs.gpu_jagg()
+    ctx16 = pk.Context(dataclasses.replace(cfg, grad_dtype=pk.BF16))
+    sv = cs.saved_pair()
+    got16 = torch.zeros(ctx16.n_params, dtype=torch.bfloat16, device="cuda")
+    ctx16.group_backward(cs.theta_dev, sv, B, cs.s_dev, cs.t, got16, 0.0)
+    ps16 = None
+    if B == 8:
+        saved = [cs.forward(j)[1] for j in range(cs.W)]
+        ps16 = torch.zeros_like(got16)
+        ctx16.perstep_group_backward(cs.theta_dev, saved, B, cs.s_dev, ps16, 0.0)
+    torch.cuda.synchronize()
+    print("gpu done; running oracle (fp32)", flush=True)
+    want = cs.oracle_jagg(dtype=np.float32)
+    eg, worst = compare_grads(cs, got32, want, 2e-2, report=True)
+    print(f"  fp32 dtheta: rel L2 {eg:.3e}, worst tensor {worst}", flush=True)
+    eg, worst = compare_grads(cs, got16, want, 2e-2, report=True)
+    print(f"  bf16 dtheta: rel L2 {eg:.3e}, worst tensor {worst}", flush=True)
+    if ps16 is not None:
+        want_e = cs.oracle_exact(dtype=np.float32)
+        eg, worst = compare_grads(cs, ps16, want_e, 2e-2, report=True)
+        print(f"  per-step, bf16 dtheta: rel L2 {eg:.3e}, worst tensor {worst}", flush=True)

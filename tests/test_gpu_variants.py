@@ -77,6 +77,10 @@ def test_grad_compare_sums(n, dt):
     want = (float(x @ y), float(x @ x), float(y @ y))
     for g, w in zip(got, want):
         assert abs(g - w) <= 1e-12 * max(1.0, abs(want[1]) + abs(want[2])), (got, want)
+    # the library's quality figures: cos = a.b / sqrt(a.a b.b), rho = sqrt(a.a / b.b)
+    cos = float(x @ y) / (np.linalg.norm(x) * np.linalg.norm(y))
+    rho = np.linalg.norm(x) / np.linalg.norm(y)
+    assert abs(got[3] - cos) <= 1e-10 and abs(got[4] - rho) <= 1e-10 * rho
 
 
 def test_gradient_quality_tool_matches_oracle():

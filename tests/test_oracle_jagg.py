@@ -189,3 +189,131 @@ def test_windows_with_tail():
     assert full == [list(range(8)), list(range(8, 16))] and tail == [16, 17, 18, 19]
     full, tail = jagg.windows(16, 4)
     assert len(full) == 4 and tail == []
+
+
+def test_alpha_rejects_non_monotone_windows():
+    with pytest.raises(ValueError):
+        jagg.alpha([0.9, 0.95, 0.3])
+    with pytest.raises(ValueError):
+        jagg.alpha([0.3, 0.5])  # increasing
+
+
+# ---------------------------------------------------------------- ablation
+def test_ablate_is_the_endpoint_only_backward():
+    """Endpoint-only ablation (Experiments): the gradient of
+    <v(z_0, t_0), s_0> + <v(z_{W-1}, t_{W-1}), s_{W-1}> with weight one each,
+    checked against central finite differences of that scalar in random
+    parameter directions.  It equals JAGG when the middle signals vanish
+    (then s_base = s_0 and s_corr = s_{W-1}) and differs otherwise."""
+    from test_oracle_model import loss
+    cfg = TINY
+    th = theta(cfg)
+    P = mmdit.unflatten(cfg, th)
+    W = 4
+    t, inps, ss = _window(cfg, W, 600)
+    ga = _flat(cfg, jagg.g_ablate(cfg, P, inps, ss))
+    rs = np.random.default_rng(7)
+    h = 1e-5
+    for _ in range(4):
+        d = rs.standard_normal(ga.shape[0])
+        f = lambda x: loss(cfg, x, inps[0], ss[0]) + loss(cfg, x, inps[W - 1], ss[W - 1])  # noqa: E731
+        fd = (f(th + h * d) - f(th - h * d)) / (2 * h)
+        assert abs(fd - float(np.dot(ga, d))) <= 1e-7 * max(1.0, abs(fd))
+    zero = np.zeros_like(ss[1])
+    ss0 = [ss[0], zero, zero, ss[3]]
+    np.testing.assert_allclose(_flat(cfg, jagg.g_jagg(cfg, P, inps, ss0, t)), ga, rtol=1e-12, atol=1e-13)
+    gj = _flat(cfg, jagg.g_jagg(cfg, P, inps, ss, t))
+    assert np.linalg.norm(gj - ga) > 1e-2 * np.linalg.norm(ga)
+
+
+# ------------------------------------------------------------- trajectory
+def _traj(cfg, T, seed, B=1):
+    t = synth.uniform_grid(T)
+    inps = [jagg.step_inputs(inputs(cfg, B, seed + 7 * j), t[j]) for j in range(T)]
+    ss = [cot(cfg, B, seed + 500 + 7 * j) for j in range(T)]
+    return t, inps, ss
+
+
+def _batched_vjp(cfg, th, inps, ss):
+    """One VJP over all steps stacked as one batch (batch additivity)."""
+    cat = lambda xs: None if xs[0] is None else np.concatenate(xs, axis=0)  # noqa: E731
+    inp = mmdit.Inputs(t=np.concatenate([i.t for i in inps]), z=cat([i.z for i in inps]),
+                       txt=cat([i.txt for i in inps]), x_txt=cat([i.x_txt for i in inps]),
+                       x_img=cat([i.x_img for i in inps]))
+    return mmdit.vjp_flat(cfg, th, inp, np.concatenate(ss, axis=0))
+
+
+def test_trajectory_per_step_and_w2_equal_one_batched_vjp():
+    """All windows per step (and W = 2, where JAGG is exact) give the plain
+    gradient of the whole trajectory, here formed as a single VJP of all T
+    steps stacked as one batch: every step, the tail included, counted once."""
+    cfg = TINY
+    th = theta(cfg)
+    P = mmdit.unflatten(cfg, th)
+    T = 7
+    t, inps, ss = _traj(cfg, T, 700)
+    want = _batched_vjp(cfg, th, inps, ss)
+    m, g = jagg.trajectory(cfg, P, inps, ss, t, 3, frac=0.0)     # windows [0..2], [3..5], tail [6]
+    assert list(m) == [0, 0]
+    np.testing.assert_allclose(_flat(cfg, g), want, rtol=1e-11, atol=1e-12)
+    m, g = jagg.trajectory(cfg, P, inps, ss, t, 2, frac=1.0)     # 3 JAGG windows of 2, tail [6]
+    assert list(m) == [1, 1, 1]
+    np.testing.assert_allclose(_flat(cfg, g), want, rtol=1e-11, atol=1e-12)
+
+
+def test_trajectory_final_bias_exact_and_routing_matters():
+    cfg = TINY
+    th = theta(cfg)
+    P = mmdit.unflatten(cfg, th)
+    T, W = 10, 4                                               # windows [0..3], [4..7], tail [8, 9]
+    t, inps, ss = _traj(cfg, T, 800)
+    _, g_j = jagg.trajectory(cfg, P, inps, ss, t, W, mask=[1, 1])
+    _, g_e = jagg.trajectory(cfg, P, inps, ss, t, W, mask=[0, 0])
+    want_b = sum(mmdit.patchify(cfg, s).sum(axis=(0, 1)) for s in ss)
+    np.testing.assert_allclose(g_j["final.b"], want_b, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(g_e["final.b"], want_b, rtol=1e-12, atol=1e-13)
+    fj, fe = _flat(cfg, g_j), _flat(cfg, g_e)
+    assert np.linalg.norm(fj - fe) > 1e-3 * np.linalg.norm(fe)
+    # a mixed mask changes only its window: (JAGG, per step) - (per step, per step)
+    # equals (JAGG, JAGG) - (per step, JAGG)
+    _, g_10 = jagg.trajectory(cfg, P, inps, ss, t, W, mask=[1, 0])
+    _, g_01 = jagg.trajectory(cfg, P, inps, ss, t, W, mask=[0, 1])
+    np.testing.assert_allclose(_flat(cfg, g_10) - fe, fj - _flat(cfg, g_01), rtol=1e-9, atol=1e-12)
+
+
+def test_trajectory_linear_toy_exact_on_each_windows_path():
+    """Theorem 1 window by window: when every window's latents lie on its own
+    affine path in alpha, the all-JAGG trajectory gradient (tail per step)
+    equals the exact one; off the paths it does not."""
+    toy = _toy()
+    T, W = 10, 4
+    t = synth.uniform_grid(T)
+    zs = []
+    for g in range(T // W):
+        a = jagg.alpha(t[g * W:(g + 1) * W])
+        za, zb = synth.normal(64, 40 + g), synth.normal(64, 50 + g)
+        zs += [(1 - aj) * za + aj * zb for aj in a]
+    zs += [synth.normal(64, 60 + k) for k in range(T % W)]
+    ss = [synth.normal(64, 70 + k) for k in range(T)]
+    ge = toy.g_exact(zs, t, ss)
+    for x, y in zip(ge, toy.trajectory(zs, t, ss, W, [1, 1])):
+        np.testing.assert_allclose(y, x, rtol=1e-12, atol=1e-14)
+    zs_off = [synth.normal(64, 90 + k) for k in range(T)]
+    dA = toy.trajectory(zs_off, t, ss, W, [1, 1])[0] - toy.g_exact(zs_off, t, ss)[0]
+    assert np.linalg.norm(dA) > 0.1 * np.linalg.norm(toy.g_exact(zs_off, t, ss)[0])
+
+
+def test_trajectory_plan_routing_and_tail():
+    """T = 20, W = 8: two full windows and a 4-step per-step tail; with half
+    the windows falling back, window 0 (highest noise) takes JAGG.  T = 20,
+    W = 4 with the gradient-quality table's QwenImage cosines: 3 JAGG windows."""
+    plan = jagg.trajectory_plan(20, 8, jagg.route(2, frac=0.5)[0])
+    assert plan == [(list(range(8)), True), (list(range(8, 16)), False), ([16, 17, 18, 19], False)]
+    g = json.load(open(GOLDEN))
+    m, _ = jagg.route(5, scores=g["models"]["QwenImage"]["cos"], tau=g["tau"])
+    plan = jagg.trajectory_plan(20, 4, m)
+    assert [u for _, u in plan] == [True, True, True, False, False] and plan[-1][0] == [16, 17, 18, 19]
+    with pytest.raises(ValueError):
+        jagg.trajectory_plan(20, 8, [1, 0, 1])
+    with pytest.raises(ValueError):
+        jagg.trajectory(TINY, None, [None] * 3, [None] * 3, [0.5, 0.6, 0.1], 2)

@@ -225,3 +225,62 @@ def test_param_counts_match_architecture_sizes():
     D = 3072
     assert dbl == 36 * D * D + 2 * (6 * D + 3 * D + D + 4 * D + D + 2 * 128)
     assert sgl == 15 * D * D + 3 * D + 7 * D + D + 2 * 128
+
+
+def test_attention_composition_worked_example():
+    """One double block, one head of Dh = 4, one text token and a 2 x 2 image
+    grid, written so that the block's output minus its input is the attention
+    output itself: modulation weights zero with gate1 = 1 and every other
+    chunk 0, query and key rows of the qkv projection zero with bias (1, 1, 1,
+    1), value rows the identity, output projection the identity, MLP gate 0.
+    Every token row has mean 0 and variance 1, so LayerNorm divides it by
+    r = sqrt(1 + eps), and the RMS of the all-ones query/key bias is the same r.
+
+    Worked by hand: the normalised query of a token is g_q / r (its stream's
+    gain), the key g_k / r; RoPE turns pair (0,1) by the token's grid row and
+    pair (2,3) by its grid column (frequency 1 for Dh = 4; text at (0, 0)).
+    For rotations R(a), R(b): R(a)x . R(b)y = (x0 y0 + x1 y1) cos(b - a) +
+    (x1 y0 - x0 y1) sin(b - a), so the logit of query i and key j is half the
+    sum of that expression over the two pairs; the probabilities are the
+    softmax of row i over the keys j, and the output of token i is
+    sum_j p_ij x_j / r.  The gains differ within each pair, so RoPE applied
+    before the RMSNorm gain, pairs taken as halves instead of interleaved,
+    another logit scale, or a softmax over queries would all change it."""
+    import math
+    cfg = mmdit.Config(n_double=1, n_single=0, hidden=4, heads=1, head_dim=4, mlp_hidden=4, patch=1,
+                       lat_h=2, lat_w=2, n_txt=1, t_freq_dim=4, block_only=True)
+    P = mmdit.unflatten(cfg, np.zeros(mmdit.param_layout(cfg)[1]))
+    gains = {"txt": ((1.5, 0.5, 1.0, 2.0), (1.0, 2.0, 0.5, 1.0)),
+             "img": ((0.5, 2.5, 2.0, 1.0), (2.0, 0.5, 1.0, 1.5))}
+    for s in ("txt", "img"):
+        pre = f"double.0.{s}."
+        P[pre + "mod.b"][8:12] = 1.0                       # gate1
+        P[pre + "qkv.b"][0:8] = 1.0                        # query and key bias
+        P[pre + "qkv.w"][8:12] = np.eye(4)                 # value = normalised input
+        P[pre + "o.w"][:] = np.eye(4)
+        P[pre + "q_gain"][:] = gains[s][0]
+        P[pre + "k_gain"][:] = gains[s][1]
+    rows = [(1, -1, 1, -1), (-1, 1, -1, 1), (1, 1, -1, -1), (-1, -1, 1, 1), (1, -1, -1, 1)]
+    pos = [(0, 0), (0, 0), (0, 1), (1, 0), (1, 1)]        # text token, then the image grid row-major
+    stream = ["txt", "img", "img", "img", "img"]
+    x = np.array(rows, dtype=np.float64)
+    inp = mmdit.Inputs(t=np.array([0.5]), x_txt=x[None, :1], x_img=x[None, 1:])
+    (ot, oi), _ = mmdit.forward(cfg, P, inp)
+    got = np.concatenate([ot[0], oi[0]], axis=0) - x
+    r = math.sqrt(1.0 + 1e-6)
+
+    def dot_rot(xv, a, yv, b):
+        return (xv[0] * yv[0] + xv[1] * yv[1]) * math.cos(b - a) + (xv[1] * yv[0] - xv[0] * yv[1]) * math.sin(b - a)
+
+    for i in range(5):
+        q = [g / r for g in gains[stream[i]][0]]
+        logits = []
+        for j in range(5):
+            k = [g / r for g in gains[stream[j]][1]]
+            l0 = dot_rot(q[0:2], pos[i][0], k[0:2], pos[j][0])
+            l1 = dot_rot(q[2:4], pos[i][1], k[2:4], pos[j][1])
+            logits.append(0.5 * (l0 + l1))
+        e = [math.exp(v) for v in logits]
+        p = [v / sum(e) for v in e]
+        want = [sum(p[j] * rows[j][d] / r for j in range(5)) for d in range(4)]
+        np.testing.assert_allclose(got[i], want, rtol=1e-12, atol=1e-13)
