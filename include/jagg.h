@@ -149,6 +149,20 @@ jagg_status jagg_aggregate(jagg_ctx* ctx, const void* const* s, const float* t, 
  * small, on a null pointer, n = 0 or an unknown dtype. */
 jagg_status jagg_group_scores(jagg_ctx* ctx, const void* const* h, size_t n, int W, int dtype, double* score_out);
 
+/* Allocation-free jagg_group_scores, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the same kernels and the same score, with their
+ * partial sums in a static device array of the library (147,456 bytes per
+ * device, held until the process ends) instead of the bound workspace, which
+ * this call does not need.  score_dev: device, one double (8-byte aligned),
+ * written on the context's stream; the call does not synchronise.  Calls
+ * no allocator.  EINVAL on a null pointer, n = 0, an unknown dtype or W
+ * outside 2..8 (W = 8 is the largest the static array holds).  Every call on
+ * one device shares that array: calls that overlap on one device (on two
+ * streams or threads) race and must be serialised by the caller. */
+jagg_status jagg_group_scores_noalloc(jagg_ctx* ctx, const void* const* h, size_t n, int W, int dtype,
+                                      double* score_dev);
+
 /* Routing (high-noise vs low-noise scheduling; gradient-quality appendix).
  * Groups are ordered from high to low noise.  frac >= 0: the first
  * floor(frac * n_groups + 1e-6) groups use JAGG (static jagg_frac).  frac < 0:

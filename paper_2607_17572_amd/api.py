@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
             "jagg_alpha": [ctypes.POINTER(f), i, ctypes.POINTER(f)],
             "jagg_aggregate": [vp, ctypes.POINTER(vp), ctypes.POINTER(f), i, sz, i, vp, vp],
             "jagg_group_scores": [vp, ctypes.POINTER(vp), sz, i, i, ctypes.POINTER(d)],
+            "jagg_group_scores_noalloc": [vp, ctypes.POINTER(vp), sz, i, i, vp],
             "jagg_route": [ctypes.POINTER(d), i, d, d, ctypes.POINTER(ctypes.c_ubyte), ctypes.POINTER(d)],
             "jagg_group_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, vp, f],
             "perstep_group_backward": [vp, vp, ctypes.POINTER(vp), i, ctypes.POINTER(vp), i, vp, f],
@@ -276,6 +277,14 @@ class Context:
         dt = BF16 if h_list[0].dtype == _torch().bfloat16 else F32
         _check(lib().jagg_group_scores(self._h, _ptrs(h_list), h_list[0].numel(), len(h_list), dt, ctypes.byref(out)))
         return out.value
+
+    def group_score_noalloc(self, h_list, score_dev):
+        """Allocation-free group score: written into score_dev (a device fp64
+        tensor of one element) on the stream; needs no workspace."""
+        dt = BF16 if h_list[0].dtype == _torch().bfloat16 else F32
+        _check(lib().jagg_group_scores_noalloc(self._h, _ptrs(h_list), h_list[0].numel(), len(h_list), dt,
+                                               score_dev.data_ptr()))
+        return score_dev
 
     def group_backward(self, theta, saved_pair, batch: int, s_list, t, dtheta, beta: float = 0.0):
         """JAGG: composites + one VJP over the batch-2B endpoint pair."""

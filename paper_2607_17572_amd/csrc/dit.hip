@@ -6,6 +6,7 @@
 #include <array>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -987,6 +988,70 @@ jagg_status jagg_group_scores(jagg_ctx* ctx, const void* const* h, size_t n, int
       hipStreamSynchronize(ctx->stream) != hipSuccess)
     return fail(JAGG_EDEVICE, "jagg_group_scores: copy of the score failed");
   return JAGG_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------ allocation-free scoring
+// Device scratch of jagg_group_scores_noalloc: the score pass's per-block fp64
+// partial sums (SC_BLOCKS blocks x W(W+1)/2 pair products; 147,456 bytes at
+// the largest W, 8).  Each device holds its own copy until the process ends.
+// In host code `scratch` names a host-side stand-in, never the device memory:
+// kernels get the address hipGetSymbolAddress returns for the current device.
+static constexpr size_t NOALLOC_SCRATCH_BYTES = 147456;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_dev[64] = {};
+
+// The current device's copy of `scratch`, looked up on the first call made on
+// that device and kept for the later ones.
+jagg_status scratch_ptr(void** out, const char* who) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+    return fail(JAGG_EDEVICE, std::string(who) + ": no current device");
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(JAGG_EDEVICE, std::string(who) + ": address of the static scratch: " + hipGetErrorString(e));
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return JAGG_OK;
+}
+}  // namespace
+
+extern "C" {
+
+jagg_status jagg_group_scores_noalloc(jagg_ctx* ctx, const void* const* h, size_t n, int W, int dtype,
+                                      double* score_dev) {
+  const char* f = "jagg_group_scores_noalloc";
+  if (!ctx || !h || !score_dev) return fail(JAGG_EINVAL, std::string(f) + ": null argument");
+  if (W < 2 || W > 8) return fail(JAGG_EINVAL, std::string(f) + ": W must be 2..8");
+  if (n == 0) return fail(JAGG_EINVAL, std::string(f) + ": empty vectors");
+  if (dtype != JAGG_F32 && dtype != JAGG_BF16) return fail(JAGG_EINVAL, std::string(f) + ": unknown dtype");
+  if ((uintptr_t)score_dev % 8) return fail(JAGG_EINVAL, std::string(f) + ": score_dev must be 8-byte aligned");
+  const size_t need = jg::score_part_doubles(W) * sizeof(double);
+  if (need > NOALLOC_SCRATCH_BYTES)
+    return fail(JAGG_EINVAL, std::string(f) + ": W = " + std::to_string(W) + " needs " + std::to_string(need) +
+                                 " bytes of scratch, more than the static " + std::to_string(NOALLOC_SCRATCH_BYTES));
+  jg::ScoreArgs a;
+  std::memset(&a, 0, sizeof(a));
+  for (int j = 0; j < W; ++j) {
+    if (!h[j]) return fail(JAGG_EINVAL, std::string(f) + ": null h_j");
+    a.h[j] = h[j];
+  }
+  a.W = W;
+  a.n = n;
+  a.dt = dtype;
+  void* part = nullptr;
+  jagg_status st = scratch_ptr(&part, f);
+  if (st) return st;
+  // pass 1 writes every partial it reads back, so nothing needs clearing
+  return to_status(jg::group_scores(a, (double*)part, score_dev, ctx->stream));
 }
 
 jagg_status jagg_route(const double* scores, int n_groups, double tau, double frac, unsigned char* use_jagg_out,
