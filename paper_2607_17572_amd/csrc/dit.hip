@@ -245,10 +245,9 @@ struct Ws {
   float* delta = nullptr;
   void* dS = nullptr;  // dS^T of the attention backward (bf16 MFMA path)
   float *p1 = nullptr, *p2 = nullptr;
-  float *p1b = nullptr, *p2b = nullptr;  // the text stream's partials while it runs on the side stream
   float* dmod[2] = {nullptr, nullptr};
-  float *dmvec = nullptr, *dvec = nullptr, *dsh1 = nullptr, *tmp = nullptr, *tmp2 = nullptr;
-  float *slpart = nullptr, *slpart2 = nullptr;  // second copies: the text stream on the side stream
+  float *dmvec = nullptr, *dvec = nullptr, *dsh1 = nullptr, *tmp = nullptr;
+  float* slpart = nullptr;
   void* gact = nullptr;
   void* fout = nullptr;
   float* dfa = nullptr;
@@ -292,22 +291,18 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   W.p1 = a.f32((size_t)nch * W.maxcols);
   W.p2 = a.f32((size_t)nch * W.maxcols);
-  W.p1b = a.f32((size_t)nch * W.maxcols);
-  W.p2b = a.f32((size_t)nch * W.maxcols);
   W.dmod[0] = a.f32((size_t)B * 6 * m.D);
   W.dmod[1] = a.f32((size_t)B * 6 * m.D);
   W.dmvec = a.f32((size_t)B * m.D);
   W.dvec = a.f32((size_t)B * m.D);
   W.dsh1 = a.f32((size_t)B * m.D);
   W.tmp = a.f32((size_t)B * m.D);
-  W.tmp2 = a.f32((size_t)B * m.D);
   // partials of every small-linear backward with an input gradient: the
   // modulations (D -> 6D or 3D or 2D) and the second time-MLP layer (D -> D)
   const size_t slp = std::max({small_linear_bwd_part_floats(B, m.D, 6 * m.D), small_linear_bwd_part_floats(B, m.D, 3 * m.D),
                                small_linear_bwd_part_floats(B, m.D, 2 * m.D), small_linear_bwd_part_floats(B, m.D, m.D),
                                small_linear_bwd_part_floats(B, m.tf, m.D)});
   W.slpart = a.f32(slp);
-  W.slpart2 = a.f32(slp);
   W.gact = a.take(rows * m.D * es);
   if (!m.c.block_only) {
     W.fout = a.take((size_t)B * m.ni * m.pd * es);
@@ -326,17 +321,6 @@ struct jagg_ctx {
   hipStream_t stream = nullptr;
   void* ws = nullptr;
   size_t ws_bytes = 0;
-  // side stream for the text-stream half of a double block's backward, with
-  // the fork / join events; created on the first backward (a context can be
-  // made without a device), released with the context
-  hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  bool side_tried = false;
-  ~jagg_ctx() {
-    if (ev_fork) (void)hipEventDestroy(ev_fork);
-    if (ev_join) (void)hipEventDestroy(ev_join);
-    if (side) (void)hipStreamDestroy(side);
-  }
 };
 
 namespace jg {
@@ -348,34 +332,7 @@ struct Ctx {
   const char* th;  // theta base
   size_t es;       // theta element size
   const void* P(size_t off) const { return th + off * es; }
-  // text-stream work of a double block may run on `side` (nullptr: on s)
-  hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  Ctx on(hipStream_t st) const {
-    Ctx c = *this;
-    c.s = st;
-    return c;
-  }
 };
-
-// Fork: work later issued on cx.side waits for everything issued on cx.s so
-// far.  Join: work later issued on cx.s waits for everything issued on side.
-static int fork_side(const Ctx& cx) {
-  if (!cx.side) return 0;
-  if (hipEventRecord(cx.ev_fork, cx.s) != hipSuccess || hipStreamWaitEvent(cx.side, cx.ev_fork, 0) != hipSuccess) {
-    set_error("backward: fork of the side stream failed");
-    return 3;
-  }
-  return 0;
-}
-static int join_side(const Ctx& cx) {
-  if (!cx.side) return 0;
-  if (hipEventRecord(cx.ev_join, cx.side) != hipSuccess || hipStreamWaitEvent(cx.s, cx.ev_join, 0) != hipSuccess) {
-    set_error("backward: join of the side stream failed");
-    return 3;
-  }
-  return 0;
-}
 
 // Y[M][:] = X[M][K] W[rows w_row0..][K]^T + b  (one linear layer or a row slice of it)
 static int lin_fwd(const Ctx& cx, const void* X, int ldx, int M, const Lin& L, int w_row0, int nout, void* Y,
@@ -550,6 +507,33 @@ static int forward(jagg_ctx* ctx, const void* theta, const void* z, const float*
 }
 
 // ------------------------------------------------------------------ VJP
+// The text- and image-stream products of one layer of a double block (separate
+// weights, disjoint row ranges) as one grouped GEMM launch.
+static GemmArgs wgrad_args(const Ctx& cx, const void* dY, int ld_dy, int dy_dt, const void* X, int ldx, int rows,
+                           int Nout, int Kin, void* dW, float beta) {
+  GemmArgs g;
+  g.A = dY; g.lda = ld_dy; g.ta = 1; g.a_dt = dy_dt;
+  g.B = X; g.ldb = ldx; g.tb = 1; g.b_dt = cx.m.act;
+  g.M = Nout; g.N = Kin; g.K = rows;
+  g.epi.C = dW; g.epi.ldc = Kin; g.epi.c_dt = cx.m.grad; g.epi.beta = beta;
+  return g;
+}
+static GemmArgs dgrad_args(const Ctx& cx, const void* dY, int ld_dy, int rows, const void* W, int ldw, int Nout,
+                           int Kin, void* out, int ldo, int odt, int mode = EPI_STORE, void* aux = nullptr,
+                           int ldaux = 0) {
+  GemmArgs g;
+  g.A = dY; g.lda = ld_dy; g.ta = 0; g.a_dt = cx.m.act;
+  g.B = W; g.ldb = ldw; g.tb = 1; g.b_dt = cx.m.act;
+  g.M = rows; g.N = Kin; g.K = Nout;
+  g.epi.C = out; g.epi.ldc = ldo; g.epi.c_dt = odt;
+  g.epi.mode = mode; g.epi.aux = aux; g.epi.ldaux = ldaux; g.epi.aux_dt = cx.m.act;
+  return g;
+}
+
+// Double-block backward.  Both streams' rows go through every memory-bound
+// kernel in one launch (the modulation vectors are picked per row), and the
+// two streams' products of each layer run as one grouped GEMM; only the
+// per-stream reductions of the column partials are separate launches.
 static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int B, Ws& W, void* dth, float beta) {
   const Model& m = cx.m;
   const int D = m.D, F = m.F, act = m.act;
@@ -561,81 +545,80 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   auto rowf = [&](float* p, int r, int ld) { return p + (size_t)r * ld; };
   const auto& st = m.dbl[i];
   const int nchunk = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
-  // The two streams' chains are independent between the joint steps
-  // (attention, q/k norm): the text stream's work goes to the side stream
-  // and overlaps the image stream's on the main one.  They touch disjoint
-  // rows and parameter gradients and each has its own partial-sum buffers
-  // (the chunk partials of different kernels use different row strides, so
-  // one buffer cannot be split by chunk between two running kernels); the
-  // one shared sum (d SiLU(vec)) is formed after the join in the fixed order
-  // text, image.
-  const Ctx cs[2] = {cx.side ? cx.on(cx.side) : cx, cx};
-  float* const tmp[2] = {W.tmp2, W.tmp};
-  float* const slp[2] = {W.slpart2, W.slpart};
-  float* const P1[2] = {W.p1b, W.p1};
-  float* const P2[2] = {W.p2b, W.p2};
-  TRY(fork_side(cx));
+  int c0[2], nc[2];
+  for (int s = 0; s < 2; ++s) TRY(chunk_range(rm, r0[s], nr[s], &c0[s], &nc[s]));
+  const hipStream_t S = cx.s;
+  auto wg2 = [&](void* dY, int ld_dy, void* X, int ldx, int Nout, int Kin, size_t w0, size_t w1) {
+    const GemmArgs a = wgrad_args(cx, row(dY, r0[0], ld_dy), ld_dy, act, row(X, r0[0], ldx), ldx, nr[0], Nout, Kin,
+                                  G(dth, m, w0), beta);
+    const GemmArgs b = wgrad_args(cx, row(dY, r0[1], ld_dy), ld_dy, act, row(X, r0[1], ldx), ldx, nr[1], Nout, Kin,
+                                  G(dth, m, w1), beta);
+    return gemm2(a, b, S);
+  };
+  auto dg2 = [&](void* dY, int ld_dy, size_t w0, size_t w1, int ldw, int Nout, int Kin, void* out, int ldo, int odt,
+                 int mode = EPI_STORE, void* aux = nullptr, int ldaux = 0) {
+    const size_t oes = dsize(odt);
+    auto orow = [&](void* p, int r) { return (void*)((char*)p + (size_t)r * ldo * oes); };
+    const GemmArgs a = dgrad_args(cx, row(dY, r0[0], ld_dy), ld_dy, nr[0], cx.P(w0), ldw, Nout, Kin, orow(out, r0[0]),
+                                  ldo, odt, mode, aux ? row(aux, r0[0], ldaux) : nullptr, ldaux);
+    const GemmArgs b = dgrad_args(cx, row(dY, r0[1], ld_dy), ld_dy, nr[1], cx.P(w1), ldw, Nout, Kin, orow(out, r0[1]),
+                                  ldo, odt, mode, aux ? row(aux, r0[1], ldaux) : nullptr, ldaux);
+    return gemm2(a, b, S);
+  };
+  // MLP branch: x_out = xm + gate2 * y2
+  TRY(gate_bwd(W.g, A.y2, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, W.p1, W.p2, S));
   for (int s = 0; s < 2; ++s) {
-    const DStream& L = st[s];
-    const Ctx& c = cs[s];
-    int c0, nc;
-    TRY(chunk_range(rm, r0[s], nr[s], &c0, &nc));
-    // MLP branch: x_out = xm + gate2 * y2
-    TRY(gate_bwd(W.g, A.y2, act, D, rm, r0[s], nr[s], A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, P1[s], P2[s], c.s));
-    TRY(reduce_per_sample(P1[s], D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 5 * D, c.s));
-    TRY(reduce_to_grad(P2[s], D, c0, nc, D, G(dth, m, L.fc2.b), m.grad, beta, c.s));
-    void* dY = row(W.dY, r0[s], D);
-    TRY(wgrad(c, dY, D, act, row(A.h, r0[s], F), F, nr[s], D, F, G(dth, m, L.fc2.w), beta));
-    void* dpre = row(W.dbig, r0[s], F);
-    TRY(dgrad(c, dY, D, nr[s], cx.P(L.fc2.w), F, D, F, dpre, F, act, EPI_GELU_BWD, row(A.pre, r0[s], F), F));
-    TRY(colsum_partials(W.dbig, act, F, F, rm, r0[s], nr[s], P1[s], c.s));
-    TRY(reduce_to_grad(P1[s], F, c0, nc, F, G(dth, m, L.fc1.b), m.grad, beta, c.s));
-    TRY(wgrad(c, dpre, F, act, row(A.a2, r0[s], D), D, nr[s], F, D, G(dth, m, L.fc1.w), beta));
-    TRY(dgrad(c, dpre, F, nr[s], cx.P(L.fc1.w), D, F, D, rowf(W.dA, r0[s], D), D, F32));
-    TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, r0[s], nr[s], A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, W.g, P1[s],
-                   P2[s], c.s));
-    TRY(reduce_per_sample(P1[s], D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D, c.s));
-    TRY(reduce_per_sample(P2[s], D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D, c.s));
-    // attention branch: xm = x + gate1 * y1
-    TRY(gate_bwd(W.g, A.y1, act, D, rm, r0[s], nr[s], A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, P1[s], P2[s], c.s));
-    TRY(reduce_per_sample(P1[s], D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 2 * D, c.s));
-    TRY(reduce_to_grad(P2[s], D, c0, nc, D, G(dth, m, L.o.b), m.grad, beta, c.s));
-    TRY(wgrad(c, dY, D, act, row(A.O, r0[s], D), D, nr[s], D, D, G(dth, m, L.o.w), beta));
-    TRY(dgrad(c, dY, D, nr[s], cx.P(L.o.w), D, D, D, row(W.dO, r0[s], D), D, act));
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 5 * D, S));
+    TRY(reduce_to_grad(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].fc2.b), m.grad, beta, S));
   }
-  TRY(join_side(cx));
+  TRY(wg2(W.dY, D, A.h, F, D, F, st[0].fc2.w, st[1].fc2.w));
+  TRY(dg2(W.dY, D, st[0].fc2.w, st[1].fc2.w, F, D, F, W.dbig, F, act, EPI_GELU_BWD, A.pre, F));
+  TRY(colsum_partials(W.dbig, act, F, F, rm, 0, R, W.p1, S));
+  for (int s = 0; s < 2; ++s) TRY(reduce_to_grad(W.p1, F, c0[s], nc[s], F, G(dth, m, st[s].fc1.b), m.grad, beta, S));
+  TRY(wg2(W.dbig, F, A.a2, D, F, D, st[0].fc1.w, st[1].fc1.w));
+  TRY(dg2(W.dbig, F, st[0].fc1.w, st[1].fc1.w, D, F, D, W.dA, D, F32));
+  TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, 0, R, A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, W.g, W.p1, W.p2, S));
+  for (int s = 0; s < 2; ++s) {
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D, S));
+    TRY(reduce_per_sample(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D, S));
+  }
+  // attention branch: xm = x + gate1 * y1
+  TRY(gate_bwd(W.g, A.y1, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, W.p1, W.p2, S));
+  for (int s = 0; s < 2; ++s) {
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 2 * D, S));
+    TRY(reduce_to_grad(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].o.b), m.grad, beta, S));
+  }
+  TRY(wg2(W.dY, D, A.O, D, D, D, st[0].o.w, st[1].o.w));
+  TRY(dg2(W.dY, D, st[0].o.w, st[1].o.w, D, D, D, W.dO, D, act));
   AttnBwd ab{A.Qh, A.Kh, A.Vh, A.O, D, W.dO, D, A.lse, W.delta, W.dQh, W.dKh, W.dVh, act, B, m.H, m.N, m.Dh, act, rm,
              W.dS, attn_ds_ld(m.N), attn_ds_rows(m.N)};
-  TRY(attention_bwd(ab, cx.s));
+  TRY(attention_bwd(ab, S));
   Gains gn{{cx.P(st[0].qg), cx.P(st[1].qg)}, {cx.P(st[0].kg), cx.P(st[1].kg)}};
   TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.qkv, 3 * D, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
-                       A.rk, W.dbig, 3 * D, W.p2, cx.s));
-  TRY(fork_side(cx));
+                       A.rk, W.dbig, 3 * D, W.p2, S));
   for (int s = 0; s < 2; ++s) {
-    const DStream& L = st[s];
-    const Ctx& c = cs[s];
-    int c0, nc;
-    TRY(chunk_range(rm, r0[s], nr[s], &c0, &nc));
-    TRY(reduce_to_grad(W.p2, 2 * m.Dh, c0 * QK_PARTS, nc * QK_PARTS, m.Dh, G(dth, m, L.qg), m.grad, beta, c.s));
-    TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, c0 * QK_PARTS, nc * QK_PARTS, m.Dh, G(dth, m, L.kg), m.grad, beta,
-                       c.s));
-    TRY(colsum_partials(W.dbig, act, 3 * D, 3 * D, rm, r0[s], nr[s], P1[s], c.s));
-    TRY(reduce_to_grad(P1[s], 3 * D, c0, nc, 3 * D, G(dth, m, L.qkv.b), m.grad, beta, c.s));
-    void* dq = row(W.dbig, r0[s], 3 * D);
-    TRY(wgrad(c, dq, 3 * D, act, row(A.a1, r0[s], D), D, nr[s], 3 * D, D, G(dth, m, L.qkv.w), beta));
-    TRY(dgrad(c, dq, 3 * D, nr[s], cx.P(L.qkv.w), D, 3 * D, D, rowf(W.dA, r0[s], D), D, F32));
-    TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, r0[s], nr[s], A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, P1[s],
-                   P2[s] + (size_t)nchunk * QK_PARTS * 2 * m.Dh, c.s));
-    TRY(reduce_per_sample(P1[s], D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D, c.s));
-    TRY(reduce_per_sample(P2[s] + (size_t)nchunk * QK_PARTS * 2 * m.Dh, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0,
-                          c.s));
-    // adaLN modulation: mod = SiLU(vec) W_mod^T + b
-    TRY(small_linear_bwd(W.dmod[s], mvec, 0, B, D, cx.P(L.mod.w), m.act, 6 * D, G(dth, m, L.mod.w),
-                         G(dth, m, L.mod.b), m.grad, beta, tmp[s], slp[s], c.s));
+    TRY(reduce_to_grad(W.p2, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh, G(dth, m, st[s].qg), m.grad, beta, S));
+    TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh, G(dth, m, st[s].kg), m.grad,
+                       beta, S));
   }
-  TRY(join_side(cx));
-  TRY(add_into(W.dmvec, tmp[0], (size_t)B * D, cx.s));
-  TRY(add_into(W.dmvec, tmp[1], (size_t)B * D, cx.s));
+  TRY(colsum_partials(W.dbig, act, 3 * D, 3 * D, rm, 0, R, W.p1, S));
+  for (int s = 0; s < 2; ++s)
+    TRY(reduce_to_grad(W.p1, 3 * D, c0[s], nc[s], 3 * D, G(dth, m, st[s].qkv.b), m.grad, beta, S));
+  TRY(wg2(W.dbig, 3 * D, A.a1, D, 3 * D, D, st[0].qkv.w, st[1].qkv.w));
+  TRY(dg2(W.dbig, 3 * D, st[0].qkv.w, st[1].qkv.w, D, 3 * D, D, W.dA, D, F32));
+  float* const p2s = W.p2 + (size_t)nchunk * QK_PARTS * 2 * m.Dh;
+  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, W.p1, p2s, S));
+  for (int s = 0; s < 2; ++s) {
+    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D, S));
+    TRY(reduce_per_sample(p2s, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0, S));
+  }
+  // adaLN modulation: mod = SiLU(vec) W_mod^T + b, per stream; d SiLU(vec) in the order text, image
+  for (int s = 0; s < 2; ++s) {
+    TRY(small_linear_bwd(W.dmod[s], mvec, 0, B, D, cx.P(st[s].mod.w), m.act, 6 * D, G(dth, m, st[s].mod.w),
+                         G(dth, m, st[s].mod.b), m.grad, beta, W.tmp, W.slpart, S));
+    TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, S));
+  }
+  (void)rowf;
   return 0;
 }
 
@@ -676,32 +659,9 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   return 0;
 }
 
-// The side stream of a context: created on first use; if that fails the
-// backward runs on the context's stream alone.
-static void ensure_side(jagg_ctx* ctx) {
-  if (ctx->side_tried) return;
-  ctx->side_tried = true;
-  if (hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking) != hipSuccess) { ctx->side = nullptr; return; }
-  if (hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming) != hipSuccess) {
-    if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
-    (void)hipStreamDestroy(ctx->side);
-    ctx->side = nullptr;
-    ctx->ev_fork = ctx->ev_join = nullptr;
-  }
-  (void)hipGetLastError();
-}
-
 static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const void* cot, void* dth, float beta) {
   const Model& m = ctx->m;
   Ctx cx{m, ctx->stream, (const char*)theta, dsize(m.act)};
-  ensure_side(ctx);
-  // while a kernel class is being timed every kernel runs alone on one stream
-  if (ctx->side && !prof_armed()) {
-    cx.side = ctx->side;
-    cx.ev_fork = ctx->ev_fork;
-    cx.ev_join = ctx->ev_join;
-  }
   const int act = m.act, D = m.D;
   const size_t es = dsize(act);
   const RowMap rm{B, m.nt, m.ni};

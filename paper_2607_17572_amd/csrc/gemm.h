@@ -40,7 +40,17 @@ struct GemmArgs {
 
 // Returns 0 on success, 1 on invalid arguments, 3 on a launch error.
 int gemm(const GemmArgs& g, hipStream_t s);
-// Tile configuration used by the MFMA kernel (tuning hook; 0 = default).
-void gemm_set_tile_cfg(int c);
+
+// Up to two independent products in one launch (for example the text- and
+// image-stream products of one layer of a double-stream block): the problems
+// keep their own operands, sizes and outputs; the tiles of the longer
+// contraction come first.  Products the grouped kernel does not cover run as
+// two gemm() calls.
+struct GemmGroup {
+  GemmArgs p[2];
+  int np = 1;      // problems in the group
+  int tiles0 = 0;  // workgroups of p[0] (set by the launcher)
+};
+int gemm2(const GemmArgs& a, const GemmArgs& b, hipStream_t s);
 
 }  // namespace jg

@@ -875,7 +875,7 @@ __device__ __forceinline__ void dtl_epilogue(const GemmArgs& g, f32x16 (&acc)[BM
 }
 
 template <bool TA, bool TB, int EK, int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_dtl_kernel(GemmArgs g) {
+__global__ __launch_bounds__(64 * WM * WN) void gemm_dtl_kernel(GemmGroup gg) {
   constexpr int BK = 32, NW = WM * WN, FM = BM / (32 * WM), FN = BN / (32 * WN);
   constexpr int SB = BM * 64;  // byte offset of the B tile in a stage
   constexpr int STG = 32768;   // bytes per stage (room for 256 + 256 rows)
@@ -887,9 +887,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dtl_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) char st2[STG];
   __shared__ __attribute__((aligned(1024))) char st3[STG];
 
+  // the first tiles0 workgroups compute problem 0, the rest problem 1
+  const int sel = (int)blockIdx.x >= gg.tiles0 ? 1 : 0;
+  const GemmArgs& g = gg.p[sel];
+  const int local = (int)blockIdx.x - sel * gg.tiles0;
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
   int tm, tn;
-  tile_coords(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
+  tile_coords(xcd_remap(local, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -1095,25 +1099,45 @@ static int launch_mfma(const GemmArgs& g, hipStream_t s) {
 }
 
 template <bool TA, bool TB, int EK, int BM, int BN, int WM = 2, int WN = 2>
-static int launch_dtl(const GemmArgs& g, hipStream_t s) {
-  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+static int launch_dtl(const GemmGroup& gr, hipStream_t s) {
+  GemmGroup g = gr;
+  int tiles = 0;
+  for (int p = 0; p < g.np; ++p) {
+    const int t = ((g.p[p].M + BM - 1) / BM) * ((g.p[p].N + BN - 1) / BN);
+    if (p == 0) g.tiles0 = t;
+    tiles += t;
+  }
+  if (g.np == 1) g.tiles0 = tiles;
   launch(gemm_dtl_kernel<TA, TB, EK, BM, BN, WM, WN>, dim3(tiles), dim3(64 * WM * WN), 0u, s, g);
   JG_CHECK_LAUNCH("gemm_dtl");
   return 0;
 }
 
 // Tile shape of the direct-to-LDS kernel: the one with the least estimated
-// time = whole rounds of 256 workgroups x tile area / relative tile efficiency
+// time = rounds of 256 workgroups x tile area / relative tile efficiency
 // (smaller tiles re-read more operand bytes per MFMA).  0: 256x256 (8 waves),
-// 1: 256x192, 2: 192x256, 3: 192x192.
-static int dtl_shape(int M, int N) {
+// 1: 256x192, 2: 192x256, 3: 192x192.  Rounds count whole rounds of problem
+// 0's tiles; the tiles of a second problem with a shorter contraction are
+// shorter and fill in behind them (the dispatcher hands a freed CU the next
+// workgroup), so they add their share of a round; equal contractions share
+// whole rounds.
+static int dtl_shape(const GemmGroup& g) {
   static const int bm[4] = {256, 256, 192, 192}, bn[4] = {256, 192, 256, 192};
   static const double eff[4] = {1.0, 0.95, 0.95, 0.9};
   int best = 0;
   double bt = 1e300;
   for (int i = 0; i < 4; ++i) {
-    const long tiles = (long)((M + bm[i] - 1) / bm[i]) * ((N + bn[i] - 1) / bn[i]);
-    const double t = (double)((tiles + 255) / 256) * bm[i] * bn[i] / eff[i];
+    long tl[2] = {0, 0};
+    for (int p = 0; p < g.np; ++p)
+      tl[p] = (long)((g.p[p].M + bm[i] - 1) / bm[i]) * ((g.p[p].N + bn[i] - 1) / bn[i]);
+    double rounds;
+    if (g.np == 1 || g.p[1].K == g.p[0].K) {
+      rounds = (double)((tl[0] + tl[1] + 255) / 256);
+    } else {
+      const double work = tl[0] + (double)tl[1] * g.p[1].K / g.p[0].K;
+      rounds = std::max((double)((tl[0] + 255) / 256), work / 256.0);
+    }
+    const double t = rounds * bm[i] * bn[i] / eff[i];
     if (t < bt * 0.999) { bt = t; best = i; }
   }
   return best;
@@ -1123,7 +1147,7 @@ static int dtl_shape(int M, int N) {
 // (input and weight gradients); -1 for the others.
 template <bool TA, bool TB, int EK>
 struct DtlLaunch {
-  static int run(const GemmArgs& g, hipStream_t s, int shape) {
+  static int run(const GemmGroup& g, hipStream_t s, int shape) {
     switch (shape) {
       case 1: return launch_dtl<TA, TB, EK, 256, 192>(g, s);
       case 2: return launch_dtl<TA, TB, EK, 192, 256>(g, s);
@@ -1134,8 +1158,15 @@ struct DtlLaunch {
 };
 template <bool TA, int EK>
 struct DtlLaunch<TA, false, EK> {
-  static int run(const GemmArgs&, hipStream_t, int) { return -1; }
+  static int run(const GemmGroup&, hipStream_t, int) { return -1; }
 };
+
+static GemmGroup single(const GemmArgs& g) {
+  GemmGroup r;
+  r.p[0] = g;
+  r.np = 1;
+  return r;
+}
 
 // The direct-to-LDS kernel computes 32-bit byte offsets up to three k tiles
 // past K; they must stay below 2^31.
@@ -1149,7 +1180,8 @@ static bool dtl_fits(const GemmArgs& g) {
 template <bool TA, bool TB, int EK>
 static int launch_cfg(const GemmArgs& g, hipStream_t s, int cfg) {
   if (TB && cfg >= 8 && cfg <= 12 && dtl_fits(g)) {
-    const int rc = DtlLaunch<TA, TB, EK>::run(g, s, cfg == 8 ? dtl_shape(g.M, g.N) : cfg - 9);
+    const GemmGroup one = single(g);
+    const int rc = DtlLaunch<TA, TB, EK>::run(one, s, cfg == 8 ? dtl_shape(one) : cfg - 9);
     if (rc >= 0) return rc;
   }
   // K not a multiple of the 64-deep k tile: the edge-checked kernel
@@ -1209,23 +1241,30 @@ int gemm(const GemmArgs& g, hipStream_t s) {
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// The epilogue kind of g if the MFMA kernels can compute it (bf16 operands,
+// 16-byte aligned rows, 32-bit operand extents), else -1.
+static int mfma_kind(const GemmArgs& g) {
+  bool mfma = g.a_dt == BF16 && g.b_dt == BF16 && g.K > 0 && aligned16(g.A) && aligned16(g.B) &&
+              g.lda % 8 == 0 && g.ldb % 8 == 0;
+  if (mfma) mfma = (g.ta ? g.M % 8 == 0 : g.K % 8 == 0) && (g.tb ? g.N % 8 == 0 : g.K % 8 == 0);
+  const int ek = mfma ? epi_kind(g.epi) : -1;
+  if (ek >= 0 && (g.epi.ldc % 8 != 0 || !aligned16(g.epi.C) || (g.epi.aux && (g.epi.ldaux % 8 || !aligned16(g.epi.aux)))))
+    return -1;
+  // operand extents must fit a 32-bit buffer offset
+  const double ea = 2.0 * (g.ta ? (double)g.K * g.lda : (double)g.M * g.lda);
+  const double eb = 2.0 * (g.tb ? (double)g.K * g.ldb : (double)g.N * g.ldb);
+  if (ea >= 2147483000.0 || eb >= 2147483000.0) return -1;
+  return ek;
+}
+
 static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   if (g.M < 0 || g.N < 0 || g.K < 0 || !g.A || !g.B || !g.epi.C) {
     set_error("gemm: invalid arguments");
     return 1;
   }
   if (g.M == 0 || g.N == 0) return 0;
-  bool mfma = g.a_dt == BF16 && g.b_dt == BF16 && g.K > 0 && aligned16(g.A) && aligned16(g.B) &&
-              g.lda % 8 == 0 && g.ldb % 8 == 0;
-  if (mfma) mfma = (g.ta ? g.M % 8 == 0 : g.K % 8 == 0) && (g.tb ? g.N % 8 == 0 : g.K % 8 == 0);
-  const int ek = mfma ? epi_kind(g.epi) : -1;
-  if (ek >= 0 && (g.epi.ldc % 8 != 0 || !aligned16(g.epi.C) || (g.epi.aux && (g.epi.ldaux % 8 || !aligned16(g.epi.aux)))))
-    mfma = false;
-  // operand extents must fit a 32-bit buffer offset
-  const double ea = 2.0 * (g.ta ? (double)g.K * g.lda : (double)g.M * g.lda);
-  const double eb = 2.0 * (g.tb ? (double)g.K * g.ldb : (double)g.N * g.ldb);
-  if (ea >= 2147483000.0 || eb >= 2147483000.0) mfma = false;
-  if (mfma && ek >= 0) {
+  const int ek = mfma_kind(g);
+  if (ek >= 0) {
     // default: products with a k-strided B operand (weight and input
     // gradients) take the direct-to-LDS kernel with the tile shape that best
     // fills whole rounds of 256 CUs; the forward product takes the 8-wave
@@ -1250,14 +1289,46 @@ static int gemm_launch(const GemmArgs& g, hipStream_t s) {
   return 0;
 }
 
+template <bool TA, int EK>
+static int launch_group(const GemmGroup& g, hipStream_t s) {
+  return DtlLaunch<TA, true, EK>::run(g, s, dtl_shape(g));
+}
+
+int gemm2(const GemmArgs& a, const GemmArgs& b, hipStream_t s) {
+  // one grouped launch when both products take the same direct-to-LDS kernel
+  const int ek = (a.M > 0 && a.N > 0 && b.M > 0 && b.N > 0 && a.A && a.B && a.epi.C && b.A && b.B && b.epi.C)
+                     ? mfma_kind(a) : -1;
+  const bool grouped = ek >= 0 && mfma_kind(b) == ek && a.ta == b.ta && a.tb && b.tb && dtl_fits(a) &&
+                       dtl_fits(b);
+  if (!grouped) {
+    int rc = gemm(a, s);
+    return rc ? rc : gemm(b, s);
+  }
+  // the longer contraction first: its tiles take the whole rounds, the other's fill in
+  GemmGroup g;
+  g.np = 2;
+  g.p[0] = b.K > a.K ? b : a;
+  g.p[1] = b.K > a.K ? a : b;
+  const int pi = prof_begin(prof_class(a));
+  int rc;
+  switch (ek) {
+#define JG_GRP(E) case E: rc = a.ta ? launch_group<true, E>(g, s) : launch_group<false, E>(g, s); break;
+    JG_GRP(EK_F32) JG_GRP(EK_F32_ACC) JG_GRP(EK_BF16) JG_GRP(EK_BF16_ACC) JG_GRP(EK_BIAS) JG_GRP(EK_GELU)
+    default: rc = a.ta ? launch_group<true, EK_DGELU>(g, s) : launch_group<false, EK_DGELU>(g, s); break;
+#undef JG_GRP
+  }
+  prof_end(pi, 2.0 * ((double)a.M * a.N * a.K + (double)b.M * b.N * b.K));
+  return rc;
+}
+
 // Explicit instantiations of the direct-to-LDS kernels the dispatch can reach
 // (the host-side launch stubs of kernel templates reached only through the
 // shape switch are otherwise not always emitted).
 #define JG_DTL_SHAPES(TA, EK)                                            \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 256, 2, 4>(GemmArgs); \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 192, 2, 2>(GemmArgs); \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 256, 2, 2>(GemmArgs); \
-  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 192, 2, 2>(GemmArgs);
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 256, 2, 4>(GemmGroup); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 256, 192, 2, 2>(GemmGroup); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 256, 2, 2>(GemmGroup); \
+  template __global__ void gemm_dtl_kernel<TA, true, EK, 192, 192, 2, 2>(GemmGroup);
 #define JG_DTL_KINDS(TA) \
   JG_DTL_SHAPES(TA, 0) JG_DTL_SHAPES(TA, 1) JG_DTL_SHAPES(TA, 2) JG_DTL_SHAPES(TA, 3) JG_DTL_SHAPES(TA, 4) \
   JG_DTL_SHAPES(TA, 5) JG_DTL_SHAPES(TA, 6)
