@@ -335,8 +335,8 @@ struct Ctx {
 };
 
 // Y[M][:] = X[M][K] W[rows w_row0..][K]^T + b  (one linear layer or a row slice of it)
-static int lin_fwd(const Ctx& cx, const void* X, int ldx, int M, const Lin& L, int w_row0, int nout, void* Y,
-                   int ldy, int mode = EPI_STORE, void* aux = nullptr, int ldaux = 0) {
+static GemmArgs lin_args(const Ctx& cx, const void* X, int ldx, int M, const Lin& L, int w_row0, int nout, void* Y,
+                         int ldy, int mode = EPI_STORE, void* aux = nullptr, int ldaux = 0) {
   GemmArgs g;
   g.A = X; g.lda = ldx; g.ta = 0; g.a_dt = cx.m.act;
   g.B = (const char*)cx.P(L.w) + (size_t)w_row0 * L.in * cx.es; g.ldb = L.in; g.tb = 0; g.b_dt = cx.m.act;
@@ -344,7 +344,11 @@ static int lin_fwd(const Ctx& cx, const void* X, int ldx, int M, const Lin& L, i
   g.epi.C = Y; g.epi.ldc = ldy; g.epi.c_dt = cx.m.act;
   g.epi.bias = (const char*)cx.P(L.b) + (size_t)w_row0 * cx.es; g.epi.bias_dt = cx.m.act;
   g.epi.mode = mode; g.epi.aux = aux; g.epi.ldaux = ldaux; g.epi.aux_dt = cx.m.act;
-  return gemm(g, cx.s);
+  return g;
+}
+static int lin_fwd(const Ctx& cx, const void* X, int ldx, int M, const Lin& L, int w_row0, int nout, void* Y,
+                   int ldy, int mode = EPI_STORE, void* aux = nullptr, int ldaux = 0) {
+  return gemm(lin_args(cx, X, ldx, M, L, w_row0, nout, Y, ldy, mode, aux, ldaux), cx.s);
 }
 
 // dW[Nout][Kin] = beta dW + dY[rows][Nout]^T X[rows][Kin]
@@ -385,22 +389,26 @@ static int dbl_fwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   for (int s = 0; s < 2; ++s)
     TRY(small_linear_fwd(mvec, 0, B, D, cx.P(st[s].mod.w), cx.P(st[s].mod.b), m.act, A.mod[s], 6 * D, cx.s));
   TRY(ln_mod_fwd(A.x_in, m.act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 0, D, A.a1, A.m1, A.r1, cx.s));
-  for (int s = 0; s < 2; ++s)
-    TRY(lin_fwd(cx, row(A.a1, r0[s], D), D, nr[s], st[s].qkv, 0, 3 * D, row(A.qkv, r0[s], 3 * D), 3 * D));
+  // the two streams' products of each layer: one grouped launch
+  auto fwd2 = [&](void* X, int ldx, const Lin& L0, const Lin& L1, int nout, void* Y, int ldy, int mode = EPI_STORE,
+                  void* aux = nullptr, int ldaux = 0) {
+    const GemmArgs a = lin_args(cx, row(X, r0[0], ldx), ldx, nr[0], L0, 0, nout, row(Y, r0[0], ldy), ldy, mode,
+                                aux ? row(aux, r0[0], ldaux) : nullptr, ldaux);
+    const GemmArgs b = lin_args(cx, row(X, r0[1], ldx), ldx, nr[1], L1, 0, nout, row(Y, r0[1], ldy), ldy, mode,
+                                aux ? row(aux, r0[1], ldaux) : nullptr, ldaux);
+    return gemm2(a, b, cx.s);
+  };
+  TRY(fwd2(A.a1, D, st[0].qkv, st[1].qkv, 3 * D, A.qkv, 3 * D));
   Gains gn{{cx.P(st[0].qg), cx.P(st[1].qg)}, {cx.P(st[0].kg), cx.P(st[1].kg)}};
   TRY(qk_norm_rope_fwd(A.qkv, 3 * D, m.act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.Qh, A.Kh, A.Vh, A.rq, A.rk,
                        cx.s));
   AttnFwd af{A.Qh, A.Kh, A.Vh, A.O, D, A.lse, B, m.H, m.N, m.Dh, m.act, rm};
   TRY(attention_fwd(af, cx.s));
-  for (int s = 0; s < 2; ++s)
-    TRY(lin_fwd(cx, row(A.O, r0[s], D), D, nr[s], st[s].o, 0, D, row(A.y1, r0[s], D), D));
+  TRY(fwd2(A.O, D, st[0].o, st[1].o, D, A.y1, D));
   TRY(gated_residual(A.x_in, A.y1, m.act, D, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, A.xm, cx.s));
   TRY(ln_mod_fwd(A.xm, m.act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 3 * D, 4 * D, A.a2, A.m2, A.r2, cx.s));
-  for (int s = 0; s < 2; ++s) {
-    TRY(lin_fwd(cx, row(A.a2, r0[s], D), D, nr[s], st[s].fc1, 0, F, row(A.h, r0[s], F), F, EPI_GELU_FWD,
-                row(A.pre, r0[s], F), F));
-    TRY(lin_fwd(cx, row(A.h, r0[s], F), F, nr[s], st[s].fc2, 0, D, row(A.y2, r0[s], D), D));
-  }
+  TRY(fwd2(A.a2, D, st[0].fc1, st[1].fc1, F, A.h, F, EPI_GELU_FWD, A.pre, F));
+  TRY(fwd2(A.h, F, st[0].fc2, st[1].fc2, D, A.y2, D));
   TRY(gated_residual(A.xm, A.y2, m.act, D, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, A.x_out, cx.s));
   return 0;
 }

@@ -505,7 +505,7 @@ __device__ __forceinline__ void pipe_sched() {
 }
 
 template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
+__global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmGroup gg) {
   static_assert(BK == 64, "the schedule is written for four 16-deep MFMA steps per k tile");
   constexpr int NT = WM * WN * 64;
   constexpr int LDSK = BK + 8;
@@ -514,9 +514,13 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_pipe_kernel(GemmArgs g) {
   constexpr int STAGE = (BM + BN) * LDSK;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
 
+  // the first tiles0 workgroups compute problem 0, the rest problem 1
+  const int sel = (int)blockIdx.x >= gg.tiles0 ? 1 : 0;
+  const GemmArgs& g = gg.p[sel];
+  const int local = (int)blockIdx.x - sel * gg.tiles0;
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
   int tm, tn;
-  tile_coords(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
+  tile_coords(xcd_remap(local, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -1071,31 +1075,64 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(GemmArgs g) {
 }
 
 // ------------------------------------------------------------------ launch
-template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK, bool PIPE>
-static int launch_mfma(const GemmArgs& g, hipStream_t s) {
-  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  const size_t lds = 2 * (size_t)(BM + BN) * (BK + 8) * sizeof(uint16_t);
-  void (*kern)(GemmArgs);
-  if constexpr (PIPE) kern = gemm_pipe_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
-  else kern = gemm_mfma_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
-  // the dynamic-LDS limit is a per-device attribute of the kernel: set once
-  // per device (bit d of `attr`), safe to race (the call is idempotent)
-  static std::atomic<unsigned long long> attr{0};
+static GemmGroup single(const GemmArgs& g) {
+  GemmGroup r;
+  r.p[0] = g;
+  r.np = 1;
+  return r;
+}
+
+// Sets a kernel's dynamic-LDS limit once per device (bit d of `bits`; safe to
+// race, the call is idempotent).
+static int reserve_lds(std::atomic<unsigned long long>& bits, const void* kern, size_t lds, const char* who) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev > 63) {
-    set_error("gemm_mfma: no current device");
+    set_error(std::string(who) + ": no current device");
     return 3;
   }
-  if (!(attr.load(std::memory_order_acquire) & (1ull << dev))) {
-    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
-      set_error("gemm_mfma: cannot reserve the LDS tile stages");
+  if (!(bits.load(std::memory_order_acquire) & (1ull << dev))) {
+    if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
+      set_error(std::string(who) + ": cannot reserve the LDS tile stages");
       return 3;
     }
-    attr.fetch_or(1ull << dev, std::memory_order_acq_rel);
+    bits.fetch_or(1ull << dev, std::memory_order_acq_rel);
   }
-  launch(kern, dim3(tiles), dim3(WM * WN * 64), (uint32_t)lds, s, g);
-  JG_CHECK_LAUNCH("gemm_mfma");
   return 0;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK>
+static int launch_pipe(const GemmGroup& gr, hipStream_t s) {
+  GemmGroup g = gr;
+  int tiles = 0;
+  for (int p = 0; p < g.np; ++p) {
+    const int t = ((g.p[p].M + BM - 1) / BM) * ((g.p[p].N + BN - 1) / BN);
+    if (p == 0) g.tiles0 = t;
+    tiles += t;
+  }
+  if (g.np == 1) g.tiles0 = tiles;
+  const size_t lds = 2 * (size_t)(BM + BN) * (BK + 8) * sizeof(uint16_t);
+  void (*kern)(GemmGroup) = gemm_pipe_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
+  static std::atomic<unsigned long long> attr{0};
+  if (int rc = reserve_lds(attr, (const void*)kern, lds, "gemm_pipe")) return rc;
+  launch(kern, dim3(tiles), dim3(WM * WN * 64), (uint32_t)lds, s, g);
+  JG_CHECK_LAUNCH("gemm_pipe");
+  return 0;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EK, bool PIPE>
+static int launch_mfma(const GemmArgs& g, hipStream_t s) {
+  if constexpr (PIPE) {
+    return launch_pipe<BM, BN, BK, WM, WN, TA, TB, EK>(single(g), s);
+  } else {
+    const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+    const size_t lds = 2 * (size_t)(BM + BN) * (BK + 8) * sizeof(uint16_t);
+    void (*kern)(GemmArgs) = gemm_mfma_kernel<BM, BN, BK, WM, WN, TA, TB, EK>;
+    static std::atomic<unsigned long long> attr{0};
+    if (int rc = reserve_lds(attr, (const void*)kern, lds, "gemm_mfma")) return rc;
+    launch(kern, dim3(tiles), dim3(WM * WN * 64), (uint32_t)lds, s, g);
+    JG_CHECK_LAUNCH("gemm_mfma");
+    return 0;
+  }
 }
 
 template <bool TA, bool TB, int EK, int BM, int BN, int WM = 2, int WN = 2>
@@ -1160,13 +1197,6 @@ template <bool TA, int EK>
 struct DtlLaunch<TA, false, EK> {
   static int run(const GemmGroup&, hipStream_t, int) { return -1; }
 };
-
-static GemmGroup single(const GemmArgs& g) {
-  GemmGroup r;
-  r.p[0] = g;
-  r.np = 1;
-  return r;
-}
 
 // The direct-to-LDS kernel computes 32-bit byte offsets up to three k tiles
 // past K; they must stay below 2^31.
@@ -1294,12 +1324,23 @@ static int launch_group(const GemmGroup& g, hipStream_t s) {
   return DtlLaunch<TA, true, EK>::run(g, s, dtl_shape(g));
 }
 
+template <int EK>
+static int launch_fwd_group(const GemmGroup& g, hipStream_t s) {
+  long t256 = 0;
+  for (int p = 0; p < g.np; ++p) t256 += (long)((g.p[p].M + 255) / 256) * ((g.p[p].N + 255) / 256);
+  if (t256 < 64) return launch_pipe<128, 128, 64, 2, 2, false, false, EK>(g, s);
+  return launch_pipe<256, 256, 64, 2, 4, false, false, EK>(g, s);
+}
+
 int gemm2(const GemmArgs& a, const GemmArgs& b, hipStream_t s) {
-  // one grouped launch when both products take the same direct-to-LDS kernel
+  // one grouped launch when both products take the same kernel: the
+  // direct-to-LDS kernel (k-strided B: input and weight gradients) or the
+  // register-staged one (forward products, K a multiple of its 64-deep tile)
   const int ek = (a.M > 0 && a.N > 0 && b.M > 0 && b.N > 0 && a.A && a.B && a.epi.C && b.A && b.B && b.epi.C)
                      ? mfma_kind(a) : -1;
-  const bool grouped = ek >= 0 && mfma_kind(b) == ek && a.ta == b.ta && a.tb && b.tb && dtl_fits(a) &&
-                       dtl_fits(b);
+  const bool same = ek >= 0 && mfma_kind(b) == ek && a.ta == b.ta && a.tb == b.tb;
+  const bool fwd = same && !a.ta && !a.tb && a.K % 64 == 0 && b.K % 64 == 0;
+  const bool grouped = fwd || (same && a.tb && dtl_fits(a) && dtl_fits(b));
   if (!grouped) {
     int rc = gemm(a, s);
     return rc ? rc : gemm(b, s);
@@ -1311,6 +1352,16 @@ int gemm2(const GemmArgs& a, const GemmArgs& b, hipStream_t s) {
   g.p[1] = b.K > a.K ? a : b;
   const int pi = prof_begin(prof_class(a));
   int rc;
+  if (fwd) {
+    switch (ek) {
+#define JG_FWD(E) case E: rc = launch_fwd_group<E>(g, s); break;
+      JG_FWD(EK_F32) JG_FWD(EK_F32_ACC) JG_FWD(EK_BF16) JG_FWD(EK_BF16_ACC) JG_FWD(EK_BIAS) JG_FWD(EK_GELU)
+      default: rc = launch_fwd_group<EK_DGELU>(g, s); break;
+#undef JG_FWD
+    }
+    prof_end(pi, 2.0 * ((double)a.M * a.N * a.K + (double)b.M * b.N * b.K));
+    return rc;
+  }
   switch (ek) {
 #define JG_GRP(E) case E: rc = a.ta ? launch_group<true, E>(g, s) : launch_group<false, E>(g, s); break;
     JG_GRP(EK_F32) JG_GRP(EK_F32_ACC) JG_GRP(EK_BF16) JG_GRP(EK_BF16_ACC) JG_GRP(EK_BIAS) JG_GRP(EK_GELU)
