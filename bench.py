@@ -52,10 +52,12 @@ MFMA_BF16_PEAK = 2.5e15     # dense bf16 MFMA, MI355X
 HBM_PEAK = 8.0e12
 
 # HBM traffic of the weight-gradient GEMM class per launch in the block
-# workload, from two rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by
-# the same counters on a 1 GiB device copy; valid only for the GEMM source
-# it was measured on (sha256 of gemm.hip, first 16 hex digits).
-WGRAD_TRAFFIC = {"gemm_src": "ee046861998b99f4", "bytes_per_launch": 710.12e6}
+# workload (one launch = both streams' products of one layer), from two
+# rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters
+# on a 1 GiB device copy (FETCH_SIZE reads 0.5x, WRITE_SIZE 1.0x the bytes);
+# valid only for the GEMM source it was measured on (sha256 of gemm.hip,
+# first 16 hex digits).
+WGRAD_TRAFFIC = {"gemm_src": "93aef00644e157f4", "bytes_per_launch": 1444.0e6}
 
 CLASSES = {"gemm_fwd": 1, "gemm_dgrad": 2, "gemm_wgrad": 3, "attn_fwd": 4, "attn_bwd_kv": 5, "attn_bwd_q": 6,
            "aggregate": 7}
