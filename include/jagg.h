@@ -207,6 +207,16 @@ jagg_status jagg_endpoint_backward(jagg_ctx* ctx, const void* theta, const void*
  * synchronises the context's stream. */
 jagg_status jagg_grad_compare(jagg_ctx* ctx, const void* a, const void* b, size_t n, int dtype, double* out);
 
+/* Failure detection (no operation of the paper: a guard a caller runs on a
+ * gradient before using it): the number of elements of the device vector x
+ * (n elements of `dtype`, 16-byte aligned) that are NaN or +-Inf, i.e. whose
+ * exponent bits are all ones.  count (host): one unsigned 64-bit value, exact.
+ * Flat gradient buffers may be scanned whole: their zero padding counts as
+ * finite.  Uses the head of the bound workspace; synchronises the context's
+ * stream.  EINVAL for a null pointer, n == 0, an unknown dtype, a misaligned x
+ * or a missing or too small workspace, before any launch. */
+jagg_status jagg_count_nonfinite(jagg_ctx* ctx, const void* x, size_t n, int dtype, unsigned long long* count);
+
 /* Gradient quality of one window (gradient-quality appendix, per-group
  * cos(g_jagg, g_exact) and rho; the endpoint-only ablation of the
  * experiments): runs the JAGG group backward into g_jagg, the per-step

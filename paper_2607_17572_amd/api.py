@@ -70,6 +70,7 @@ def lib() -> ctypes.CDLL:
             "jagg_linear_grad": [vp, i, vp, vp, vp, i, i, i, vp, i, f],
             "jagg_endpoint_backward": [vp, vp, vp, i, ctypes.POINTER(vp), ctypes.POINTER(f), i, i, vp, f],
             "jagg_grad_compare": [vp, vp, vp, sz, i, ctypes.POINTER(d)],
+            "jagg_count_nonfinite": [vp, vp, sz, i, ctypes.POINTER(ctypes.c_ulonglong)],
             "jagg_window_quality": [vp, vp, vp, ctypes.POINTER(vp), i, ctypes.POINTER(vp), ctypes.POINTER(f), i, vp, vp,
                                     vp, ctypes.POINTER(d)],
             "jagg_grpo_composites": [vp, ctypes.POINTER(_GrpoWindow), i, vp, vp, vp],
@@ -313,6 +314,14 @@ class Context:
         assert a.numel() == b.numel() and a.dtype == b.dtype
         _check(lib().jagg_grad_compare(self._h, a.data_ptr(), b.data_ptr(), a.numel(), dt, out))
         return tuple(out)
+
+    def count_nonfinite(self, x) -> int:
+        """Number of NaN / +-Inf elements of a device tensor (fp32 or bf16)."""
+        self.ensure_workspace(1)
+        out = ctypes.c_ulonglong()
+        dt = BF16 if x.dtype == _torch().bfloat16 else F32
+        _check(lib().jagg_count_nonfinite(self._h, x.data_ptr(), x.numel(), dt, ctypes.byref(out)))
+        return int(out.value)
 
     def window_quality(self, theta, saved_pair, saved_steps, batch: int, s_list, t, g_jagg, g_exact, g_ablate):
         """(cos_jagg, rho_jagg, cos_ablate, rho_ablate) of one window; the three

@@ -946,20 +946,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
 // ------------------------------------------------------------ dQ from dS^T
 // dQ = dS K with dS^T as stored by the dK/dV kernel: 128 queries per
-// workgroup (32 per wave), 64-key tiles of K and of dS^T stream through four
-// LDS stages.  Per 16-key block c: the K^T fragments of the four 32-row head
-// dimension blocks and the wave's dS^T fragment are transposing LDS reads in
-// the same contraction-slot order; dQ^T += K^T dS^T.  No scores are
-// recomputed: the pass is bound by reading dS^T once.
-constexpr int Q3_QB = 128, Q3_KT = 64;
+// workgroup, 64-key tiles of K and of dS^T stream through four LDS stages
+// (three tiles in flight).  Per 16-key block c: the K^T fragments of the
+// wave's 32-row head-dimension blocks and its dS^T fragment are transposing
+// LDS reads in the same contraction-slot order; dQ^T += K^T dS^T.  No scores
+// are recomputed: the pass is bound by reading dS^T once.  Eight waves, two
+// per SIMD: wave w takes query block w % 4 (32 queries) and head-dimension
+// half w / 4 (two 32-row blocks of dQ^T), so a wave that waits to issue its
+// direct loads leaves the SIMD to the other wave's fragment reads and MFMAs.
+// Each wave issues two of the sixteen 1 KB loads of each 64 x 128 tile.
+constexpr int Q4_QB = 128, Q4_KT = 64;
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_q3_k(AttnBwd a) {
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_q4_k(AttnBwd a) {
   __shared__ __attribute__((aligned(1024))) char K0[16384], S0[16384], K1[16384], S1[16384], K2[16384], S2[16384],
       K3[16384], S3[16384];
   const int bh = blockIdx.y;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
-  const int qb = blockIdx.x * Q3_QB;
-  const int q = qb + w * 32 + c32;
+  const int qw = w & 3, dh = w >> 2;
+  const int qb = blockIdx.x * Q4_QB;
+  const int q = qb + qw * 32 + c32;
   const int N = a.N;
   const size_t base = (size_t)bh * N * DH;
   const float sc = rsqrtf((float)DH);
@@ -968,50 +973,61 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       arsrc((const uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds, (long)a.nk_pad * a.ld_ds * 2);
   ATile at;
   at.init();
-  const int2 wsel = at.tr_sel(w);  // this wave's 32 query columns of the dS^T tile
-  f32x16 dq[4];
+  // direct-load slots of this wave: tile rows 4 (2w + t) + lane / 16, t = 0, 1
+  int lrow[2], lch[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dq[i] = zero16();
-  auto load_tile = [&](char* Kd, char* Sd, int k0) {
-    at.load(RK, Kd, [&](int r) { return k0 + r < N ? (k0 + r) * (DH * 2) : -1; });
-    at.load(RS, Sd, [&](int r) { return ((k0 + r) * a.ld_ds + qb) * 2; });
+  for (int t = 0; t < 2; ++t) {
+    lrow[t] = 4 * (2 * w + t) + lane / 16;
+    lch[t] = (lane % 16) ^ asw(lrow[t]);
+  }
+  const int2 wsel = at.tr_sel(qw), dsel0 = at.tr_sel(2 * dh), dsel1 = at.tr_sel(2 * dh + 1);
+  f32x16 dq[2] = {zero16(), zero16()};
+  auto load_rows = [&](__amdgpu_buffer_rsrc_t R, char* S, auto rowoff) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int ro = rowoff(lrow[t]);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, ALDS(S + (2 * w + t) * 1024), 16, ro < 0 ? AOOB : ro + lch[t] * 16, 0,
+                                               0, 0);
+    }
   };
-  // four stages, three tiles in flight (the pass streams dS^T from HBM)
-  const int ntile = (N + Q3_KT - 1) / Q3_KT;
+  auto load_tile = [&](char* Kd, char* Sd, int k0) {
+    load_rows(RK, Kd, [&](int r) { return k0 + r < N ? (k0 + r) * (DH * 2) : -1; });
+    load_rows(RS, Sd, [&](int r) { return ((k0 + r) * a.ld_ds + qb) * 2; });
+  };
+  const int ntile = (N + Q4_KT - 1) / Q4_KT;
   load_tile(K0, S0, 0);
-  if (ntile > 1) load_tile(K1, S1, Q3_KT);
-  if (ntile > 2) load_tile(K2, S2, 2 * Q3_KT);
+  if (ntile > 1) load_tile(K1, S1, Q4_KT);
+  if (ntile > 2) load_tile(K2, S2, 2 * Q4_KT);
   auto iter = [&](auto ic, int it) {
     constexpr int c = decltype(ic)::value;
     char* Kc = c == 0 ? K0 : (c == 1 ? K1 : (c == 2 ? K2 : K3));
     char* Sc = c == 0 ? S0 : (c == 1 ? S1 : (c == 2 ? S2 : S3));
-    const int k0 = it * Q3_KT;
+    const int k0 = it * Q4_KT;
     // tile it has landed once at most the loads of the later tiles in flight
-    // (8 direct loads per tile and wave) are outstanding
-    if (it + 2 < ntile) attn_barrier<16>();
-    else if (it + 1 < ntile) attn_barrier<8>();
+    // (4 direct loads per tile and wave) are outstanding
+    if (it + 2 < ntile) attn_barrier<8>();
+    else if (it + 1 < ntile) attn_barrier<4>();
     else attn_barrier<0>();
-    // the stage of tile it+3 was last read in iteration it-1
     if (it + 3 < ntile) {
-      if constexpr (c == 0) load_tile(K3, S3, k0 + 3 * Q3_KT);
-      else if constexpr (c == 1) load_tile(K0, S0, k0 + 3 * Q3_KT);
-      else if constexpr (c == 2) load_tile(K1, S1, k0 + 3 * Q3_KT);
-      else load_tile(K2, S2, k0 + 3 * Q3_KT);
+      if constexpr (c == 0) load_tile(K3, S3, k0 + 3 * Q4_KT);
+      else if constexpr (c == 1) load_tile(K0, S0, k0 + 3 * Q4_KT);
+      else if constexpr (c == 2) load_tile(K1, S1, k0 + 3 * Q4_KT);
+      else load_tile(K2, S2, k0 + 3 * Q4_KT);
     }
-    bf16x8 tk[2][4], ts[2];
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) tk[0][dt] = at.tr(Kc, 0, dt);
+    bf16x8 tk[2][2], ts[2];
+    tk[0][0] = at.tr(Kc, 0, dsel0);
+    tk[0][1] = at.tr(Kc, 0, dsel1);
     ts[0] = at.tr(Sc, 0, wsel);
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
       const int cur = cb & 1, nxt = cur ^ 1;
       if (cb + 1 < 4) {
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) tk[nxt][dt] = at.tr(Kc, cb + 1, dt);
+        tk[nxt][0] = at.tr(Kc, cb + 1, dsel0);
+        tk[nxt][1] = at.tr(Kc, cb + 1, dsel1);
         ts[nxt] = at.tr(Sc, cb + 1, wsel);
       }
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(tk[cur][dt], ts[cur], dq[dt]);
+      dq[0] = mfma(tk[cur][0], ts[cur], dq[0]);
+      dq[1] = mfma(tk[cur][1], ts[cur], dq[1]);
     }
   };
   int it = 0;
@@ -1027,13 +1043,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   __builtin_amdgcn_s_waitcnt(0);
   if (q >= N) return;
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       bf16x4 v;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(dq[dt][4 * g + i] * sc);
-      *(bf16x4*)((uint16_t*)a.dQ + base + (size_t)q * DH + 32 * dt + 8 * g + 4 * h) = v;
+      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(dq[j][4 * g + i] * sc);
+      *(bf16x4*)((uint16_t*)a.dQ + base + (size_t)q * DH + 32 * (2 * dh + j) + 8 * g + 4 * h) = v;
     }
 }
 
@@ -1071,7 +1087,7 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   prof_end(pi, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
   pi = prof_begin(PROF_ATTN_BWD_Q);
-  if (v2 && ds) launch(attn_bwd_q3_k, dim3((a.N + Q3_QB - 1) / Q3_QB, a.B * a.H), dim3(256), 0u, s, a);
+  if (v2 && ds) launch(attn_bwd_q4_k, dim3((a.N + Q4_QB - 1) / Q4_QB, a.B * a.H), dim3(512), 0u, s, a);
   else if (v2) launch(attn_bwd_q2_k, dim3((a.N + Q2_QB - 1) / Q2_QB, a.B * a.H), dim3(256), 0u, s, a);
   else launch(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0u, s, a);
   prof_end(pi, 2.0 * nn);

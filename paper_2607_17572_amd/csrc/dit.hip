@@ -1162,6 +1162,24 @@ jagg_status jagg_grad_compare(jagg_ctx* ctx, const void* a, const void* b, size_
   return JAGG_OK;
 }
 
+jagg_status jagg_count_nonfinite(jagg_ctx* ctx, const void* x, size_t n, int dtype, unsigned long long* count) {
+  if (!ctx || !x || !count) return fail(JAGG_EINVAL, "jagg_count_nonfinite: null argument");
+  if (n == 0) return fail(JAGG_EINVAL, "jagg_count_nonfinite: empty vector");
+  if (dtype != JAGG_F32 && dtype != JAGG_BF16) return fail(JAGG_EINVAL, "jagg_count_nonfinite: unknown dtype");
+  if ((uintptr_t)x % 16) return fail(JAGG_EINVAL, "jagg_count_nonfinite: vector must be 16-byte aligned");
+  jg::Ws W0;
+  jagg_status st = need_head_ws(ctx, W0, "jagg_count_nonfinite");
+  if (st) return st;
+  auto* part = (unsigned long long*)W0.spart;
+  auto* slot = (unsigned long long*)W0.score;
+  int rc = jg::count_nonfinite(x, n, dtype, part, slot, ctx->stream);
+  if (rc) return (jagg_status)rc;
+  if (hipMemcpyAsync(count, slot, sizeof(unsigned long long), hipMemcpyDeviceToHost, ctx->stream) != hipSuccess ||
+      hipStreamSynchronize(ctx->stream) != hipSuccess)
+    return fail(JAGG_EDEVICE, "jagg_count_nonfinite: copy of the count failed");
+  return JAGG_OK;
+}
+
 jagg_status jagg_window_quality(jagg_ctx* ctx, const void* theta, const void* saved_pair,
                                 const void* const* saved_steps, int batch, const void* const* s, const float* t, int W,
                                 void* g_jagg, void* g_exact, void* g_ablate, double* out) {

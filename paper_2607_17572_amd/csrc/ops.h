@@ -157,5 +157,9 @@ int grpo_window(const GrpoArgs& a, double* part, float* coef, double* stats, hip
 constexpr int CMP_BLOCKS = 1024;
 size_t compare_part_doubles();
 int grad_compare(const void* a, const void* b, size_t n, int dt, double* part, double* out_dev, hipStream_t s);
+// Number of NaN / +-Inf elements of x (n elements of dt, 16-byte aligned) into
+// *out_dev; part holds CMP_BLOCKS 64-bit partial counts.
+int count_nonfinite(const void* x, size_t n, int dt, unsigned long long* part, unsigned long long* out_dev,
+                    hipStream_t s);
 
 }  // namespace jg

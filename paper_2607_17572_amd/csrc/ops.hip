@@ -55,6 +55,32 @@ __device__ inline void ld8f(const float* p, float* f) {
   const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
   f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
 }
+// 8 consecutive elements of a row kept in their storage type (bf16: 4 VGPRs),
+// converted to fp32 on use exactly as ld8f converts them
+template <typename T>
+struct Raw8;
+template <>
+struct Raw8<uint16_t> {
+  uint4 u;
+  __device__ inline void load(const uint16_t* p) { u = *(const uint4*)p; }
+  __device__ inline float operator[](int e) const {
+    const uint32_t w = e < 2 ? u.x : (e < 4 ? u.y : (e < 6 ? u.z : u.w));
+    return bf2f((e & 1) ? (w >> 16) : (w & 0xffffu));
+  }
+};
+template <>
+struct Raw8<float> {
+  float4 a, b;
+  __device__ inline void load(const float* p) {
+    a = *(const float4*)p;
+    b = *(const float4*)(p + 4);
+  }
+  __device__ inline float operator[](int e) const {
+    const float4 v = e < 4 ? a : b;
+    const int k = e & 3;
+    return k == 0 ? v.x : (k == 1 ? v.y : (k == 2 ? v.z : v.w));
+  }
+};
 __device__ inline void st8f(uint16_t* p, const float* f) {
   uint4 u;
   u.x = f2bf(f[0]) | ((uint32_t)f2bf(f[1]) << 16);
@@ -573,80 +599,95 @@ __global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA
 }
 
 // One wave per row (rows of the chunk dealt round-robin to the LN_W waves),
-// each lane owning NV runs of 8 consecutive columns (16-byte loads).  The row
-// is read once into registers and the next row of the wave is fetched while
-// the current one is finished (one block per CU: 256 KB of registers per wave
-// slot are free for that); the per-column partial sums of the waves are
-// combined through LDS in wave order.
+// each lane owning NV runs of 8 consecutive columns (16-byte loads).  The
+// per-sample factors 1 + scale sit in LDS, x stays in its storage type and the
+// shift-gradient column sums accumulate in the wave's own LDS row, so a wave
+// keeps under 256 VGPRs: two blocks share a CU, and all chunks of a double
+// block's pair (288 of 32 rows) run in one round on 256 CUs.  The per-column
+// partial sums of the waves are combined through LDS in wave order.
 constexpr int LN_W = 4;
 template <typename T, int NV>
-__global__ __launch_bounds__(64 * LN_W) __attribute__((amdgpu_waves_per_eu(1, 1))) void ln_mod_bwd_vec_k(
+__global__ __launch_bounds__(64 * LN_W) __attribute__((amdgpu_waves_per_eu(2, 2))) void ln_mod_bwd_vec_k(
     const float* __restrict__ dA, const T* __restrict__ x, Chunks ch, int c0, const float* __restrict__ mean,
     const float* __restrict__ rstd, const float* __restrict__ mt, const float* __restrict__ mi, int mod_w,
     int sc_off, float* __restrict__ g, float* __restrict__ psc, float* __restrict__ psh) {
   constexpr int D = NV * 512;
-  extern __shared__ float red[];  // [LN_W][D] reduction space
+  extern __shared__ float red[];  // [LN_W][D] column sums per wave, then [D] factors 1 + scale
+  float* const ms = red + LN_W * D;
   const int q = c0 + blockIdx.x;
   int r0, n, b;
   chunk_rows(ch, q, r0, n, b);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const float* mg = ((r0 < ch.B * ch.nt) ? mt : mi) + (size_t)b * mod_w + sc_off;
-  float m[NV * 8];  // 1 + scale of this lane's columns
+  for (int c = threadIdx.x; c < D; c += 64 * LN_W) ms[c] = mg[c] + 1.f;
+  float* const sh = red + w * D + 8 * lane;  // this lane's shift sums
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    ld8f(mg + 8 * lane + 512 * i, m + 8 * i);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) m[8 * i + e] += 1.f;
+    *(float4*)(sh + 512 * i) = make_float4(0.f, 0.f, 0.f, 0.f);
+    *(float4*)(sh + 512 * i + 4) = make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  float asc[NV * 8], ash[NV * 8];
+  __syncthreads();
+  float asc[NV * 8];
 #pragma unroll
-  for (int i = 0; i < NV * 8; ++i) asc[i] = ash[i] = 0.f;
-  float xv[NV * 8], da[NV * 8], xn[NV * 8], dn[NV * 8];
-  auto load_row = [&](int r, float* xo, float* dout) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      ld8f(x + (size_t)r * D + 8 * lane + 512 * i, xo + 8 * i);
-      ld8f(dA + (size_t)r * D + 8 * lane + 512 * i, dout + 8 * i);
-    }
-  };
-  if (w < n) load_row(r0 + w, xv, da);
+  for (int i = 0; i < NV * 8; ++i) asc[i] = 0.f;
+  Raw8<T> xr[NV];
+  float da[NV * 8];
   for (int rr = w; rr < n; rr += LN_W) {
     const int r = r0 + rr;
-    if (rr + LN_W < n) load_row(r + LN_W, xn, dn);  // next row in flight
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      xr[i].load(x + (size_t)r * D + 8 * lane + 512 * i);
+      ld8f(dA + (size_t)r * D + 8 * lane + 512 * i, da + 8 * i);
+    }
     const float mu = mean[r], rs = rstd[r];
+    // opaque per row: the factor reads stay in the loop instead of being
+    // hoisted into 48 registers
+    int mo = 8 * lane;
+    asm volatile("" : "+v"(mo));
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-    for (int i = 0; i < NV * 8; ++i) {
-      const float xhat = (xv[i] - mu) * rs;
-      const float d = da[i] * m[i];
-      asc[i] = fmaf(da[i], xhat, asc[i]);
-      ash[i] += da[i];
-      s1 += d;
-      s2 += d * xhat;
+    for (int i = 0; i < NV; ++i) {
+      float m[8], t[8];
+      ld8f(ms + mo + 512 * i, m);
+      ld8f(sh + 512 * i, t);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = 8 * i + e;
+        const float xhat = (xr[i][e] - mu) * rs;
+        const float d = da[k] * m[e];
+        asc[k] = fmaf(da[k], xhat, asc[k]);
+        t[e] += da[k];
+        s1 += d;
+        s2 += d * xhat;
+      }
+      st8f(sh + 512 * i, t);
     }
     const float m1 = wave_sum(s1) / D, m2 = wave_sum(s2) / D;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int c = 8 * lane + 512 * i;
-      float gv[8];
+      float m[8], gv[8];
+      ld8f(ms + mo + 512 * i, m);
       ld8f(g + (size_t)r * D + c, gv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float xhat = (xv[8 * i + e] - mu) * rs;
-        gv[e] += rs * (da[8 * i + e] * m[8 * i + e] - m1 - xhat * m2);
+        const float xhat = (xr[i][e] - mu) * rs;
+        gv[e] += rs * (da[8 * i + e] * m[e] - m1 - xhat * m2);
       }
       st8f(g + (size_t)r * D + c, gv);
+      // one 8-column block at a time: hoisting all gradient loads spills
+      __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int i = 0; i < NV * 8; ++i) { xv[i] = xn[i]; da[i] = dn[i]; }
   }
+  // shift sums first (already in LDS), then the scale sums through the same rows
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
-    const float* a = pass == 0 ? asc : ash;
+    if (pass == 1) {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) st8f(red + w * D + 8 * lane + 512 * i, a + 8 * i);
+      for (int i = 0; i < NV; ++i) st8f(sh + 512 * i, asc + 8 * i);
+    }
     __syncthreads();
-    float* out = (pass == 0 ? psc : psh) + (size_t)q * D;
+    float* out = (pass == 0 ? psh : psc) + (size_t)q * D;
     for (int c = threadIdx.x; c < D; c += 64 * LN_W) {
       float t = red[c];
 #pragma unroll
@@ -666,7 +707,7 @@ int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int
   if (nc == 0) return 0;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
   if (D % 512 == 0 && D <= 3584 && al16(dA) && al16(x) && al16(g)) {
-    const size_t lds = LN_W * (size_t)D * sizeof(float);
+    const size_t lds = (LN_W + 1) * (size_t)D * sizeof(float);
 #define LNB(T, NV)                                                                                             \
   case NV: {                                                                                                   \
     auto k = ln_mod_bwd_vec_k<T, NV>;                                                                          \
@@ -1641,6 +1682,67 @@ int grad_compare(const void* a, const void* b, size_t n, int dt, double* part, d
   return 0;
 }
 
+
+// ---- non-finite scan: elements whose exponent bits are all ones (NaN, +-Inf),
+// counted exactly in 64-bit integers: per-block counts, then one sum.
+template <typename T>
+__device__ __forceinline__ unsigned nonfinite8(const T* p) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+  unsigned c = 0;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) c += ((w[e] & 0x7f80u) == 0x7f80u) + ((w[e] & 0x7f800000u) == 0x7f800000u);
+  } else {
+    const uint4 v = *(const uint4*)(p + 4);
+    const uint32_t z[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) c += ((w[e] & 0x7f800000u) == 0x7f800000u) + ((z[e] & 0x7f800000u) == 0x7f800000u);
+  }
+  return c;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void nonfinite_pass1_k(const T* x, size_t n, unsigned long long* part) {
+  __shared__ unsigned long long sh[4];
+  unsigned long long c = 0;
+  const size_t nv = n / 8, stride = (size_t)gridDim.x * blockDim.x;
+  const size_t t0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (size_t v = t0; v < nv; v += stride) c += nonfinite8<T>(x + v * 8);
+  if (t0 == 0)  // ragged tail (n % 8 elements)
+    for (size_t e = nv * 8; e < n; ++e) {
+      uint32_t u;
+      if constexpr (sizeof(T) == 2) u = (uint32_t)((const uint16_t*)x)[e] << 16;
+      else u = ((const uint32_t*)x)[e];
+      c += (u & 0x7f800000u) == 0x7f800000u;
+    }
+  for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = sh[0] + sh[1] + sh[2] + sh[3];
+}
+
+__global__ void nonfinite_pass2_k(const unsigned long long* part, int nblk, unsigned long long* out) {
+  if (threadIdx.x == 0) {
+    unsigned long long c = 0;
+    for (int b = 0; b < nblk; ++b) c += part[b];
+    *out = c;
+  }
+}
+
+int count_nonfinite(const void* x, size_t n, int dt, unsigned long long* part, unsigned long long* out_dev,
+                    hipStream_t s) {
+  if (!x || n == 0) { set_error("count_nonfinite: empty or null vector"); return 1; }
+  if (((uintptr_t)x & 15) != 0) { set_error("count_nonfinite: vector must be 16-byte aligned"); return 1; }
+  const size_t nv = n / 8;
+  const unsigned grid = (unsigned)std::max<size_t>(1, std::min<size_t>((nv + 255) / 256, CMP_BLOCKS));
+  if (dt == BF16) hipLaunchKernelGGL(nonfinite_pass1_k<uint16_t>, dim3(grid), dim3(256), 0, s, (const uint16_t*)x, n, part);
+  else hipLaunchKernelGGL(nonfinite_pass1_k<float>, dim3(grid), dim3(256), 0, s, (const float*)x, n, part);
+  LAUNCH_OK("count_nonfinite_pass1");
+  hipLaunchKernelGGL(nonfinite_pass2_k, dim3(1), dim3(64), 0, s, part, (int)grid, out_dev);
+  LAUNCH_OK("count_nonfinite_pass2");
+  return 0;
+}
 
 // ================================================================ GRPO window
 // Phase 2 (upstream gradients of the PPO-clipped GRPO loss through the

@@ -152,6 +152,14 @@ def test_variant_entry_points_reject_bad_arguments():
         assert L.jagg_grad_compare(h, p, p + 4, 8, 0, out) == 1      # unaligned
         assert L.jagg_grad_compare(h, p, p, 8, 5, out) == 1          # dtype
         assert L.jagg_grad_compare(h, p, p, 8, 0, out) == 1          # no workspace bound
+        cnt = ctypes.c_ulonglong(7)
+        assert L.jagg_count_nonfinite(h, None, 8, 0, ctypes.byref(cnt)) == 1   # null vector
+        assert L.jagg_count_nonfinite(h, p, 8, 0, None) == 1                   # null count
+        assert L.jagg_count_nonfinite(h, p, 0, 0, ctypes.byref(cnt)) == 1      # empty
+        assert L.jagg_count_nonfinite(h, p + 4, 8, 0, ctypes.byref(cnt)) == 1  # unaligned
+        assert L.jagg_count_nonfinite(h, p, 8, 5, ctypes.byref(cnt)) == 1      # dtype
+        assert L.jagg_count_nonfinite(h, p, 8, 0, ctypes.byref(cnt)) == 1      # no workspace bound
+        assert cnt.value == 7                                                 # untouched on error
     finally:
         L.jagg_ctx_destroy(h)
 

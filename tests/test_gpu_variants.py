@@ -118,3 +118,29 @@ def test_gradient_quality_w2_is_exact():
     say(f"  {q}")
     for k, v in q.items():
         assert abs(v - 1.0) <= 1e-6, (k, v)
+
+
+@pytest.mark.parametrize("n", [1, 7, 4096, 1000003])
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
+def test_count_nonfinite_matches_numpy(n, dt):
+    """NaN / +-Inf count of a device vector: exact against numpy's isfinite on
+    the same values, with planted NaN, +-Inf, the largest finite magnitudes and
+    subnormals, in the vector body and in its ragged tail."""
+    say(f"case: count non-finite n={n} {dt}")
+    ctx = pk.Context(TINY)
+    x = synth.normal((n,), 900 + n).astype(np.float32)
+    rng = np.random.default_rng(901 + n)
+    big = np.float32(3.3895314e38) if dt == torch.bfloat16 else np.finfo(np.float32).max  # largest finite
+    specials = [np.nan, np.inf, -np.inf, big, -big, np.float32(1e-40), -np.nan]
+    k = min(n, 3 * len(specials))
+    pos = rng.choice(n, size=k, replace=False)
+    for i, p in enumerate(pos):
+        x[p] = specials[i % len(specials)]
+    if n % 8:
+        x[-1] = np.inf  # the ragged tail is scanned too
+    xd = torch.from_numpy(x).to(dt).cuda()
+    got = ctx.count_nonfinite(xd)
+    want = int(np.count_nonzero(~np.isfinite(xd.float().cpu().numpy())))
+    say(f"  count {got} (numpy {want})")
+    assert got == want
+    assert ctx.count_nonfinite(torch.zeros(n, dtype=dt, device="cuda")) == 0
