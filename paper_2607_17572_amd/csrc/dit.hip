@@ -575,26 +575,42 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   };
   // MLP branch: x_out = xm + gate2 * y2
   TRY(gate_bwd(W.g, A.y2, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, W.p1, W.p2, S));
-  for (int s = 0; s < 2; ++s) {
-    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 5 * D, S));
-    TRY(reduce_to_grad(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].fc2.b), m.grad, beta, S));
+  {
+    RedJob j[4];
+    for (int s = 0; s < 2; ++s) {
+      j[s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 5 * D);
+      j[2 + s] = to_grad_job(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].fc2.b), m.grad, beta);
+    }
+    TRY(reduce_jobs(j, 4, S));
   }
   TRY(wg2(W.dY, D, A.h, F, D, F, st[0].fc2.w, st[1].fc2.w));
   TRY(dg2(W.dY, D, st[0].fc2.w, st[1].fc2.w, F, D, F, W.dbig, F, act, EPI_GELU_BWD, A.pre, F));
   TRY(colsum_partials(W.dbig, act, F, F, rm, 0, R, W.p1, S));
-  for (int s = 0; s < 2; ++s) TRY(reduce_to_grad(W.p1, F, c0[s], nc[s], F, G(dth, m, st[s].fc1.b), m.grad, beta, S));
+  {
+    RedJob j[2];
+    for (int s = 0; s < 2; ++s) j[s] = to_grad_job(W.p1, F, c0[s], nc[s], F, G(dth, m, st[s].fc1.b), m.grad, beta);
+    TRY(reduce_jobs(j, 2, S));
+  }
   TRY(wg2(W.dbig, F, A.a2, D, F, D, st[0].fc1.w, st[1].fc1.w));
   TRY(dg2(W.dbig, F, st[0].fc1.w, st[1].fc1.w, D, F, D, W.dA, D, F32));
   TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, 0, R, A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, W.g, W.p1, W.p2, S));
-  for (int s = 0; s < 2; ++s) {
-    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D, S));
-    TRY(reduce_per_sample(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D, S));
+  {
+    RedJob j[4];
+    for (int s = 0; s < 2; ++s) {
+      j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D);
+      j[2 * s + 1] = per_sample_job(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D);
+    }
+    TRY(reduce_jobs(j, 4, S));
   }
   // attention branch: xm = x + gate1 * y1
   TRY(gate_bwd(W.g, A.y1, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, W.p1, W.p2, S));
-  for (int s = 0; s < 2; ++s) {
-    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 2 * D, S));
-    TRY(reduce_to_grad(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].o.b), m.grad, beta, S));
+  {
+    RedJob j[4];
+    for (int s = 0; s < 2; ++s) {
+      j[s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 2 * D);
+      j[2 + s] = to_grad_job(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].o.b), m.grad, beta);
+    }
+    TRY(reduce_jobs(j, 4, S));
   }
   TRY(wg2(W.dY, D, A.O, D, D, D, st[0].o.w, st[1].o.w));
   TRY(dg2(W.dY, D, st[0].o.w, st[1].o.w, D, D, D, W.dO, D, act));
@@ -604,21 +620,30 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   Gains gn{{cx.P(st[0].qg), cx.P(st[1].qg)}, {cx.P(st[0].kg), cx.P(st[1].kg)}};
   TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.qkv, 3 * D, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
                        A.rk, W.dbig, 3 * D, W.p2, S));
-  for (int s = 0; s < 2; ++s) {
-    TRY(reduce_to_grad(W.p2, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh, G(dth, m, st[s].qg), m.grad, beta, S));
-    TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh, G(dth, m, st[s].kg), m.grad,
-                       beta, S));
-  }
+  // the gain partials (W.p2) wait for the qkv bias partials (W.p1): one launch
   TRY(colsum_partials(W.dbig, act, 3 * D, 3 * D, rm, 0, R, W.p1, S));
-  for (int s = 0; s < 2; ++s)
-    TRY(reduce_to_grad(W.p1, 3 * D, c0[s], nc[s], 3 * D, G(dth, m, st[s].qkv.b), m.grad, beta, S));
+  {
+    RedJob j[6];
+    for (int s = 0; s < 2; ++s) {
+      j[3 * s] = to_grad_job(W.p2, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh, G(dth, m, st[s].qg), m.grad,
+                             beta);
+      j[3 * s + 1] = to_grad_job(W.p2 + m.Dh, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh,
+                                 G(dth, m, st[s].kg), m.grad, beta);
+      j[3 * s + 2] = to_grad_job(W.p1, 3 * D, c0[s], nc[s], 3 * D, G(dth, m, st[s].qkv.b), m.grad, beta);
+    }
+    TRY(reduce_jobs(j, 6, S));
+  }
   TRY(wg2(W.dbig, 3 * D, A.a1, D, 3 * D, D, st[0].qkv.w, st[1].qkv.w));
   TRY(dg2(W.dbig, 3 * D, st[0].qkv.w, st[1].qkv.w, D, 3 * D, D, W.dA, D, F32));
   float* const p2s = W.p2 + (size_t)nchunk * QK_PARTS * 2 * m.Dh;
   TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, W.p1, p2s, S));
-  for (int s = 0; s < 2; ++s) {
-    TRY(reduce_per_sample(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D, S));
-    TRY(reduce_per_sample(p2s, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0, S));
+  {
+    RedJob j[4];
+    for (int s = 0; s < 2; ++s) {
+      j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D);
+      j[2 * s + 1] = per_sample_job(p2s, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0);
+    }
+    TRY(reduce_jobs(j, 4, S));
   }
   // adaLN modulation: mod = SiLU(vec) W_mod^T + b, per stream; d SiLU(vec) in the order text, image
   for (int s = 0; s < 2; ++s) {
@@ -639,8 +664,11 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   const SBlock& L = m.sgl[i];
   const int nchunk = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   TRY(gate_bwd(W.g, A.y, act, D, rm, 0, R, A.mod, A.mod, 3 * D, 2 * D, W.dY, D, W.p1, W.p2, cx.s));
-  TRY(reduce_per_sample(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, 2 * D, cx.s));
-  TRY(reduce_to_grad(W.p2, D, 0, nchunk, D, G(dth, m, L.out.b), m.grad, beta, cx.s));
+  {
+    const RedJob j[2] = {per_sample_job(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, 2 * D),
+                         to_grad_job(W.p2, D, 0, nchunk, D, G(dth, m, L.out.b), m.grad, beta)};
+    TRY(reduce_jobs(j, 2, cx.s));
+  }
   TRY(wgrad(cx, W.dY, D, act, A.cat, LC, R, D, LC, G(dth, m, L.out.w), beta));
   // d[O, gelu(u)] = dY W_out: attention part, then the MLP part through GELU'
   TRY(dgrad(cx, W.dY, D, R, cx.P(L.out.w), LC, D, D, W.dO, D, act));
@@ -652,15 +680,22 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   Gains gn{{cx.P(L.qg), cx.P(L.qg)}, {cx.P(L.kg), cx.P(L.kg)}};
   TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.proj, LD, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
                        A.rk, W.dbig, LD, W.p2, cx.s));
-  TRY(reduce_to_grad(W.p2, 2 * m.Dh, 0, nchunk * QK_PARTS, m.Dh, G(dth, m, L.qg), m.grad, beta, cx.s));
-  TRY(reduce_to_grad(W.p2 + m.Dh, 2 * m.Dh, 0, nchunk * QK_PARTS, m.Dh, G(dth, m, L.kg), m.grad, beta, cx.s));
+  // the gain partials (W.p2) wait for the input-projection bias partials (W.p1): one launch
   TRY(colsum_partials(W.dbig, act, LD, LD, rm, 0, R, W.p1, cx.s));
-  TRY(reduce_to_grad(W.p1, LD, 0, nchunk, LD, G(dth, m, L.in.b), m.grad, beta, cx.s));
+  {
+    const RedJob j[3] = {to_grad_job(W.p2, 2 * m.Dh, 0, nchunk * QK_PARTS, m.Dh, G(dth, m, L.qg), m.grad, beta),
+                         to_grad_job(W.p2 + m.Dh, 2 * m.Dh, 0, nchunk * QK_PARTS, m.Dh, G(dth, m, L.kg), m.grad, beta),
+                         to_grad_job(W.p1, LD, 0, nchunk, LD, G(dth, m, L.in.b), m.grad, beta)};
+    TRY(reduce_jobs(j, 3, cx.s));
+  }
   TRY(wgrad(cx, W.dbig, LD, act, A.a, D, R, LD, D, G(dth, m, L.in.w), beta));
   TRY(dgrad(cx, W.dbig, LD, R, cx.P(L.in.w), D, LD, D, W.dA, D, F32));
   TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m, A.r, A.mod, A.mod, 3 * D, D, W.g, W.p1, W.p2, cx.s));
-  TRY(reduce_per_sample(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, D, cx.s));
-  TRY(reduce_per_sample(W.p2, D, rm, 0, R, W.dmod[0], 3 * D, 0, cx.s));
+  {
+    const RedJob j[2] = {per_sample_job(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, D),
+                         per_sample_job(W.p2, D, rm, 0, R, W.dmod[0], 3 * D, 0)};
+    TRY(reduce_jobs(j, 2, cx.s));
+  }
   TRY(small_linear_bwd(W.dmod[0], mvec, 0, B, D, cx.P(L.mod.w), m.act, 3 * D, G(dth, m, L.mod.w), G(dth, m, L.mod.b),
                        m.grad, beta, W.tmp, W.slpart, cx.s));
   TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, cx.s));

@@ -98,6 +98,28 @@ int reduce_to_grad(const float* part, int ld, int chunk0, int nchunk, int N, voi
                    float beta, hipStream_t s);
 int chunk_range(RowMap rm, int row0, int nrows, int* c0, int* nc);
 
+// A list of independent chunk reductions run as one launch, each job with the
+// arithmetic (and so the bits) of reduce_per_sample or reduce_to_grad.
+struct RedJob {
+  const float* part = nullptr;
+  int ld = 0, N = 0;          // partial row stride and columns
+  int kind = 0;               // 0: per sample, 1: into a parameter gradient
+  Chunks ch{};                // per sample: chunk geometry
+  int c0 = 0, nc = 0;         // chunk range
+  float* out = nullptr;       // per sample: out[b*out_stride + out_off + c]
+  int out_stride = 0, out_off = 0;
+  void* g = nullptr;          // gradient: g[c] = beta*g[c] + sum
+  int g_dt = 0;
+  float beta = 0.f;
+  int blk0 = 0;               // first block of the job (set by reduce_jobs)
+};
+constexpr int RED_MAX_JOBS = 8;
+RedJob per_sample_job(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
+                      int out_off);
+RedJob to_grad_job(const float* part, int ld, int chunk0, int nchunk, int N, void* g, int g_dt, float beta);
+// Runs jobs[0..n) (n <= RED_MAX_JOBS) in one launch; 1 on an invalid job.
+int reduce_jobs(const RedJob* jobs, int n, hipStream_t s);
+
 // ---- misc ----
 int patchify(const void* z, int dt, int B, int C, int Hh, int Ww, int p, void* out, hipStream_t s);
 int unpatchify(const void* x, int dt, int B, int C, int Hh, int Ww, int p, void* z, hipStream_t s);

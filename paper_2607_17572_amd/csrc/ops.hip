@@ -1309,6 +1309,104 @@ int reduce_to_grad(const float* part, int ld, int chunk0, int nchunk, int N, voi
   return 0;
 }
 
+// ---- reduction jobs in one launch ----
+struct RedJobs {
+  RedJob j[RED_MAX_JOBS];
+  int n;
+};
+
+RedJob per_sample_job(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
+                      int out_off) {
+  RedJob r;
+  r.part = part;
+  r.ld = r.N = N;
+  r.kind = 0;
+  r.ch = Chunks{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (chunk_range(rm, row0, nrows, &r.c0, &r.nc)) r.N = -1;  // rejected by reduce_jobs
+  r.out = out;
+  r.out_stride = out_stride;
+  r.out_off = out_off;
+  return r;
+}
+
+RedJob to_grad_job(const float* part, int ld, int chunk0, int nchunk, int N, void* g, int g_dt, float beta) {
+  RedJob r;
+  r.part = part;
+  r.ld = ld;
+  r.N = N;
+  r.kind = 1;
+  r.c0 = chunk0;
+  r.nc = nchunk;
+  r.g = g;
+  r.g_dt = g_dt;
+  r.beta = beta;
+  return r;
+}
+
+// Block x of the launch belongs to the job whose block range holds it; inside
+// the job, the block's column group and (per sample) its sample follow the
+// grids of reduce_per_sample_k and reduce_to_grad_k, and so do the sums.
+__global__ __launch_bounds__(1024) void reduce_jobs_k(RedJobs js) {
+  __shared__ float sh[RC_SL][RC_COLS + 1];
+  int k = 0;
+  while (k + 1 < js.n && (int)blockIdx.x >= js.j[k + 1].blk0) ++k;
+  const RedJob& J = js.j[k];
+  const int cl = threadIdx.x % RC_COLS, sl = threadIdx.x / RC_COLS;
+  const int ncol = (J.N + RC_COLS - 1) / RC_COLS;
+  const int local = (int)blockIdx.x - J.blk0;
+  const int c = (local % ncol) * RC_COLS + cl;
+  float acc = 0.f;
+  if (J.kind == 0) {
+    const int b = local / ncol;
+    const int ct = J.ch.ct(), ci = J.ch.ci();
+    const int runs[2][2] = {{b * ct, b * ct + ct}, {J.ch.B * ct + b * ci, J.ch.B * ct + b * ci + ci}};
+    if (c < J.N)
+      for (int r = 0; r < 2; ++r) {
+        const int lo = max(runs[r][0], J.c0), hi = min(runs[r][1], J.c0 + J.nc);
+#pragma unroll 4
+        for (int q = lo + sl; q < hi; q += RC_SL) acc += J.part[(size_t)q * J.ld + c];
+      }
+    const float t = slice_total(acc, sh);
+    if (sl == 0 && c < J.N) J.out[(size_t)b * J.out_stride + J.out_off + c] = t;
+  } else {
+    if (c < J.N) {
+#pragma unroll 4
+      for (int q = J.c0 + sl; q < J.c0 + J.nc; q += RC_SL) acc += J.part[(size_t)q * J.ld + c];
+    }
+    float t = slice_total(acc, sh);
+    if (sl == 0 && c < J.N) {
+      if (J.g_dt == BF16) {
+        if (J.beta != 0.f) t += J.beta * ldf((const uint16_t*)J.g, c);
+        stf((uint16_t*)J.g, c, t);
+      } else {
+        if (J.beta != 0.f) t += J.beta * ldf((const float*)J.g, c);
+        stf((float*)J.g, c, t);
+      }
+    }
+  }
+}
+
+int reduce_jobs(const RedJob* jobs, int n, hipStream_t s) {
+  if (n < 1 || n > RED_MAX_JOBS) { set_error("reduce_jobs: 1..8 jobs"); return 1; }
+  RedJobs js;
+  js.n = n;
+  int blk = 0;
+  for (int k = 0; k < n; ++k) {
+    js.j[k] = jobs[k];
+    const RedJob& J = js.j[k];
+    if (J.N <= 0 || !J.part || (J.kind == 0 && (!J.out || J.ld != J.N)) || (J.kind == 1 && !J.g) || J.kind < 0 ||
+        J.kind > 1) {
+      set_error("reduce_jobs: invalid job");
+      return 1;
+    }
+    js.j[k].blk0 = blk;
+    blk += (J.N + RC_COLS - 1) / RC_COLS * (J.kind == 0 ? J.ch.B : 1);
+  }
+  hipLaunchKernelGGL(reduce_jobs_k, dim3(blk), dim3(RC_COLS * RC_SL), 0, s, js);
+  LAUNCH_OK("reduce_jobs");
+  return 0;
+}
+
 // ================================================================ misc
 template <typename T>
 __global__ void patchify_k(const T* __restrict__ z, int B, int C, int Hh, int Ww, int p, T* __restrict__ out,
