@@ -653,18 +653,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const __amdgpu_buffer_rsrc_t RD = arsrc(a.delta + (size_t)bh * N, (long)N * 4);
   ATile at;
   at.init();
-  // dS in the dQ pass's fragment order (keys beyond N are written too: finite
-  // values that multiply zero key rows there).  Per head, a 1 KB sub-tile per
-  // block of 32 queries and 16 keys, sub-tiles of a query block consecutive:
-  // byte (lane * 16 + 2 p) of sub-tile (q / 32, k / 16) holds query
-  // q = 32 (q / 32) + lane % 32 and, with kk = k % 16, lane / 32 = (kk / 4) % 2,
-  // p = 4 (kk / 8) + kk % 4.  This lane writes key `key` for queries
-  // 4h + {0..3, 8..11, 16..19, 24..27} of each 32-query half.
-  const int kk = c32 & 15;
-  const size_t ds_qblk = (size_t)(a.nk_pad >> 4) * 1024;  // bytes per 32-query block
-  char* const dsl = a.dS ? (char*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds * 2 + (size_t)(key >> 4) * 1024 +
-                               ((kk >> 2) & 1) * 512 + (((kk >> 3) << 2) | (kk & 3)) * 2 + h * 64
-                         : nullptr;
+  // this lane's dS^T row (padded rows beyond N are written too: finite values
+  // that multiply zero key rows in the dQ pass)
+  uint16_t* const dsr = a.dS ? (uint16_t*)a.dS + ((size_t)bh * a.nk_pad + key) * a.ld_ds : nullptr;
 
   bf16x8 kf[8], vf[8];
 #pragma unroll
@@ -764,14 +755,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         const bf16x8 pb = pack8(st, half), db = pack8(dpt, half);
-        if (dsl) {
-          // element i of db: query 16 half + 8 (i / 4) + 4h + i % 4 of this
-          // 32-query half, i.e. lane row + 16 half + 8 (i / 4) + i % 4
+        if (dsr) {
+          // dS^T row of this lane's key: queries 16 half + 4h + 0..3 and
+          // 16 half + 8 + 4h + 0..3 of this 32-query half
           const u32x4 u = __builtin_bit_cast(u32x4, db);
-          char* pt = dsl + (size_t)((q0 >> 5) + t) * ds_qblk + half * 256;
-#pragma unroll
-          for (int i = 0; i < 8; ++i)
-            *(uint16_t*)(pt + (8 * (i >> 2) + (i & 3)) * 16) = (uint16_t)((i & 1) ? (u[i >> 1] >> 16) : u[i >> 1]);
+          uint16_t* pr = dsr + q0 + 32 * t + 16 * half + 4 * h;
+          *(u32x2*)pr = u32x2{u[0], u[1]};
+          *(u32x2*)(pr + 8) = u32x2{u[2], u[3]};
         }
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
@@ -954,84 +944,93 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
 }
 
-// ------------------------------------------------------------ dQ from dS
-// dQ = dS K with dS as stored by the dK/dV kernel, in 1 KB sub-tiles already
-// in the B-operand lane order: each wave (32 queries) streams its query
-// block's sub-tiles from HBM straight into registers, four 64-key tiles ahead
-// (16 KB in flight per wave), with one contiguous 1 KB load per 16-key block.
-// K tiles (64 keys x 128) stream through four LDS stages shared by the four
-// waves; per 16-key block c the K^T fragments of the four 32-row head-dimension
-// blocks are transposing LDS reads whose contraction slots follow the same key
-// order as the sub-tiles: dQ^T += K^T dS.  No scores are recomputed.  64 KB of
-// LDS and under 256 VGPRs: two workgroups per CU.
-constexpr int Q5_QB = 128, Q5_KT = 64;
+// ------------------------------------------------------------ dQ from dS^T
+// dQ = dS K with dS^T as stored by the dK/dV kernel: 128 queries per
+// workgroup, 64-key tiles of K and of dS^T stream through four LDS stages
+// (three tiles in flight).  Per 16-key block c: the K^T fragments of the
+// wave's 32-row head-dimension blocks and its dS^T fragment are transposing
+// LDS reads in the same contraction-slot order; dQ^T += K^T dS^T.  No scores
+// are recomputed: the pass is bound by reading dS^T once.  Eight waves, two
+// per SIMD: wave w takes query block w % 4 (32 queries) and head-dimension
+// half w / 4 (two 32-row blocks of dQ^T), so a wave that waits to issue its
+// direct loads leaves the SIMD to the other wave's fragment reads and MFMAs.
+// Each wave issues two of the sixteen 1 KB loads of each 64 x 128 tile.
+constexpr int Q4_QB = 128, Q4_KT = 64;
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_q5_k(AttnBwd a) {
-  __shared__ __attribute__((aligned(1024))) char K0[16384], K1[16384], K2[16384], K3[16384];
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_q4_k(AttnBwd a) {
+  __shared__ __attribute__((aligned(1024))) char K0[16384], S0[16384], K1[16384], S1[16384], K2[16384], S2[16384],
+      K3[16384], S3[16384];
   const int bh = blockIdx.y;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
-  const int qblk = blockIdx.x * 4 + w;  // this wave's 32-query block
-  const int q = qblk * 32 + c32;
+  const int qw = w & 3, dh = w >> 2;
+  const int qb = blockIdx.x * Q4_QB;
+  const int q = qb + qw * 32 + c32;
   const int N = a.N;
   const size_t base = (size_t)bh * N * DH;
   const float sc = rsqrtf((float)DH);
   const __amdgpu_buffer_rsrc_t RK = arsrc((const uint16_t*)a.K + base, (long)N * DH * 2);
-  // this lane's 16 bytes of the wave's sub-tiles: key block kb at + kb * 1024
-  const char* const dsw = (const char*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds * 2 +
-                          (size_t)qblk * (a.nk_pad >> 4) * 1024 + lane * 16;
-  const int kb_last = (a.nk_pad >> 4) - 1;
+  const __amdgpu_buffer_rsrc_t RS =
+      arsrc((const uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds, (long)a.nk_pad * a.ld_ds * 2);
   ATile at;
   at.init();
-  f32x16 dq[4];
+  // direct-load slots of this wave: tile rows 4 (2w + t) + lane / 16, t = 0, 1
+  int lrow[2], lch[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dq[i] = zero16();
-  // Every load is issued whether its tile exists or not, so that the issue
-  // order (and the waits the compiler derives from it) is the same in every
-  // iteration: K rows at or past N read as zeros through the resource's range
-  // check, and key blocks past the last one re-read the last one.  The tile
-  // count is rounded up to a multiple of 4; the extra tiles add exact zeros
-  // (zero K rows times finite dS).
-  const int ntile = ((N + Q5_KT - 1) / Q5_KT + 3) & ~3;
-  auto load_k = [&](char* Kd, int k0) { at.load(RK, Kd, [&](int r) { return k0 + r < N ? (k0 + r) * (DH * 2) : -1; }); };
-  u32x4 f0[4], f1[4], f2[4], f3[4];  // dS fragments of four tiles in flight
-  auto load_s = [&](u32x4* f, int it) {
+  for (int t = 0; t < 2; ++t) {
+    lrow[t] = 4 * (2 * w + t) + lane / 16;
+    lch[t] = (lane % 16) ^ asw(lrow[t]);
+  }
+  const int2 wsel = at.tr_sel(qw), dsel0 = at.tr_sel(2 * dh), dsel1 = at.tr_sel(2 * dh + 1);
+  f32x16 dq[2] = {zero16(), zero16()};
+  auto load_rows = [&](__amdgpu_buffer_rsrc_t R, char* S, auto rowoff) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) f[c] = *(const u32x4*)(dsw + (size_t)min(4 * it + c, kb_last) * 1024);
+    for (int t = 0; t < 2; ++t) {
+      const int ro = rowoff(lrow[t]);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, ALDS(S + (2 * w + t) * 1024), 16, ro < 0 ? AOOB : ro + lch[t] * 16, 0,
+                                               0, 0);
+    }
   };
-  // issue order: K(0) S(0) K(1) S(1) K(2) S(2) S(3), then per iteration it:
-  // K(it + 3), S(it + 4) (4 loads each per wave)
-  load_k(K0, 0);
-  load_s(f0, 0);
-  load_k(K1, Q5_KT);
-  load_s(f1, 1);
-  load_k(K2, 2 * Q5_KT);
-  load_s(f2, 2);
-  load_s(f3, 3);
+  auto load_tile = [&](char* Kd, char* Sd, int k0) {
+    load_rows(RK, Kd, [&](int r) { return k0 + r < N ? (k0 + r) * (DH * 2) : -1; });
+    load_rows(RS, Sd, [&](int r) { return ((k0 + r) * a.ld_ds + qb) * 2; });
+  };
+  // Every tile load is issued whether the tile exists or not, so that the
+  // issue order (and the waits the compiler derives from it) is the same in
+  // every iteration: K rows at or past N and dS^T rows past the padded key
+  // count read as zeros through the resources' range checks.  The tile count
+  // is rounded up to a multiple of 4; the extra tiles add exact zeros.
+  const int ntile = ((N + Q4_KT - 1) / Q4_KT + 3) & ~3;
+  load_tile(K0, S0, 0);
+  load_tile(K1, S1, Q4_KT);
+  load_tile(K2, S2, 2 * Q4_KT);
   auto iter = [&](auto ic, int it) {
     constexpr int c = decltype(ic)::value;
     char* Kc = c == 0 ? K0 : (c == 1 ? K1 : (c == 2 ? K2 : K3));
-    char* Kn = c == 0 ? K3 : (c == 1 ? K0 : (c == 2 ? K1 : K2));  // stage of tile it+3, read in iteration it-1
-    u32x4* fc = c == 0 ? f0 : (c == 1 ? f1 : (c == 2 ? f2 : f3));
-    // K(it) and S(it) have landed once at most the 20 loads issued after them
-    // are outstanding
-    attn_barrier<20>();
-    load_k(Kn, (it + 3) * Q5_KT);
-    bf16x8 tk[2][4];
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) tk[0][dt] = at.tr(Kc, 0, dt);
+    char* Sc = c == 0 ? S0 : (c == 1 ? S1 : (c == 2 ? S2 : S3));
+    const int k0 = it * Q4_KT;
+    // tile it has landed once at most the loads of the two later tiles in
+    // flight (4 direct loads per tile and wave) are outstanding
+    attn_barrier<8>();
+    // the stage of tile it+3 was last read in iteration it-1
+    if constexpr (c == 0) load_tile(K3, S3, k0 + 3 * Q4_KT);
+    else if constexpr (c == 1) load_tile(K0, S0, k0 + 3 * Q4_KT);
+    else if constexpr (c == 2) load_tile(K1, S1, k0 + 3 * Q4_KT);
+    else load_tile(K2, S2, k0 + 3 * Q4_KT);
+    bf16x8 tk[2][2], ts[2];
+    tk[0][0] = at.tr(Kc, 0, dsel0);
+    tk[0][1] = at.tr(Kc, 0, dsel1);
+    ts[0] = at.tr(Sc, 0, wsel);
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
       const int cur = cb & 1, nxt = cur ^ 1;
       if (cb + 1 < 4) {
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) tk[nxt][dt] = at.tr(Kc, cb + 1, dt);
+        tk[nxt][0] = at.tr(Kc, cb + 1, dsel0);
+        tk[nxt][1] = at.tr(Kc, cb + 1, dsel1);
+        ts[nxt] = at.tr(Sc, cb + 1, wsel);
       }
-      const bf16x8 sf = __builtin_bit_cast(bf16x8, fc[cb]);
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) dq[dt] = mfma(tk[cur][dt], sf, dq[dt]);
+      dq[0] = mfma(tk[cur][0], ts[cur], dq[0]);
+      dq[1] = mfma(tk[cur][1], ts[cur], dq[1]);
     }
-    // the registers of S(it) are free: S(it + 4) goes there
-    load_s(fc, it + 4);
   };
   for (int it = 0; it < ntile; it += 4) {
     iter(std::integral_constant<int, 0>(), it);
@@ -1042,13 +1041,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   __builtin_amdgcn_s_waitcnt(0);
   if (q >= N) return;
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       bf16x4 v;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(dq[dt][4 * g + i] * sc);
-      *(bf16x4*)((uint16_t*)a.dQ + base + (size_t)q * DH + 32 * dt + 8 * g + 4 * h) = v;
+      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(dq[j][4 * g + i] * sc);
+      *(bf16x4*)((uint16_t*)a.dQ + base + (size_t)q * DH + 32 * (2 * dh + j) + 8 * g + 4 * h) = v;
     }
 }
 
@@ -1086,7 +1085,7 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   prof_end(pi, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
   pi = prof_begin(PROF_ATTN_BWD_Q);
-  if (v2 && ds) launch(attn_bwd_q5_k, dim3((a.N + Q5_QB - 1) / Q5_QB, a.B * a.H), dim3(256), 0u, s, a);
+  if (v2 && ds) launch(attn_bwd_q4_k, dim3((a.N + Q4_QB - 1) / Q4_QB, a.B * a.H), dim3(512), 0u, s, a);
   else if (v2) launch(attn_bwd_q2_k, dim3((a.N + Q2_QB - 1) / Q2_QB, a.B * a.H), dim3(256), 0u, s, a);
   else launch(attn_bwd_q_mfma_k, dim3((a.N + Q_QB - 1) / Q_QB, a.B * a.H), dim3(256), 0u, s, a);
   prof_end(pi, 2.0 * nn);
