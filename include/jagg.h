@@ -91,8 +91,13 @@ jagg_status dit_param_layout(const dit_config* cfg, size_t* n_tensors, size_t* n
                              size_t cap);
 
 /* Create a context bound to `hip_stream` (a hipStream_t, or NULL for the null
- * stream) on the current device.  Validates the config.  Host only. */
+ * stream) on the current device.  Validates the config.  Host only.  On its
+ * first backward the context creates one more stream of its own (default
+ * priority) for the double blocks' weight-gradient products; that work is
+ * forked from and joined back into `hip_stream` with events inside each call,
+ * so every call stays ordered on `hip_stream` alone. */
 jagg_status jagg_ctx_create(const dit_config* cfg, void* hip_stream, jagg_ctx** out);
+/* Release the context (and its own stream, after that stream's work is done). */
 void jagg_ctx_destroy(jagg_ctx* ctx);
 
 /* Bytes of the saved-activation buffer for a forward of `batch` samples, and

@@ -321,6 +321,10 @@ struct jagg_ctx {
   hipStream_t stream = nullptr;
   void* ws = nullptr;
   size_t ws_bytes = 0;
+  // second stream for the weight-gradient products of the backward, created on
+  // first use (default priority), with its fork and join events
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
 };
 
 namespace jg {
@@ -331,7 +335,27 @@ struct Ctx {
   hipStream_t s;
   const char* th;  // theta base
   size_t es;       // theta element size
+  // weight-gradient stream of the backward (nullptr: everything on s) and
+  // its fork / join events
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   const void* P(size_t off) const { return th + off * es; }
+  // the stream the next weight-gradient product goes to: the side stream,
+  // after everything issued on s so far
+  hipStream_t fork() const {
+    if (!side) return s;
+    if (hipEventRecord(ev_fork, s) != hipSuccess || hipStreamWaitEvent(side, ev_fork, 0) != hipSuccess) return s;
+    return side;
+  }
+  // s waits for every weight-gradient product issued so far
+  int join() const {
+    if (!side) return 0;
+    if (hipEventRecord(ev_join, side) != hipSuccess || hipStreamWaitEvent(s, ev_join, 0) != hipSuccess) {
+      set_error("backward: joining the weight-gradient stream failed");
+      return 3;
+    }
+    return 0;
+  }
 };
 
 // Y[M][:] = X[M][K] W[rows w_row0..][K]^T + b  (one linear layer or a row slice of it)
@@ -561,7 +585,9 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
                                   G(dth, m, w0), beta);
     const GemmArgs b = wgrad_args(cx, row(dY, r0[1], ld_dy), ld_dy, act, row(X, r0[1], ldx), ldx, nr[1], Nout, Kin,
                                   G(dth, m, w1), beta);
-    return gemm2(a, b, S);
+    // weight gradients feed nothing later in the pass: they go to the
+    // weight-gradient stream, which s joins before dY's buffer is reused
+    return gemm2(a, b, cx.fork());
   };
   auto dg2 = [&](void* dY, int ld_dy, size_t w0, size_t w1, int ldw, int Nout, int Kin, void* out, int ldo, int odt,
                  int mode = EPI_STORE, void* aux = nullptr, int ldaux = 0) {
@@ -602,7 +628,9 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
     }
     TRY(reduce_jobs(j, 4, S));
   }
-  // attention branch: xm = x + gate1 * y1
+  // attention branch: xm = x + gate1 * y1 (W.dY and W.dbig are rewritten
+  // from here on: the fc2 and fc1 weight gradients that read them are done)
+  TRY(cx.join());
   TRY(gate_bwd(W.g, A.y1, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, W.p1, W.p2, S));
   {
     RedJob j[4];
@@ -651,6 +679,7 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
                          G(dth, m, st[s].mod.b), m.grad, beta, W.tmp, W.slpart, S));
     TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, S));
   }
+  TRY(cx.join());  // the next block reuses W.dY and W.dbig
   (void)rowf;
   return 0;
 }
@@ -702,9 +731,37 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   return 0;
 }
 
+// The context's weight-gradient stream and events, created on first use;
+// false (everything stays on the context's stream) if any creation fails.
+static bool side_stream(jagg_ctx* ctx) {
+  if (ctx->side) return true;
+  hipStream_t st = nullptr;
+  hipEvent_t f = nullptr, j = nullptr;
+  if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) == hipSuccess &&
+      hipEventCreateWithFlags(&f, hipEventDisableTiming) == hipSuccess &&
+      hipEventCreateWithFlags(&j, hipEventDisableTiming) == hipSuccess) {
+    ctx->side = st;
+    ctx->fork = f;
+    ctx->join = j;
+    return true;
+  }
+  if (j) (void)hipEventDestroy(j);
+  if (f) (void)hipEventDestroy(f);
+  if (st) (void)hipStreamDestroy(st);
+  (void)hipGetLastError();
+  return false;
+}
+
 static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const void* cot, void* dth, float beta) {
   const Model& m = ctx->m;
   Ctx cx{m, ctx->stream, (const char*)theta, dsize(m.act)};
+  // the double-block weight gradients overlap the rest of the pass on a second
+  // stream, except while a kernel class is timed (each timed kernel runs alone)
+  if (!prof_armed() && side_stream(ctx)) {
+    cx.side = ctx->side;
+    cx.ev_fork = ctx->fork;
+    cx.ev_join = ctx->join;
+  }
   const int act = m.act, D = m.D;
   const size_t es = dsize(act);
   const RowMap rm{B, m.nt, m.ni};
@@ -876,7 +933,16 @@ jagg_status jagg_ctx_create(const dit_config* cfg, void* hip_stream, jagg_ctx** 
   return JAGG_OK;
 }
 
-void jagg_ctx_destroy(jagg_ctx* ctx) { delete ctx; }
+void jagg_ctx_destroy(jagg_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->side) {
+    (void)hipStreamSynchronize(ctx->side);
+    (void)hipEventDestroy(ctx->fork);
+    (void)hipEventDestroy(ctx->join);
+    (void)hipStreamDestroy(ctx->side);
+  }
+  delete ctx;
+}
 
 jagg_status dit_saved_bytes(const jagg_ctx* ctx, int batch, size_t* bytes) {
   if (!ctx || !bytes) return fail(JAGG_EINVAL, "dit_saved_bytes: null argument");
