@@ -28,9 +28,15 @@ struct AttnBwd {
   void* dQ; void* dK; void* dV; int dt_d;
   int B, H, N, Dh, dt;
   RowMap rm;
-  // bf16 MFMA path: the dK/dV kernel stores dS^T here, [B*H][nk_pad][ld_ds]
-  // (key rows, query columns), and dQ = dS K is formed from it without
-  // recomputing the scores (nullptr: the dQ kernel recomputes them)
+  // bf16 MFMA path: the dK/dV kernel stores dS^T here and dQ = dS K is
+  // formed from it without recomputing the scores (nullptr: the dQ kernel
+  // recomputes them).  nk_pad x ld_ds elements per (sample, head), in chunks
+  // of 128 keys x 64 queries (16 KB, key rows of 64 queries): element
+  // (key k, query q) of head bh at
+  //   ((bh * nk_pad / 128 + k / 128) * ld_ds / 64 + q / 64) * 8192
+  //     + (k % 128) * 64 + q % 64,
+  // so that one query tile of a key block is one contiguous 16 KB write and
+  // the dQ pass streams contiguous 8 KB pieces.
   void* dS = nullptr;
   int ld_ds = 0, nk_pad = 0;
 };

@@ -653,9 +653,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const __amdgpu_buffer_rsrc_t RD = arsrc(a.delta + (size_t)bh * N, (long)N * 4);
   ATile at;
   at.init();
-  // this lane's dS^T row (padded rows beyond N are written too: finite values
-  // that multiply zero key rows in the dQ pass)
-  uint16_t* const dsr = a.dS ? (uint16_t*)a.dS + ((size_t)bh * a.nk_pad + key) * a.ld_ds : nullptr;
+  // this lane's dS^T row in the chunks of its key block (rows of keys beyond
+  // N are written too: finite values that multiply zero key rows in the dQ
+  // pass); query tile q0 of the block is chunk q0 / 64
+  uint16_t* const dsr = a.dS ? (uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds +
+                                   (size_t)blockIdx.x * KV2_KB * a.ld_ds + (w * 32 + c32) * 64
+                             : nullptr;
 
   bf16x8 kf[8], vf[8];
 #pragma unroll
@@ -757,9 +760,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const bf16x8 pb = pack8(st, half), db = pack8(dpt, half);
         if (dsr) {
           // dS^T row of this lane's key: queries 16 half + 4h + 0..3 and
-          // 16 half + 8 + 4h + 0..3 of this 32-query half
+          // 16 half + 8 + 4h + 0..3 of this 32-query half, in the tile's
+          // chunk (64 * 128 elements per query tile of the key block)
           const u32x4 u = __builtin_bit_cast(u32x4, db);
-          uint16_t* pr = dsr + q0 + 32 * t + 16 * half + 4 * h;
+          uint16_t* pr = dsr + (size_t)q0 * KV2_KB + 32 * t + 16 * half + 4 * h;
           *(u32x2*)pr = u32x2{u[0], u[1]};
           *(u32x2*)(pr + 8) = u32x2{u[2], u[3]};
         }
@@ -973,13 +977,18 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       arsrc((const uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds, (long)a.nk_pad * a.ld_ds * 2);
   ATile at;
   at.init();
-  // direct-load slots of this wave: tile rows 4 (2w + t) + lane / 16, t = 0, 1
-  int lrow[2], lch[2];
+  // direct-load slots of this wave: tile rows 4 (2w + t) + lane / 16, t = 0, 1;
+  // sof[t]: the slot's byte offset in a tile of the chunked dS^T (a tile row
+  // is 128 queries: source chunks 0-7 in the chunk of the block's first 64
+  // queries, 8-15 in the next chunk, 16 KB on)
+  int lrow[2], lch[2], sof[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     lrow[t] = 4 * (2 * w + t) + lane / 16;
     lch[t] = (lane % 16) ^ asw(lrow[t]);
+    sof[t] = lrow[t] * 128 + (lch[t] >> 3) * 16384 + (lch[t] & 7) * 16;
   }
+  const int nqt = a.ld_ds / 64;
   const int2 wsel = at.tr_sel(qw), dsel0 = at.tr_sel(2 * dh), dsel1 = at.tr_sel(2 * dh + 1);
   f32x16 dq[2] = {zero16(), zero16()};
   auto load_rows = [&](__amdgpu_buffer_rsrc_t R, char* S, auto rowoff) {
@@ -992,7 +1001,13 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   };
   auto load_tile = [&](char* Kd, char* Sd, int k0) {
     load_rows(RK, Kd, [&](int r) { return k0 + r < N ? (k0 + r) * (DH * 2) : -1; });
-    load_rows(RS, Sd, [&](int r) { return ((k0 + r) * a.ld_ds + qb) * 2; });
+    // keys k0 .. k0+63 lie in key block k0 / 128, rows (k0 % 128) ..; key
+    // blocks past the padded count are past the resource and read as zeros
+    const int spart = ((k0 >> 7) * nqt + qb / 64) * 16384 + (k0 & 64) * 128;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(RS, ALDS(Sd + (2 * wave + t) * 1024), 16, spart + sof[t], 0, 0, 0);
   };
   // Every tile load is issued whether the tile exists or not, so that the
   // issue order (and the waits the compiler derives from it) is the same in
@@ -1075,8 +1090,9 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   // the direct-load kernels address dO with 32-bit byte offsets
   const bool v2 = (double)a.rm.rows() * a.ld_do * 2.0 < 2147483000.0 && (double)a.N * DH * 2.0 * 3 < 2147483000.0;
   // stored dS^T: the geometry the kernels assume, and 32-bit offsets per head
+  // (the dQ pass fetches up to four key tiles past the padded count)
   const bool ds = a.dS && a.nk_pad == attn_ds_rows(a.N) && a.ld_ds == attn_ds_ld(a.N) &&
-                  (double)a.nk_pad * a.ld_ds * 2.0 < 2147483000.0 && (uintptr_t)a.dS % 16 == 0;
+                  (double)(a.nk_pad + 512) * a.ld_ds * 2.0 < 2147483000.0 && (uintptr_t)a.dS % 16 == 0;
   AttnBwd ak = a;
   if (!ds) ak.dS = nullptr;
   int pi = prof_begin(PROF_ATTN_BWD_KV);
