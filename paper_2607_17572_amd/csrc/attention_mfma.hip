@@ -593,6 +593,13 @@ struct ATile {
                                                0, 0, 0);
     }
   }
+  // the same 16 loads with precomputed byte offsets off[t] (AOOB: a padding row)
+  __device__ inline void load_at(__amdgpu_buffer_rsrc_t R, char* S, const int* off) const {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, ALDS(S + (wave * 4 + t) * 1024), 16, off[t], 0, 0, 0);
+  }
   // A fragment of rows 32t + (lane % 32), elements 16kb + 8(lane / 32) .. +7
   __device__ inline bf16x8 row(const char* S, int t, int kb) const {
     return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + roff[kb] + t * 8192));
@@ -636,6 +643,7 @@ __device__ __forceinline__ void attn_barrier() {
 // through three LDS stages.
 constexpr int KV2_KB = 128, KV2_QT = 64;
 
+template <bool DS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_kv2_k(AttnBwd a) {
   __shared__ __attribute__((aligned(1024))) char Q0[16384], G0[16384], Q1[16384], G1[16384], Q2[16384], G2[16384];
   __shared__ __attribute__((aligned(256))) float L0[64], D0[64], L1[64], D1[64], L2[64], D2[64];
@@ -656,9 +664,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // this lane's dS^T row in the chunks of its key block (rows of keys beyond
   // N are written too: finite values that multiply zero key rows in the dQ
   // pass); query tile q0 of the block is chunk q0 / 64
-  uint16_t* const dsr = a.dS ? (uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds +
-                                   (size_t)blockIdx.x * KV2_KB * a.ld_ds + (w * 32 + c32) * 64
-                             : nullptr;
+  uint16_t* const dsr = DS ? (uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds +
+                                 (size_t)blockIdx.x * KV2_KB * a.ld_ds + (w * 32 + c32) * 64
+                           : nullptr;
 
   bf16x8 kf[8], vf[8];
 #pragma unroll
@@ -675,16 +683,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
 
   // token q of sample b sits at row q + gofs_t (text, q < nt) or q + gofs_i
-  // (image) of dO: branch-free byte offsets (rows and row bytes < 2^24)
+  // (image) of dO (rows and row bytes < 2^24).  Per load slot t, the byte
+  // offsets at q0 = 0 of the lane's chunk in Q and in a text or an image row
+  // of dO; a tile adds its q0 part.
   const int gofs_t = b * a.rm.nt, gofs_i = a.rm.B * a.rm.nt + b * a.rm.ni - a.rm.nt;
-  const int grow = a.ld_do * 2, gcol = hd * DH * 2;
+  const int grow = a.ld_do * 2, nt = a.rm.nt;
+  int qoff[4], gtxt[4], gimg[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int ch = at.lchunk[t] * 16;
+    qoff[t] = at.lrow[t] * (DH * 2) + ch;
+    gtxt[t] = __mul24(at.lrow[t] + gofs_t, grow) + hd * DH * 2 + ch;
+    gimg[t] = __mul24(at.lrow[t] + gofs_i, grow) + hd * DH * 2 + ch;
+  }
   auto load_tile = [&](char* Qd, char* Gd, float* Ld, float* Dd, int q0) {
-    at.load(RQ, Qd, [&](int r) { return (q0 + r) * (DH * 2); });
-    at.load(RG, Gd, [&](int r) {
-      const int q = q0 + r;
-      const int row = q + (q < a.rm.nt ? gofs_t : gofs_i);
-      return q < N ? __mul24(row, grow) + gcol : -1;
-    });
+    int oq[4], og[4];
+    const int qb = q0 * (DH * 2), gb = __mul24(q0, grow);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int q = q0 + at.lrow[t];
+      oq[t] = qoff[t] + qb;
+      og[t] = q < N ? (q < nt ? gtxt[t] : gimg[t]) + gb : AOOB;
+    }
+    at.load_at(RQ, Qd, oq);
+    at.load_at(RG, Gd, og);
     if (w == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(RL, ALDS(Ld), 4, (q0 + lane) * 4, 0, 0, 0);
     if (w == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(RD, ALDS(Dd), 4, (q0 + lane) * 4, 0, 0, 0);
   };
@@ -758,7 +780,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         const bf16x8 pb = pack8(st, half), db = pack8(dpt, half);
-        if (dsr) {
+        if constexpr (DS) {
           // dS^T row of this lane's key: queries 16 half + 4h + 0..3 and
           // 16 half + 8 + 4h + 0..3 of this 32-query half, in the tile's
           // chunk (64 * 128 elements per query tile of the key block)
@@ -1096,7 +1118,8 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   AttnBwd ak = a;
   if (!ds) ak.dS = nullptr;
   int pi = prof_begin(PROF_ATTN_BWD_KV);
-  if (v2) launch(attn_bwd_kv2_k, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0u, s, ak);
+  if (v2 && ds) launch(attn_bwd_kv2_k<true>, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0u, s, ak);
+  else if (v2) launch(attn_bwd_kv2_k<false>, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0u, s, ak);
   else launch(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0u, s, a);
   prof_end(pi, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");

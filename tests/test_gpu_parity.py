@@ -37,6 +37,11 @@ BLOCK_MID = pk.Config(n_double=1, n_single=0, hidden=512, heads=4, head_dim=128,
 BLOCK_GRP = pk.Config(n_double=1, n_single=0, hidden=384, heads=3, head_dim=128, mlp_hidden=1536, in_ch=16, patch=2,
                       lat_h=16, lat_w=16, n_txt=32, txt_dim=384, t_freq_dim=256, block_only=1, act_dtype=pk.BF16,
                       grad_dtype=pk.F32)
+# 144 image + 37 text tokens: two 128-key blocks of the attention backward,
+# the second ragged, and a ragged last 64-query tile
+BLOCK_2KB = pk.Config(n_double=1, n_single=0, hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_ch=16, patch=2,
+                      lat_h=24, lat_w=24, n_txt=37, txt_dim=256, t_freq_dim=256, block_only=1, act_dtype=pk.BF16,
+                      grad_dtype=pk.F32)
 FULL_SMALL = pk.Config(n_double=1, n_single=1, hidden=256, heads=2, head_dim=128, mlp_hidden=512, in_ch=16, patch=2,
                        lat_h=16, lat_w=20, n_txt=24, txt_dim=128, t_freq_dim=256, act_dtype=pk.BF16, grad_dtype=pk.F32)
 
@@ -102,6 +107,17 @@ def test_bf16_block_hidden512_matches_oracle():
     cs = Case(BLOCK_MID, B=2, W=4)
     eg, worst = compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 2e-2)
     say(f"bf16 block512 jagg rel L2 {eg:.2e}, worst {worst}")
+
+
+def test_bf16_block_two_key_blocks_ragged_matches_oracle():
+    """The stored dS^T chunks (128 keys x 64 queries) across two key blocks
+    and four query tiles, with a ragged key block and query tile."""
+    say("case: bf16 block 144+37 tokens (two key blocks, ragged) jagg W=4 B=2")
+    cs = Case(BLOCK_2KB, B=2, W=4)
+    eg, worst = compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 2e-2)
+    say(f"bf16 block 181 tokens jagg rel L2 {eg:.2e}, worst {worst}")
+    eg, worst = compare_grads(cs, cs.gpu_perstep(), cs.oracle_exact(), 2e-2)
+    say(f"  per-step rel L2 {eg:.2e}, worst {worst}")
 
 
 @pytest.mark.parametrize("gdt", [pk.F32, pk.BF16], ids=["f32grad", "bf16grad"])
