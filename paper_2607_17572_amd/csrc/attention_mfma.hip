@@ -1003,30 +1003,26 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // sof[t]: the slot's byte offset in a tile of the chunked dS^T (a tile row
   // is 128 queries: source chunks 0-7 in the chunk of the block's first 64
   // queries, 8-15 in the next chunk, 16 KB on)
-  int lrow[2], lch[2], sof[2];
+  // kof[t]: the slot's byte offset in a K tile at k0 = 0
+  int sof[2], kof[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    lrow[t] = 4 * (2 * w + t) + lane / 16;
-    lch[t] = (lane % 16) ^ asw(lrow[t]);
-    sof[t] = lrow[t] * 128 + (lch[t] >> 3) * 16384 + (lch[t] & 7) * 16;
+    const int lrow = 4 * (2 * w + t) + lane / 16, lch = (lane % 16) ^ asw(lrow);
+    sof[t] = lrow * 128 + (lch >> 3) * 16384 + (lch & 7) * 16;
+    kof[t] = lrow * (DH * 2) + lch * 16;
   }
   const int nqt = a.ld_ds / 64;
   const int2 wsel = at.tr_sel(qw), dsel0 = at.tr_sel(2 * dh), dsel1 = at.tr_sel(2 * dh + 1);
   f32x16 dq[2] = {zero16(), zero16()};
-  auto load_rows = [&](__amdgpu_buffer_rsrc_t R, char* S, auto rowoff) {
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int ro = rowoff(lrow[t]);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(R, ALDS(S + (2 * w + t) * 1024), 16, ro < 0 ? AOOB : ro + lch[t] * 16, 0,
-                                               0, 0);
-    }
-  };
   auto load_tile = [&](char* Kd, char* Sd, int k0) {
-    load_rows(RK, Kd, [&](int r) { return k0 + r < N ? (k0 + r) * (DH * 2) : -1; });
-    // keys k0 .. k0+63 lie in key block k0 / 128, rows (k0 % 128) ..; key
-    // blocks past the padded count are past the resource and read as zeros
-    const int spart = ((k0 >> 7) * nqt + qb / 64) * 16384 + (k0 & 64) * 128;
+    // K rows at or past N and key blocks past the padded count lie past
+    // their resources and read as zeros; keys k0 .. k0+63 lie in key block
+    // k0 / 128 of dS^T, rows (k0 % 128) ..
+    const int kpart = k0 * (DH * 2), spart = ((k0 >> 7) * nqt + qb / 64) * 16384 + (k0 & 64) * 128;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(RK, ALDS(Kd + (2 * wave + t) * 1024), 16, kpart + kof[t], 0, 0, 0);
 #pragma unroll
     for (int t = 0; t < 2; ++t)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(RS, ALDS(Sd + (2 * wave + t) * 1024), 16, spart + sof[t], 0, 0, 0);
