@@ -842,6 +842,150 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
 }
 
+// ------------------------------------------------------------ forward (v2)
+// 128 queries per workgroup (32 per wave, Q^T fragments in registers); key
+// tiles of 64 rows of K and V stream through two LDS stages by direct loads,
+// one barrier per tile.  Two stages (64 KB) and 228 registers let two
+// workgroups share a CU, so that one's softmax work overlaps the other's
+// MFMAs (with three stages and one workgroup per CU the kernel was 1.3x
+// slower).  S^T = K Q^T from row fragments of the K tile;
+// O^T += V^T P^T from transposing reads of the V tile, in the contraction-slot
+// order of the accumulator-fed P^T.  Rows of K and V past N load as zeros; the
+// keys past N are masked in the ragged last tile only.
+constexpr int F2_QB = 128, F2_KT = 64;
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd2_k(AttnFwd a) {
+  __shared__ __attribute__((aligned(1024))) char K0[16384], V0[16384], K1[16384], V1[16384];
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
+  const int q = blockIdx.x * F2_QB + w * 32 + c32;  // this lane's query
+  const int N = a.N;
+  const size_t base = (size_t)bh * N * DH;
+  const uint16_t* Q = (const uint16_t*)a.Q + base;
+  const float sc = rsqrtf((float)DH) * LOG2E;
+  const __amdgpu_buffer_rsrc_t RK = arsrc((const uint16_t*)a.K + base, (long)N * DH * 2);
+  const __amdgpu_buffer_rsrc_t RV = arsrc((const uint16_t*)a.V + base, (long)N * DH * 2);
+  ATile at;
+  at.init();
+  // per load slot: byte offset of the lane's chunk in a tile at k0 = 0
+  int koff[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) koff[t] = at.lrow[t] * (DH * 2) + at.lchunk[t] * 16;
+  auto load_tile = [&](char* Kd, char* Vd, int k0) {
+    int o[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) o[t] = koff[t] + k0 * (DH * 2);
+    at.load_at(RK, Kd, o);
+    at.load_at(RV, Vd, o);
+  };
+
+  bf16x8 qf[8];
+#pragma unroll
+  for (int kb = 0; kb < 8; ++kb) {
+    if (q < N) qf[kb] = ld8(Q + (size_t)q * DH + kb * 16 + h * 8);
+    else qf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+  }
+  f32x16 o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = zero16();
+  float m = -INFINITY, l = 0.f;
+
+  const int ntile = (N + F2_KT - 1) / F2_KT, nfull = N / F2_KT;
+  load_tile(K0, V0, 0);
+  // one key tile; MASK: the ragged last tile (no further loads)
+  auto iter = [&](auto ic, auto mc, int it) {
+    constexpr int c = decltype(ic)::value;
+    constexpr bool MASK = decltype(mc)::value;
+    const char* Kc = c == 0 ? K0 : K1;
+    const char* Vc = c == 0 ? V0 : V1;
+    const int k0 = it * F2_KT;
+    // tile it has landed (its loads are this wave's last); the other stage,
+    // for tile it+1, was last read in the previous iteration
+    attn_barrier<0>();
+    if constexpr (!MASK) {
+      if constexpr (c == 0) load_tile(K1, V1, k0 + F2_KT);
+      else load_tile(K0, V0, k0 + F2_KT);
+    }
+    // S^T: lane = query column, key rows 32t + 8(e/4) + 4h + e%4
+    f32x16 st[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      bf16x8 fk[8];
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) fk[kb] = at.row(Kc, t, kb);
+      st[t] = mfma(fk[0], qf[0], zero16());
+#pragma unroll
+      for (int kb = 1; kb < 8; ++kb) st[t] = mfma(fk[kb], qf[kb], st[t]);
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float sv = st[t][e] * sc;
+        if (MASK && k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3) >= N) sv = -INFINITY;
+        st[t][e] = sv;
+        mx = fmaxf(mx, sv);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m, mx);
+    const float corr = __builtin_amdgcn_exp2f(m - mn);
+    float ls = 0.f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float p = __builtin_amdgcn_exp2f(st[t][e] - mn);
+        st[t][e] = p;
+        ls += p;
+      }
+    l = l * corr + ls;
+    m = mn;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[i][e] *= corr;
+    // O^T += V^T P^T, 16 keys (tile rows 16 cb ..) per step
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const bf16x8 pb = pack8(st[cb >> 1], cb & 1);
+      bf16x8 tv[4];
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) tv[dt] = at.tr(Vc, cb, dt);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) o[dt] = mfma(tv[dt], pb, o[dt]);
+    }
+  };
+  using F = std::false_type;
+  using T = std::true_type;
+  int it = 0;
+  for (; it + 1 < nfull; it += 2) {
+    iter(std::integral_constant<int, 0>(), F(), it);
+    iter(std::integral_constant<int, 1>(), F(), it + 1);
+  }
+  if (it < nfull) iter(std::integral_constant<int, 0>(), F(), it);
+  if (nfull < ntile) {  // ragged last tile
+    if (nfull % 2 == 0) iter(std::integral_constant<int, 0>(), T(), nfull);
+    else iter(std::integral_constant<int, 1>(), T(), nfull);
+  }
+  // no direct load may still be landing when the workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(0);
+  l += __shfl_xor(l, 32, 64);
+  if (q >= N) return;
+  const float inv = 1.f / l;
+  uint16_t* O = (uint16_t*)a.O + (size_t)row_of_tok_m(a.rm, b, q) * a.ld_o + hd * DH;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (__bf16)(o[dt][4 * g + i] * inv);
+      *(bf16x4*)(O + 32 * dt + 8 * g + 4 * h) = v;
+    }
+  if (h == 0) a.lse[(size_t)bh * N + q] = (m + __log2f(l)) * LN2;
+}
+
 // ------------------------------------------------------------ dQ (v2)
 // 128 queries per workgroup (32 per wave, Q and dO fragments in registers);
 // key tiles of 64 rows of K and V stream through three LDS stages.
@@ -1094,7 +1238,11 @@ int attention_fwd_mfma(const AttnFwd& a, hipStream_t s) {
   dim3 grid((a.N + F_QB - 1) / F_QB, a.B * a.H);
   const double nn = (double)a.B * a.H * a.N * (double)a.N * DH;
   const int pi = prof_begin(PROF_ATTN_FWD);
-  launch(attn_fwd_mfma_k, grid, dim3(256), 0u, s, a);
+  // the direct-load kernel addresses K and V with 32-bit byte offsets
+  if ((double)a.N * DH * 2.0 * 3 < 2147483000.0)
+    launch(attn_fwd2_k, dim3((a.N + F2_QB - 1) / F2_QB, a.B * a.H), dim3(256), 0u, s, a);
+  else
+    launch(attn_fwd_mfma_k, grid, dim3(256), 0u, s, a);
   prof_end(pi, 4.0 * nn);
   JG_CHECK_LAUNCH("attention_fwd_mfma");
   return 0;
