@@ -109,6 +109,20 @@ def test_bf16_block_hidden512_matches_oracle():
     say(f"bf16 block512 jagg rel L2 {eg:.2e}, worst {worst}")
 
 
+def test_bf16_full_model_forward_matches_oracle():
+    """The bf16 forward output (MFMA attention forward over two 128-query
+    blocks and a ragged last 64-key tile, 168 tokens) against the oracle on
+    the same bf16-rounded parameters and inputs."""
+    import dataclasses
+    say("case: bf16 full model forward, 144+24 tokens")
+    cs = Case(dataclasses.replace(FULL_SMALL, lat_h=24, lat_w=24), B=2, W=1, t=[0.6])
+    v, _ = cs.forward(0, saved=False)
+    want, _ = mmdit.forward(cs.oc, cs.P(), cs.inputs[0])
+    err = rel_l2(v.double().cpu().numpy(), want)
+    say(f"  forward rel L2 {err:.2e}")
+    assert err <= 2e-2
+
+
 def test_bf16_block_two_key_blocks_ragged_matches_oracle():
     """The stored dS^T chunks (128 keys x 64 queries) across two key blocks
     and four query tiles, with a ragged key block and query tile."""
