@@ -123,6 +123,25 @@ def test_bf16_full_model_forward_matches_oracle():
     assert err <= 2e-2
 
 
+@pytest.mark.parametrize("lat,n_txt", [(8, 10), (16, 64)], ids=["26_tokens", "128_tokens"])
+def test_bf16_block_tile_edges_match_oracle(lat, n_txt):
+    """Sequence lengths at the attention kernels' tile edges: 26 tokens (less
+    than one 64-key tile, only the masked tile) and 128 tokens (whole tiles,
+    no masked tile), forward output and JAGG gradient."""
+    import dataclasses
+    cfg = dataclasses.replace(BLOCK_SMALL, lat_h=lat, lat_w=lat, n_txt=n_txt)
+    say(f"case: bf16 block, {(lat // 2) ** 2}+{n_txt} tokens")
+    cs = Case(cfg, B=2, W=4)
+    v, _ = cs.forward(0, saved=False)
+    (wt, wi), _ = mmdit.forward(cs.oc, cs.P(), cs.inputs[0])
+    from harness import stream_major
+    err = rel_l2(v.double().cpu().numpy(), stream_major(wt, wi))
+    say(f"  forward rel L2 {err:.2e}")
+    assert err <= 2e-2
+    eg, worst = compare_grads(cs, cs.gpu_jagg(), cs.oracle_jagg(), 2e-2)
+    say(f"  jagg rel L2 {eg:.2e}, worst {worst}")
+
+
 def test_bf16_block_two_key_blocks_ragged_matches_oracle():
     """The stored dS^T chunks (128 keys x 64 queries) across two key blocks
     and four query tiles, with a ragged key block and query tile."""
