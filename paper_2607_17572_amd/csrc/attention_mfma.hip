@@ -637,195 +637,211 @@ __device__ __forceinline__ void attn_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// ------------------------------------------------------------ dK, dV (v2)
-// 128 keys per workgroup (32 per wave, K and V fragments in registers); query
-// tiles of 64 rows of Q and dO, with their log-sum-exp and delta, stream
-// through three LDS stages.
-constexpr int KV2_KB = 128, KV2_QT = 64;
+// Fragment reads of the direct-loaded tiles with two registers of per-lane
+// offsets: the row fragment of k16 step kb is at roff0 ^ (kb << 5) and the
+// transposing reads of column block dt at t10 ^ (dt << 6), t20 ^ (dt << 6)
+// (the swizzle XORs the 16-byte chunk index, and kb and dt select its upper
+// bits), so one offset per pattern serves all steps.
+struct ATileX {
+  int roff0, t10, t20;
+  __device__ inline void init() {
+    const int lane = threadIdx.x & 63, rr = lane & 31, h = lane >> 5;
+    roff0 = rr * 256 + ((h ^ asw(rr)) << 4);
+    const int2 o = ATile::tr_off(lane, 0);
+    t10 = o.x;
+    t20 = o.y;
+  }
+  __device__ inline bf16x8 row(const char* S, int t, int kb) const {
+    return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + (roff0 ^ (kb << 5)) + t * 8192));
+  }
+  __device__ inline bf16x8 tr(const char* S, int c, int dt) const {
+    const s16x4 lo =
+        __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + (t10 ^ (dt << 6)) + c * 4096));
+    const s16x4 hi =
+        __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + (t20 ^ (dt << 6)) + c * 4096));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+  }
+};
+
+// ------------------------------------------------------------ dK, dV (v5)
+// Two waves per SIMD: eight waves per workgroup of 128 keys.  Wave w takes
+// the 32 keys 32 (w % 4) .. of the block and the 32-query half w / 4 of every
+// 64-query tile.  K and V of the block stay in LDS and are read as B
+// fragments, so that a wave fits in 256 registers; the two waves of a key
+// group add their partial dV and dK through LDS at the end, in fixed order.
+// Query tiles stream through two stages, one barrier per tile.  No mask: rows
+// of Q, dO, log-sum-exp and delta past N load as zeros, which gives a padded
+// query dP = 0 and delta = 0, hence dS = 0 and no share of dV or dK; the tile
+// count is rounded up to the two-stage unroll with zero tiles, and dS^T stores
+// past the padded width fall outside the store resource.
+constexpr int KV5_KB = 128, KV5_QT = 64;
 
 template <bool DS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void attn_bwd_kv2_k(AttnBwd a) {
-  __shared__ __attribute__((aligned(1024))) char Q0[16384], G0[16384], Q1[16384], G1[16384], Q2[16384], G2[16384];
-  __shared__ __attribute__((aligned(256))) float L0[64], D0[64], L1[64], D1[64], L2[64], D2[64];
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_kv5_k(AttnBwd a) {
+  __shared__ __attribute__((aligned(1024))) char KS[32768], VS[32768], Q0[16384], G0[16384], Q1[16384], G1[16384];
+  __shared__ __attribute__((aligned(256))) float L0[64], D0[64], L1[64], D1[64];
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
-  const int key = blockIdx.x * KV2_KB + w * 32 + c32;
+  const int kg = w & 3, th = w >> 2;  // key group, query half
+  const int key = blockIdx.x * KV5_KB + kg * 32 + c32;
   const int N = a.N;
   const size_t base = (size_t)bh * N * DH;
-  const uint16_t* K = (const uint16_t*)a.K + base;
-  const uint16_t* V = (const uint16_t*)a.V + base;
   const float sc = rsqrtf((float)DH), scl = sc * LOG2E;
+  const __amdgpu_buffer_rsrc_t RK = arsrc((const uint16_t*)a.K + base, (long)N * DH * 2);
+  const __amdgpu_buffer_rsrc_t RV = arsrc((const uint16_t*)a.V + base, (long)N * DH * 2);
   const __amdgpu_buffer_rsrc_t RQ = arsrc((const uint16_t*)a.Q + base, (long)N * DH * 2);
   const __amdgpu_buffer_rsrc_t RG = arsrc(a.dO, (long)a.rm.rows() * a.ld_do * 2);
   const __amdgpu_buffer_rsrc_t RL = arsrc(a.delta + (size_t)a.B * a.H * N + (size_t)bh * N, (long)N * 4);
   const __amdgpu_buffer_rsrc_t RD = arsrc(a.delta + (size_t)bh * N, (long)N * 4);
-  ATile at;
+  // this head's dS^T chunks; this lane's key row in its key block
+  const __amdgpu_buffer_rsrc_t RS =
+      arsrc(DS ? (const uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds : nullptr, DS ? (long)a.nk_pad * a.ld_ds * 2 : 0);
+  const int srow = (blockIdx.x * KV5_KB * a.ld_ds + (kg * 32 + c32) * 64) * 2;
+  ATileX at;  // fragment offsets (the direct-load slots below are for 8 waves)
   at.init();
-  // this lane's dS^T row in the chunks of its key block (rows of keys beyond
-  // N are written too: finite values that multiply zero key rows in the dQ
-  // pass); query tile q0 of the block is chunk q0 / 64
-  uint16_t* const dsr = DS ? (uint16_t*)a.dS + (size_t)bh * a.nk_pad * a.ld_ds +
-                                 (size_t)blockIdx.x * KV2_KB * a.ld_ds + (w * 32 + c32) * 64
-                           : nullptr;
 
-  bf16x8 kf[8], vf[8];
-#pragma unroll
-  for (int kb = 0; kb < 8; ++kb) {
-    if (key < N) {
-      kf[kb] = ld8(K + (size_t)key * DH + kb * 16 + h * 8);
-      vf[kb] = ld8(V + (size_t)key * DH + kb * 16 + h * 8);
-    } else {
-      kf[kb] = vf[kb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
-    }
-  }
-  f32x16 dv[4], dk[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
-
-  // token q of sample b sits at row q + gofs_t (text, q < nt) or q + gofs_i
-  // (image) of dO (rows and row bytes < 2^24).  Per load slot t, the byte
-  // offsets at q0 = 0 of the lane's chunk in Q and in a text or an image row
-  // of dO; a tile adds its q0 part.
-  const int gofs_t = b * a.rm.nt, gofs_i = a.rm.B * a.rm.nt + b * a.rm.ni - a.rm.nt;
-  const int grow = a.ld_do * 2, nt = a.rm.nt;
-  int qoff[4], gtxt[4], gimg[4];
+  // direct loads for 8 waves: 1 KB slot s holds rows 4s .. 4s+3
+  auto slot_off = [&](int s) {
+    const int row = 4 * s + lane / 16;
+    return int2{row, ((lane % 16) ^ asw(row)) << 4};
+  };
+  // K and V of the block: 32 slots each, 4 per wave
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const int ch = at.lchunk[t] * 16;
-    qoff[t] = at.lrow[t] * (DH * 2) + ch;
-    gtxt[t] = __mul24(at.lrow[t] + gofs_t, grow) + hd * DH * 2 + ch;
-    gimg[t] = __mul24(at.lrow[t] + gofs_i, grow) + hd * DH * 2 + ch;
+    const int s = 4 * w + t;
+    const int2 o = slot_off(s);
+    const int off = (blockIdx.x * KV5_KB + o.x) * (DH * 2) + o.y;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(RK, ALDS(KS + s * 1024), 16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(RV, ALDS(VS + s * 1024), 16, off, 0, 0, 0);
   }
+  // query tiles: 16 slots per operand, 2 per wave
+  const int gofs_t = b * a.rm.nt, gofs_i = a.rm.B * a.rm.nt + b * a.rm.ni - a.rm.nt;
+  const int grow = a.ld_do * 2, nt = a.rm.nt;
   auto load_tile = [&](char* Qd, char* Gd, float* Ld, float* Dd, int q0) {
-    int oq[4], og[4];
-    const int qb = q0 * (DH * 2), gb = __mul24(q0, grow);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int q = q0 + at.lrow[t];
-      oq[t] = qoff[t] + qb;
-      og[t] = q < N ? (q < nt ? gtxt[t] : gimg[t]) + gb : AOOB;
+    for (int t = 0; t < 2; ++t) {
+      const int2 o = slot_off(2 * w + t);
+      const int q = q0 + o.x;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(RQ, ALDS(Qd + (2 * w + t) * 1024), 16, q * (DH * 2) + o.y, 0, 0, 0);
+      const int og = q < N ? __mul24(q + (q < nt ? gofs_t : gofs_i), grow) + hd * DH * 2 + o.y : AOOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(RG, ALDS(Gd + (2 * w + t) * 1024), 16, og, 0, 0, 0);
     }
-    at.load_at(RQ, Qd, oq);
-    at.load_at(RG, Gd, og);
     if (w == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(RL, ALDS(Ld), 4, (q0 + lane) * 4, 0, 0, 0);
     if (w == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(RD, ALDS(Dd), 4, (q0 + lane) * 4, 0, 0, 0);
   };
-  const int ntile = (N + KV2_QT - 1) / KV2_QT;
-  load_tile(Q0, G0, L0, D0, 0);
-  load_tile(Q1, G1, L1, D1, KV2_QT);
 
-  // one query tile: for each 32-row half, S and dP, the softmax terms, then
-  // the dV and dK products of that half (the halves overlap MFMA and VALU work
-  // and keep only one half's scores live); MASK: the ragged last tile
-  auto iter = [&](auto ic, auto mc, int it) {
+  f32x16 dv[4], dk[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
+  const int ntile = ((N + KV5_QT - 1) / KV5_QT + 1) & ~1;
+  load_tile(Q0, G0, L0, D0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  auto iter = [&](auto ic, int it) {
     constexpr int c = decltype(ic)::value;
-    constexpr bool MASK = decltype(mc)::value;
-    char* Qc = c == 0 ? Q0 : (c == 1 ? Q1 : Q2);
-    char* Gc = c == 0 ? G0 : (c == 1 ? G1 : G2);
-    const float* Lc = c == 0 ? L0 : (c == 1 ? L1 : L2);
-    const float* Dc = c == 0 ? D0 : (c == 1 ? D1 : D2);
-    const int q0 = it * KV2_QT;
-    // tile it has landed once at most this wave's loads of tile it+1 fly
-    if (w < 2) attn_barrier<9>(); else attn_barrier<8>();
-    // the stage of tile it+2 was last read in the previous iteration
-    if constexpr (!MASK) {
-      if constexpr (c == 0) load_tile(Q2, G2, L2, D2, q0 + 2 * KV2_QT);
-      else if constexpr (c == 1) load_tile(Q0, G0, L0, D0, q0 + 2 * KV2_QT);
-      else load_tile(Q1, G1, L1, D1, q0 + 2 * KV2_QT);
+    char* Qc = c == 0 ? Q0 : Q1;
+    char* Gc = c == 0 ? G0 : G1;
+    const float* Lc = c == 0 ? L0 : L1;
+    const float* Dc = c == 0 ? D0 : D1;
+    const int q0 = it * KV5_QT;
+    // tile it has landed (only the previous tile's dS^T stores may fly); the
+    // other stage was last read in the previous iteration
+    attn_barrier<DS ? 4 : 0>();
+    if constexpr (c == 0) load_tile(Q1, G1, L1, D1, q0 + KV5_QT);
+    else load_tile(Q0, G0, L0, D0, q0 + KV5_QT);
+    // per-iteration opaque copies of the offsets: the address arithmetic is
+    // redone in each iteration instead of kept in registers across the loop
+    int qo = at.roff0 + th * 8192, ko = at.roff0 + kg * 8192, t1 = at.t10, t2 = at.t20;
+    asm volatile("" : "+v"(qo), "+v"(ko), "+v"(t1), "+v"(t2));
+    auto rowf = [&](const char* S, int o, int kb) {
+      return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + (o ^ (kb << 5))));
+    };
+    auto trf = [&](const char* S, int c, int dt) {
+      const s16x4 lo =
+          __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + (t1 ^ (dt << 6)) + c * 4096));
+      const s16x4 hi =
+          __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + (t2 ^ (dt << 6)) + c * 4096));
+      const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      return __builtin_bit_cast(bf16x8, v);
+    };
+    // S and dP of this wave's keys and query half (lane: key column, query
+    // rows 32 th + 8(e/4) + 4h + e%4)
+    f32x16 st = zero16(), dpt = zero16();
+#pragma unroll
+    for (int kb = 0; kb < 8; ++kb) {
+      st = mfma(rowf(Qc, qo, kb), rowf(KS, ko, kb), st);
+      dpt = mfma(rowf(Gc, qo, kb), rowf(VS, ko, kb), dpt);
     }
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      // all fragments of the half's S and dP first: the reads overlap each
-      // other instead of each MFMA waiting for its own
-      bf16x8 fq[8], fg[8];
+    for (int g = 0; g < 4; ++g) {
+      const float4 L4 = *(const float4*)(Lc + 32 * th + 8 * g + 4 * h);
+      const float4 D4 = *(const float4*)(Dc + 32 * th + 8 * g + 4 * h);
+      const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
 #pragma unroll
-      for (int kb = 0; kb < 8; ++kb) {
-        fq[kb] = at.row(Qc, t, kb);
-        fg[kb] = at.row(Gc, t, kb);
+      for (int i = 0; i < 4; ++i) {
+        const int e = 4 * g + i;
+        const float p = __builtin_amdgcn_exp2f(fmaf(st[e], scl, -Lv[i]));
+        st[e] = p;
+        dpt[e] = p * (dpt[e] - Dv[i]);
       }
-      __builtin_amdgcn_sched_barrier(0);
-      f32x16 st = mfma(fq[0], kf[0], zero16());
-      f32x16 dpt = mfma(fg[0], vf[0], zero16());
+    }
+    // dS^T: queries 16 blk + 4h + 0..3 and 16 blk + 8 + 4h + 0..3 of the half;
+    // columns past the padded width fall outside the resource
+    const unsigned so =
+        q0 < a.ld_ds ? (unsigned)(srow + q0 * KV5_KB * 2 + (32 * th + 4 * h) * 2) : (unsigned)AOOB;
 #pragma unroll
-      for (int kb = 1; kb < 8; ++kb) {
-        st = mfma(fq[kb], kf[kb], st);
-        dpt = mfma(fg[kb], vf[kb], dpt);
+    for (int blk = 0; blk < 2; ++blk) {
+      const bf16x8 pb = pack8(st, blk), db = pack8(dpt, blk);
+      if constexpr (DS) {
+        const u32x4 u = __builtin_bit_cast(u32x4, db);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{u[0], u[1]}, RS, (int)(so + 32 * blk), 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{u[2], u[3]}, RS, (int)(so + 32 * blk + 16), 0, 0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-      // lane: key column, query rows 32t + 8(e/4) + 4h + e%4
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float4 L4 = *(const float4*)(Lc + 32 * t + 8 * g + 4 * h);
-        const float4 D4 = *(const float4*)(Dc + 32 * t + 8 * g + 4 * h);
-        const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = 4 * g + i;
-          float p = __builtin_amdgcn_exp2f(fmaf(st[e], scl, -Lv[i]));
-          if (MASK && q0 + 32 * t + 8 * g + 4 * h + i >= N) p = 0.f;
-          st[e] = p;
-          dpt[e] = p * (dpt[e] - Dv[i]);
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      // dV / dK, 16 query rows at a time: the transposed fragments of one
-      // block are read before its MFMAs, the next block's during them
-      bf16x8 tg[2][4], tq[2][4];
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        tg[0][dt] = at.tr(Gc, 2 * t, dt);
-        tq[0][dt] = at.tr(Qc, 2 * t, dt);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const bf16x8 pb = pack8(st, half), db = pack8(dpt, half);
-        if constexpr (DS) {
-          // dS^T row of this lane's key: queries 16 half + 4h + 0..3 and
-          // 16 half + 8 + 4h + 0..3 of this 32-query half, in the tile's
-          // chunk (64 * 128 elements per query tile of the key block)
-          const u32x4 u = __builtin_bit_cast(u32x4, db);
-          uint16_t* pr = dsr + (size_t)q0 * KV2_KB + 32 * t + 16 * half + 4 * h;
-          *(u32x2*)pr = u32x2{u[0], u[1]};
-          *(u32x2*)(pr + 8) = u32x2{u[2], u[3]};
-        }
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-          dv[dt] = mfma(tg[half][dt], pb, dv[dt]);
-          dk[dt] = mfma(tq[half][dt], db, dk[dt]);
-        }
-        if (half == 0) {  // issued behind the MFMAs that free the registers
-#pragma unroll
-          for (int dt = 0; dt < 4; ++dt) {
-            tg[1][dt] = at.tr(Gc, 2 * t + 1, dt);
-            tq[1][dt] = at.tr(Qc, 2 * t + 1, dt);
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        dv[dt] = mfma(trf(Gc, 2 * th + blk, dt), pb, dv[dt]);
+        dk[dt] = mfma(trf(Qc, 2 * th + blk, dt), db, dk[dt]);
       }
     }
   };
-  using F = std::false_type;
-  using T = std::true_type;
-  const int nfull = N / KV2_QT;
-  int it = 0;
-  for (; it + 2 < nfull; it += 3) {
-    iter(std::integral_constant<int, 0>(), F(), it);
-    iter(std::integral_constant<int, 1>(), F(), it + 1);
-    iter(std::integral_constant<int, 2>(), F(), it + 2);
+  for (int it = 0; it < ntile; it += 2) {
+    iter(std::integral_constant<int, 0>(), it);
+    iter(std::integral_constant<int, 1>(), it + 1);
   }
-  if (it < nfull) iter(std::integral_constant<int, 0>(), F(), it);
-  if (it + 1 < nfull) iter(std::integral_constant<int, 1>(), F(), it + 1);
-  if (nfull < ntile) {  // ragged last tile (no further loads)
-    switch (nfull % 3) {
-      case 0: iter(std::integral_constant<int, 0>(), T(), nfull); break;
-      case 1: iter(std::integral_constant<int, 1>(), T(), nfull); break;
-      default: iter(std::integral_constant<int, 2>(), T(), nfull); break;
-    }
-  }
-  // no direct load may still be landing when the workgroup's LDS is released
+  // the two query halves of a key group: waves 4..7 hand their partial sums
+  // to waves 0..3 through LDS (dV, then dK), which add them in that order
   __builtin_amdgcn_s_waitcnt(0);
-  if (key >= N) return;
+  __syncthreads();
+  float* const xs = (float*)((kg & 2) ? VS : KS) + (kg & 1) * 4096;  // 16 KB per key group
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    f32x16* acc = pass == 0 ? dv : dk;
+    if (th == 1) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *(float4*)(xs + ((dt * 4 + g) * 64 + lane) * 4) =
+              make_float4(acc[dt][4 * g], acc[dt][4 * g + 1], acc[dt][4 * g + 2], acc[dt][4 * g + 3]);
+    }
+    __syncthreads();
+    if (th == 0) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const float4 o = *(const float4*)(xs + ((dt * 4 + g) * 64 + lane) * 4);
+          acc[dt][4 * g] += o.x;
+          acc[dt][4 * g + 1] += o.y;
+          acc[dt][4 * g + 2] += o.z;
+          acc[dt][4 * g + 3] += o.w;
+        }
+    }
+    __syncthreads();
+  }
+  if (th != 0 || key >= N) return;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -1262,8 +1278,8 @@ int attention_bwd_mfma(const AttnBwd& a, hipStream_t s) {
   AttnBwd ak = a;
   if (!ds) ak.dS = nullptr;
   int pi = prof_begin(PROF_ATTN_BWD_KV);
-  if (v2 && ds) launch(attn_bwd_kv2_k<true>, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0u, s, ak);
-  else if (v2) launch(attn_bwd_kv2_k<false>, dim3((a.N + KV2_KB - 1) / KV2_KB, a.B * a.H), dim3(256), 0u, s, ak);
+  if (v2 && ds) launch(attn_bwd_kv5_k<true>, dim3((a.N + KV5_KB - 1) / KV5_KB, a.B * a.H), dim3(512), 0u, s, ak);
+  else if (v2) launch(attn_bwd_kv5_k<false>, dim3((a.N + KV5_KB - 1) / KV5_KB, a.B * a.H), dim3(512), 0u, s, ak);
   else launch(attn_bwd_kv_mfma_k, dim3((a.N + KV_KB - 1) / KV_KB, a.B * a.H), dim3(256), 0u, s, a);
   prof_end(pi, 6.0 * nn);
   JG_CHECK_LAUNCH("attention_bwd_kv_mfma");
