@@ -746,9 +746,9 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const float* Lc = c == 0 ? L0 : L1;
     const float* Dc = c == 0 ? D0 : D1;
     const int q0 = it * KV5_QT;
-    // tile it has landed (only the previous tile's dS^T stores may fly); the
+    // tile it has landed (only the previous tile's 2 dS^T stores may fly); the
     // other stage was last read in the previous iteration
-    attn_barrier<DS ? 4 : 0>();
+    attn_barrier<DS ? 2 : 0>();
     if constexpr (c == 0) load_tile(Q1, G1, L1, D1, q0 + KV5_QT);
     else load_tile(Q0, G0, L0, D0, q0 + KV5_QT);
     // per-iteration opaque copies of the offsets: the address arithmetic is
@@ -787,17 +787,20 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         dpt[e] = p * (dpt[e] - Dv[i]);
       }
     }
-    // dS^T: queries 16 blk + 4h + 0..3 and 16 blk + 8 + 4h + 0..3 of the half;
-    // columns past the padded width fall outside the resource
-    const unsigned so =
-        q0 < a.ld_ds ? (unsigned)(srow + q0 * KV5_KB * 2 + (32 * th + 4 * h) * 2) : (unsigned)AOOB;
+    // dS^T of the half's 16-query block blk: lane (c32, h) holds queries
+    // 4h + 0..3 and 8 + 4h + 0..3; swapping the upper half-wave's first pair of
+    // dwords with the lower half-wave's second pair leaves it queries
+    // 8h + 0..7, one 16-byte store.  Columns past the padded width fall
+    // outside the resource.
+    const unsigned so = q0 < a.ld_ds ? (unsigned)(srow + q0 * KV5_KB * 2 + 64 * th + 16 * h) : (unsigned)AOOB;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       const bf16x8 pb = pack8(st, blk), db = pack8(dpt, blk);
       if constexpr (DS) {
         const u32x4 u = __builtin_bit_cast(u32x4, db);
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{u[0], u[1]}, RS, (int)(so + 32 * blk), 0, 0);
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{u[2], u[3]}, RS, (int)(so + 32 * blk + 16), 0, 0);
+        const auto s0 = __builtin_amdgcn_permlane32_swap(u[0], u[2], false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(u[1], u[3], false, false);
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4{s0[0], s1[0], s0[1], s1[1]}, RS, (int)(so + 32 * blk), 0, 0);
       }
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
