@@ -545,6 +545,10 @@ __device__ __forceinline__ int asw(int r) { return (int)((ASW >> (4 * (r & 15)))
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 #define ALDS(p) ((__attribute__((address_space(3))) void*)(p))
+// byte address of a shared-memory location in the LDS aperture
+__device__ inline unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
 constexpr int AOOB = 0x7ffffff0;  // buffer offset past any resource: loads return zero
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t arsrc(const void* p, long bytes) {
@@ -679,7 +683,10 @@ constexpr int KV5_KB = 128, KV5_QT = 64;
 
 template <bool DS>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_kv5_k(AttnBwd a) {
-  __shared__ __attribute__((aligned(1024))) char KS[32768], VS[32768], Q0[16384], G0[16384], Q1[16384], G1[16384];
+  // K | V of the block, and per stage Q | dO of a query tile: the second
+  // operand of each array sits at a fixed offset from the first, so one
+  // offset register per read pattern serves both
+  __shared__ __attribute__((aligned(1024))) char KV[65536], QG0[32768], QG1[32768];
   __shared__ __attribute__((aligned(256))) float L0[64], D0[64], L1[64], D1[64];
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), h = lane >> 5, c32 = lane & 31;
@@ -712,13 +719,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int s = 4 * w + t;
     const int2 o = slot_off(s);
     const int off = (blockIdx.x * KV5_KB + o.x) * (DH * 2) + o.y;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(RK, ALDS(KS + s * 1024), 16, off, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(RV, ALDS(VS + s * 1024), 16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(RK, ALDS(KV + s * 1024), 16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(RV, ALDS(KV + 32768 + s * 1024), 16, off, 0, 0, 0);
   }
   // query tiles: 16 slots per operand, 2 per wave
   const int gofs_t = b * a.rm.nt, gofs_i = a.rm.B * a.rm.nt + b * a.rm.ni - a.rm.nt;
   const int grow = a.ld_do * 2, nt = a.rm.nt;
-  auto load_tile = [&](char* Qd, char* Gd, float* Ld, float* Dd, int q0) {
+  auto load_tile = [&](char* Qd, float* Ld, float* Dd, int q0) {
+    char* const Gd = Qd + 16384;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int2 o = slot_off(2 * w + t);
@@ -735,56 +743,79 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
   for (int i = 0; i < 4; ++i) { dv[i] = zero16(); dk[i] = zero16(); }
   const int ntile = ((N + KV5_QT - 1) / KV5_QT + 1) & ~1;
-  load_tile(Q0, G0, L0, D0, 0);
+  load_tile(QG0, L0, D0, 0);
   __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  // V is used only for dP; negated once in LDS, the dP products accumulate
+  // onto delta and give delta - dP, so that dS = -P (delta - dP) needs no
+  // subtraction per element (padding rows: delta = 0, dO = 0, so still 0)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    u32x4* vp = (u32x4*)(KV + 32768) + i * 512 + threadIdx.x;
+    u32x4 x = *vp;
+    x ^= 0x80008000u;
+    *vp = x;
+  }
   __syncthreads();
 
   auto iter = [&](auto ic, int it) {
     constexpr int c = decltype(ic)::value;
-    char* Qc = c == 0 ? Q0 : Q1;
-    char* Gc = c == 0 ? G0 : G1;
+    char* Qc = c == 0 ? QG0 : QG1;
     const float* Lc = c == 0 ? L0 : L1;
     const float* Dc = c == 0 ? D0 : D1;
     const int q0 = it * KV5_QT;
     // tile it has landed (only the previous tile's 2 dS^T stores may fly); the
     // other stage was last read in the previous iteration
     attn_barrier<DS ? 2 : 0>();
-    if constexpr (c == 0) load_tile(Q1, G1, L1, D1, q0 + KV5_QT);
-    else load_tile(Q0, G0, L0, D0, q0 + KV5_QT);
-    // per-iteration opaque copies of the offsets: the address arithmetic is
-    // redone in each iteration instead of kept in registers across the loop
-    int qo = at.roff0 + th * 8192, ko = at.roff0 + kg * 8192, t1 = at.t10, t2 = at.t20;
+    if constexpr (c == 0) load_tile(QG1, L1, D1, q0 + KV5_QT);
+    else load_tile(QG0, L0, D0, q0 + KV5_QT);
+    // per-iteration opaque copies of the offsets, as LDS addresses (the
+    // array's base included, so that a read needs no add: the base is a
+    // multiple of 1024 and the XORed bits lie below it); the address
+    // arithmetic is redone in each iteration instead of kept in registers
+    // across the loop
+    const unsigned bq = lds_addr(Qc), bk = lds_addr(KV);
+    unsigned qo = at.roff0 + th * 8192 + bq, ko = at.roff0 + kg * 8192 + bk;
+    unsigned t1 = at.t10 + th * 8192 + bq, t2 = at.t20 + th * 8192 + bq;
     asm volatile("" : "+v"(qo), "+v"(ko), "+v"(t1), "+v"(t2));
-    auto rowf = [&](const char* S, int o, int kb) {
-      return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + (o ^ (kb << 5))));
+    // row fragment of k16 step kb at byte cofs of array S (base b)
+    auto rowf = [&](const char* S, unsigned b, unsigned o, int kb, int cofs) {
+      return __builtin_bit_cast(bf16x8, *(const u32x4*)(S + ((o ^ (kb << 5)) - b) + cofs));
     };
-    auto trf = [&](const char* S, int c, int dt) {
-      const s16x4 lo =
-          __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + (t1 ^ (dt << 6)) + c * 4096));
-      const s16x4 hi =
-          __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(S + (t2 ^ (dt << 6)) + c * 4096));
+    auto trf = [&](int blk, int dt, int cofs) {
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(Qc + ((t1 ^ (dt << 6)) - bq) + blk * 4096 + cofs));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(Qc + ((t2 ^ (dt << 6)) - bq) + blk * 4096 + cofs));
       const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       return __builtin_bit_cast(bf16x8, v);
     };
     // S and dP of this wave's keys and query half (lane: key column, query
     // rows 32 th + 8(e/4) + 4h + e%4)
-    f32x16 st = zero16(), dpt = zero16();
+    f32x16 st = zero16(), dpt;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 D4 = *(const float4*)(Dc + 32 * th + 8 * g + 4 * h);
+      dpt[4 * g] = D4.x;
+      dpt[4 * g + 1] = D4.y;
+      dpt[4 * g + 2] = D4.z;
+      dpt[4 * g + 3] = D4.w;
+    }
 #pragma unroll
     for (int kb = 0; kb < 8; ++kb) {
-      st = mfma(rowf(Qc, qo, kb), rowf(KS, ko, kb), st);
-      dpt = mfma(rowf(Gc, qo, kb), rowf(VS, ko, kb), dpt);
+      st = mfma(rowf(Qc, bq, qo, kb, 0), rowf(KV, bk, ko, kb, 0), st);
+      dpt = mfma(rowf(Qc, bq, qo, kb, 16384), rowf(KV, bk, ko, kb, 32768), dpt);
     }
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const float4 L4 = *(const float4*)(Lc + 32 * th + 8 * g + 4 * h);
-      const float4 D4 = *(const float4*)(Dc + 32 * th + 8 * g + 4 * h);
-      const float Lv[4] = {L4.x, L4.y, L4.z, L4.w}, Dv[4] = {D4.x, D4.y, D4.z, D4.w};
+      const float Lv[4] = {L4.x, L4.y, L4.z, L4.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int e = 4 * g + i;
         const float p = __builtin_amdgcn_exp2f(fmaf(st[e], scl, -Lv[i]));
         st[e] = p;
-        dpt[e] = p * (dpt[e] - Dv[i]);
+        dpt[e] = -p * dpt[e];
       }
     }
     // dS^T of the half's 16-query block blk: lane (c32, h) holds queries
@@ -804,8 +835,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        dv[dt] = mfma(trf(Gc, 2 * th + blk, dt), pb, dv[dt]);
-        dk[dt] = mfma(trf(Qc, 2 * th + blk, dt), db, dk[dt]);
+        dv[dt] = mfma(trf(blk, dt, 16384), pb, dv[dt]);
+        dk[dt] = mfma(trf(blk, dt, 0), db, dk[dt]);
       }
     }
   };
@@ -817,7 +848,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // to waves 0..3 through LDS (dV, then dK), which add them in that order
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  float* const xs = (float*)((kg & 2) ? VS : KS) + (kg & 1) * 4096;  // 16 KB per key group
+  float* const xs = (float*)KV + kg * 4096;  // 16 KB per key group
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
     f32x16* acc = pass == 0 ? dv : dk;
