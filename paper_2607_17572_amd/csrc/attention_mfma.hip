@@ -895,7 +895,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // ------------------------------------------------------------ forward (v2)
 // 128 queries per workgroup (32 per wave, Q^T fragments in registers); key
 // tiles of 64 rows of K and V stream through two LDS stages by direct loads,
-// one barrier per tile.  Two stages (64 KB) and 228 registers let two
+// one barrier per tile.  Two stages (64 KB) and 246 registers let two
 // workgroups share a CU, so that one's softmax work overlaps the other's
 // MFMAs (with three stages and one workgroup per CU the kernel was 1.3x
 // slower).  S^T = K Q^T from row fragments of the K tile;
@@ -903,6 +903,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // order of the accumulator-fed P^T.  Rows of K and V past N load as zeros; the
 // keys past N are masked in the ragged last tile only.
 constexpr int F2_QB = 128, F2_KT = 64;
+constexpr float F2_SLACK = 8.f;
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd2_k(AttnFwd a) {
   __shared__ __attribute__((aligned(1024))) char K0[16384], V0[16384], K1[16384], V1[16384];
@@ -967,34 +968,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
       for (int kb = 1; kb < 8; ++kb) st[t] = mfma(fk[kb], qf[kb], st[t]);
     }
+    // row maximum of the raw scores (the scale is positive)
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        float sv = st[t][e] * sc;
-        if (MASK && k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3) >= N) sv = -INFINITY;
-        st[t][e] = sv;
-        mx = fmaxf(mx, sv);
+        if (MASK && k0 + 32 * t + 8 * (e >> 2) + 4 * h + (e & 3) >= N) st[t][e] = -INFINITY;
+        mx = fmaxf(mx, st[t][e]);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mn = fmaxf(m, mx);
-    const float corr = __builtin_amdgcn_exp2f(m - mn);
-    float ls = 0.f;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sc;
+    // The reference point m moves only when a row's maximum passes it by more
+    // than F2_SLACK (log2 units): P = 2^(s - m) then stays below 2^F2_SLACK,
+    // and the rescale of O and l is skipped on the tiles where no row of the
+    // wave moves (after the first tiles, nearly all of them).
+    if (__builtin_amdgcn_ballot_w64(mx > m + F2_SLACK)) {
+      const float mn = fmaxf(m, mx);
+      const float corr = __builtin_amdgcn_exp2f(m - mn);
+      l *= corr;
+      m = mn;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[i][e] *= corr;
+    }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float p = __builtin_amdgcn_exp2f(st[t][e] - mn);
+        const float p = __builtin_amdgcn_exp2f(fmaf(st[t][e], sc, -m));
         st[t][e] = p;
-        ls += p;
+        l += p;
       }
-    l = l * corr + ls;
-    m = mn;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[i][e] *= corr;
     // O^T += V^T P^T, 16 keys (tile rows 16 cb ..) per step
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
