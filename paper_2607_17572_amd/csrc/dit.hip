@@ -287,7 +287,9 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   W.delta = a.f32(2 * hn);  // delta, then the log-sum-exp in log2 units
   if (m.act == BF16 && m.Dh == 128)
     W.dS = a.take((size_t)B * m.H * attn_ds_rows(m.N) * attn_ds_ld(m.N) * 2);
-  W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, QK_PARTS * 2 * m.Dh + m.D, m.pd});
+  // per 32-row chunk: the widest partials of one launch, or the q/k gain
+  // partials followed by the LayerNorm partials (RED_ROWS / LN_ROWS blocks)
+  W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, QK_PARTS * 2 * m.Dh + RED_ROWS / LN_ROWS * m.D, m.pd});
   const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   W.p1 = a.f32((size_t)nch * W.maxcols);
   W.p2 = a.f32((size_t)nch * W.maxcols);
@@ -623,8 +625,8 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
-      j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D);
-      j[2 * s + 1] = per_sample_job(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D);
+      j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D, LN_ROWS);
+      j[2 * s + 1] = per_sample_job(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D, LN_ROWS);
     }
     TRY(reduce_jobs(j, 4, S));
   }
@@ -668,8 +670,8 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
-      j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D);
-      j[2 * s + 1] = per_sample_job(p2s, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0);
+      j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D, LN_ROWS);
+      j[2 * s + 1] = per_sample_job(p2s, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0, LN_ROWS);
     }
     TRY(reduce_jobs(j, 4, S));
   }
@@ -721,8 +723,8 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   TRY(dgrad(cx, W.dbig, LD, R, cx.P(L.in.w), D, LD, D, W.dA, D, F32));
   TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m, A.r, A.mod, A.mod, 3 * D, D, W.g, W.p1, W.p2, cx.s));
   {
-    const RedJob j[2] = {per_sample_job(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, D),
-                         per_sample_job(W.p2, D, rm, 0, R, W.dmod[0], 3 * D, 0)};
+    const RedJob j[2] = {per_sample_job(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, D, LN_ROWS),
+                         per_sample_job(W.p2, D, rm, 0, R, W.dmod[0], 3 * D, 0, LN_ROWS)};
     TRY(reduce_jobs(j, 2, cx.s));
   }
   TRY(small_linear_bwd(W.dmod[0], mvec, 0, B, D, cx.P(L.mod.w), m.act, 3 * D, G(dth, m, L.mod.w), G(dth, m, L.mod.b),
@@ -789,8 +791,8 @@ static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const
     void* xl = m.sgl.empty() ? (m.dbl.empty() ? gl.x0 : S.d.back().x_out) : S.s.back().x_out;
     TRY(ln_mod_bwd(W.dfa, xl, act, D, rm, rt, R - rt, gl.fm, gl.fr, gl.fmod, gl.fmod, 2 * D, D, W.g, W.p1, W.p2,
                    cx.s));
-    TRY(reduce_per_sample(W.p1, D, rm, rt, R - rt, W.dmod[0], 2 * D, D, cx.s));
-    TRY(reduce_per_sample(W.p2, D, rm, rt, R - rt, W.dmod[0], 2 * D, 0, cx.s));
+    TRY(reduce_per_sample(W.p1, D, rm, rt, R - rt, W.dmod[0], 2 * D, D, cx.s, LN_ROWS));
+    TRY(reduce_per_sample(W.p2, D, rm, rt, R - rt, W.dmod[0], 2 * D, 0, cx.s, LN_ROWS));
     TRY(small_linear_bwd(W.dmod[0], gl.mvec, 0, B, D, cx.P(m.fmod.w), act, 2 * D, G(dth, m, m.fmod.w),
                          G(dth, m, m.fmod.b), m.grad, beta, W.tmp, W.slpart, cx.s));
     TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, cx.s));

@@ -24,6 +24,10 @@ struct Chunks {
 };
 
 constexpr int RED_ROWS = 32;  // rows per reduction chunk
+// rows per block of the LayerNorm/adaLN backward, whose partial sums are per
+// block: the pair's 9216 rows make 1152 blocks, which the CUs take up as they
+// free (whole 32-row chunks left 32 of 256 CUs with two blocks, the rest with one)
+constexpr int LN_ROWS = 8;
 
 // ---- small-M linear layers (time MLP, adaLN modulation): M = batch <= 64 ----
 // out[b][j] = sum_d act(in[b][d]) W[j][d] + bias[j];  act: 0 identity, 1 SiLU.
@@ -51,8 +55,8 @@ int mul_silu_grad(float* y, const float* x, size_t n, hipStream_t s);
 int ln_mod_fwd(const void* x, int act_dt, int D, RowMap rm, int row0, int nrows, const float* mod_txt,
                const float* mod_img, int mod_w, int sh_off, int sc_off, void* a, float* mean, float* rstd,
                hipStream_t s);
-// g[r] += LN_bwd(dA * (1 + scale)) and per-chunk partials of
-// sum dA*xhat (-> part_scale) and sum dA (-> part_shift), [chunk][D].
+// g[r] += LN_bwd(dA * (1 + scale)) and partials of sum dA*xhat (-> part_scale)
+// and sum dA (-> part_shift) per chunk of LN_ROWS rows, [chunk][D].
 int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int row0, int nrows,
                const float* mean, const float* rstd, const float* mod_txt, const float* mod_img, int mod_w,
                int sc_off, float* g, float* part_scale, float* part_shift, hipStream_t s);
@@ -91,12 +95,13 @@ int colsum_partials(const void* X, int dt, int ld, int N, RowMap rm, int row0, i
                     hipStream_t s);
 // Per-sample reduction: out[b*out_stride + out_off + c] = sum over chunks of sample b (of the
 // chunks belonging to rows [row0, row0+nrows)) of part[chunk][c].  Overwrites.
+// R: rows per chunk of the partials.
 int reduce_per_sample(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
-                      int out_off, hipStream_t s);
+                      int out_off, hipStream_t s, int R = RED_ROWS);
 // Whole reduction into a parameter gradient: g[c] = beta*g[c] + sum_chunks part[chunk*ld + c].
 int reduce_to_grad(const float* part, int ld, int chunk0, int nchunk, int N, void* g, int g_dt,
                    float beta, hipStream_t s);
-int chunk_range(RowMap rm, int row0, int nrows, int* c0, int* nc);
+int chunk_range(RowMap rm, int row0, int nrows, int* c0, int* nc, int R = RED_ROWS);
 
 // A list of independent chunk reductions run as one launch, each job with the
 // arithmetic (and so the bits) of reduce_per_sample or reduce_to_grad.
@@ -115,7 +120,7 @@ struct RedJob {
 };
 constexpr int RED_MAX_JOBS = 8;
 RedJob per_sample_job(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
-                      int out_off);
+                      int out_off, int R = RED_ROWS);
 RedJob to_grad_job(const float* part, int ld, int chunk0, int nchunk, int N, void* g, int g_dt, float beta);
 // Runs jobs[0..n) (n <= RED_MAX_JOBS) in one launch; 1 on an invalid job.
 int reduce_jobs(const RedJob* jobs, int n, hipStream_t s);

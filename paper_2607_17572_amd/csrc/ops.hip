@@ -33,8 +33,8 @@ __device__ inline void chunk_rows(const Chunks& c, int q, int& r0, int& n, int& 
   }
 }
 
-int chunk_range(RowMap rm, int row0, int nrows, int* c0, int* nc) {
-  Chunks c{rm.B, rm.nt, rm.ni, RED_ROWS};
+int chunk_range(RowMap rm, int row0, int nrows, int* c0, int* nc, int R) {
+  Chunks c{rm.B, rm.nt, rm.ni, R};
   const int bt = rm.rows_txt();
   if (row0 == 0 && nrows == rm.rows()) { *c0 = 0; *nc = c.count(); return 0; }
   if (row0 == 0 && nrows == bt) { *c0 = 0; *nc = rm.B * c.ct(); return 0; }
@@ -602,9 +602,9 @@ __global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA
 // each lane owning NV runs of 8 consecutive columns (16-byte loads).  The
 // per-sample factors 1 + scale sit in LDS, x stays in its storage type and the
 // shift-gradient column sums accumulate in the wave's own LDS row, so a wave
-// keeps under 256 VGPRs: two blocks share a CU, and all chunks of a double
-// block's pair (288 of 32 rows) run in one round on 256 CUs.  The per-column
-// partial sums of the waves are combined through LDS in wave order.
+// keeps under 256 VGPRs and two blocks share a CU.  A block takes LN_ROWS
+// rows, so the many blocks spread evenly over the CUs.  The per-column partial
+// sums of the waves are combined through LDS in wave order.
 constexpr int LN_W = 4;
 template <typename T, int NV>
 __global__ __launch_bounds__(64 * LN_W) __attribute__((amdgpu_waves_per_eu(2, 2))) void ln_mod_bwd_vec_k(
@@ -703,9 +703,9 @@ int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int
                int sc_off, float* g, float* part_scale, float* part_shift, hipStream_t s) {
   if (D > 256 * MAXC) { set_error("ln_mod_bwd: hidden too large"); return 1; }
   int c0, nc;
-  if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
+  if (chunk_range(rm, row0, nrows, &c0, &nc, LN_ROWS)) return 1;
   if (nc == 0) return 0;
-  Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  Chunks ch{rm.B, rm.nt, rm.ni, LN_ROWS};
   if (D % 512 == 0 && D <= 3584 && al16(dA) && al16(x) && al16(g)) {
     const size_t lds = (LN_W + 1) * (size_t)D * sizeof(float);
 #define LNB(T, NV)                                                                                             \
@@ -1266,10 +1266,10 @@ __global__ __launch_bounds__(1024) void reduce_per_sample_k(const float* __restr
 }
 
 int reduce_per_sample(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
-                      int out_off, hipStream_t s) {
+                      int out_off, hipStream_t s, int R) {
   int c0, nc;
-  if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
-  Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (chunk_range(rm, row0, nrows, &c0, &nc, R)) return 1;
+  Chunks ch{rm.B, rm.nt, rm.ni, R};
   hipLaunchKernelGGL(reduce_per_sample_k, dim3((N + RC_COLS - 1) / RC_COLS, rm.B), dim3(RC_COLS * RC_SL), 0, s, part,
                      N, ch, c0, nc, out, out_stride, out_off);
   LAUNCH_OK("reduce_per_sample");
@@ -1316,13 +1316,13 @@ struct RedJobs {
 };
 
 RedJob per_sample_job(const float* part, int N, RowMap rm, int row0, int nrows, float* out, int out_stride,
-                      int out_off) {
+                      int out_off, int R) {
   RedJob r;
   r.part = part;
   r.ld = r.N = N;
   r.kind = 0;
-  r.ch = Chunks{rm.B, rm.nt, rm.ni, RED_ROWS};
-  if (chunk_range(rm, row0, nrows, &r.c0, &r.nc)) r.N = -1;  // rejected by reduce_jobs
+  r.ch = Chunks{rm.B, rm.nt, rm.ni, R};
+  if (chunk_range(rm, row0, nrows, &r.c0, &r.nc, R)) r.N = -1;  // rejected by reduce_jobs
   r.out = out;
   r.out_stride = out_stride;
   r.out_off = out_off;
