@@ -17,14 +17,9 @@ __device__ __host__ inline float bf2f(uint16_t v) {
   c.u = (uint32_t)v << 16;
   return c.f;
 }
-__device__ __host__ inline uint16_t f2bf(float f) {
-  union { uint32_t u; float f; } c;
-  c.f = f;
-  uint32_t u = c.u;
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x7fffffu)) return (uint16_t)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+// fp32 -> bf16, round to nearest even: the hardware conversion
+// (v_cvt_pk_bf16_f32), branch-free; pairs of calls fuse into one instruction
+__device__ inline uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
