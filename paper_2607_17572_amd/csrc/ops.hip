@@ -1140,6 +1140,119 @@ __global__ __launch_bounds__(256) void qk_norm_rope_bwd_k(const TD* __restrict__
   }
 }
 
+// The same backward for bf16 operands and head_dim 128 with 16-byte accesses:
+// per step a wave takes four heads of its row, 16 lanes per head, each lane
+// 4 RoPE pairs (8 consecutive elements).  The rotation of pair p is computed
+// once per row by lane p and handed to the lanes that use it; the per-head
+// sums run over the 16 lanes of the head.
+__global__ __launch_bounds__(256) void qk_norm_rope_bwd8_k(const uint16_t* __restrict__ dQh,
+                                                           const uint16_t* __restrict__ dKh,
+                                                           const uint16_t* __restrict__ dVh,
+                                                           const uint16_t* __restrict__ proj, int ld, RowMap rm,
+                                                           Rope rp, Chunks ch, int c0, Gains gn,
+                                                           const float* __restrict__ rq, const float* __restrict__ rk,
+                                                           uint16_t* __restrict__ dproj, int ld_d,
+                                                           float* __restrict__ pgain) {
+  constexpr int Dh = 128;
+  __shared__ float red[4][4][2 * Dh];  // [wave][head slot][q gains | k gains]
+  const int q = c0 + blockIdx.x;
+  int r0, n, b;
+  chunk_rows(ch, q, r0, n, b);
+  const int st = r0 < ch.B * ch.nt ? 0 : 1;
+  const int sub = (int)blockIdx.y;  // signed: an empty sub-chunk must get n <= 0
+  r0 += sub * QK_SUB;
+  n = min(QK_SUB, n - sub * QK_SUB);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int hq = lane >> 4, lp = lane & 15, e0 = 8 * lp;
+  const int H = rp.H, D = H * Dh, N = rm.nt + rm.ni;
+  float qg[8], kg[8], gq[8], gk[8];
+  ld8f((const uint16_t*)gn.q[st] + e0, qg);
+  ld8f((const uint16_t*)gn.k[st] + e0, kg);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) gq[e] = gk[e] = 0.f;
+  constexpr float inv_dh = 1.f / Dh;
+  for (int rr = wave; rr < n; rr += 4) {
+    const int r = r0 + rr;
+    int bb, j;
+    tok_of_row(rm, r, bb, j);
+    float sn0, cs0;
+    sincosf(rope_angle(rp, j, lane), &sn0, &cs0);
+    float cs[4], sn[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      cs[k] = __shfl(cs0, 4 * lp + k, 64);
+      sn[k] = __shfl(sn0, 4 * lp + k, 64);
+    }
+    const uint16_t* pr = proj + (size_t)r * ld + e0;
+    uint16_t* dp = dproj + (size_t)r * ld_d + e0;
+    const size_t ob = ((size_t)bb * H * N + j) * Dh + e0;  // head h adds h * N * Dh
+    for (int h0 = 0; h0 < H; h0 += 4) {
+      const int h = h0 + hq;
+      const bool hv = h < H;
+      const int hh = hv ? h : 0;  // lanes past the last head compute on head 0, store nothing
+      const size_t o = ob + (size_t)hh * N * Dh;
+      float qa[8], ka[8], x[8], y[8];
+      ld8f(dQh + o, qa);
+      ld8f(dKh + o, ka);
+      ld8f(pr + hh * Dh, x);
+      ld8f(pr + D + hh * Dh, y);
+      const uint4 vv = *(const uint4*)(dVh + o);
+      const float riq = rq[(size_t)r * H + hh], rik = rk[(size_t)r * H + hh];
+      // undo the rotation
+      float dq[8], dk[8];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        dq[2 * k] = qa[2 * k] * cs[k] + qa[2 * k + 1] * sn[k];
+        dq[2 * k + 1] = -qa[2 * k] * sn[k] + qa[2 * k + 1] * cs[k];
+        dk[2 * k] = ka[2 * k] * cs[k] + ka[2 * k + 1] * sn[k];
+        dk[2 * k + 1] = -ka[2 * k] * sn[k] + ka[2 * k + 1] * cs[k];
+      }
+      float sq = 0.f, sk = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        sq = fmaf(dq[e] * qg[e], x[e], sq);
+        sk = fmaf(dk[e] * kg[e], y[e], sk);
+      }
+#pragma unroll
+      for (int m = 8; m > 0; m >>= 1) {
+        sq += __shfl_xor(sq, m, 16);
+        sk += __shfl_xor(sk, m, 16);
+      }
+      const float cq = riq * riq * riq * sq * inv_dh, ck = rik * rik * rik * sk * inv_dh;
+      float oq[8], ok[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        oq[e] = dq[e] * qg[e] * riq - x[e] * cq;
+        ok[e] = dk[e] * kg[e] * rik - y[e] * ck;
+      }
+      if (hv) {
+        st8f(dp + h * Dh, oq);
+        st8f(dp + D + h * Dh, ok);
+        *(uint4*)(dp + 2 * D + h * Dh) = vv;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          gq[e] = fmaf(dq[e], x[e] * riq, gq[e]);
+          gk[e] = fmaf(dk[e], y[e] * rik, gk[e]);
+        }
+      }
+    }
+  }
+  // gain partials: the 16 head slots of the block (4 waves x 4) added in order
+  float* const rw = &red[wave][hq][0];
+  *(float4*)(rw + e0) = make_float4(gq[0], gq[1], gq[2], gq[3]);
+  *(float4*)(rw + e0 + 4) = make_float4(gq[4], gq[5], gq[6], gq[7]);
+  *(float4*)(rw + Dh + e0) = make_float4(gk[0], gk[1], gk[2], gk[3]);
+  *(float4*)(rw + Dh + e0 + 4) = make_float4(gk[4], gk[5], gk[6], gk[7]);
+  __syncthreads();
+  const int c = threadIdx.x;  // 256 threads = 2 Dh gain columns
+  float a = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) a += red[w][k][c];
+  pgain[((size_t)q * QK_PARTS + sub) * 2 * Dh + c] = a;
+}
+
 int qk_norm_rope_bwd(const void* dQh, const void* dKh, const void* dVh, int dt_d, const void* proj, int ld,
                      int act_dt, RowMap rm, Rope rp, Gains gn, const float* rinv_q,
                      const float* rinv_k, void* dproj, int ld_d, float* part_gain, hipStream_t s) {
@@ -1154,6 +1267,14 @@ int qk_norm_rope_bwd(const void* dQh, const void* dKh, const void* dVh, int dt_d
   int c0, nc;
   if (chunk_range(rm, 0, rm.rows(), &c0, &nc)) return 1;
   Chunks ch{rm.B, rm.nt, rm.ni, RED_ROWS};
+  if (act_dt == BF16 && dt_d == BF16 && rp.Dh == 128 && !((ld | ld_d) & 7) && al16(dQh) && al16(dKh) && al16(dVh) &&
+      al16(proj) && al16(dproj) && al16(gn.q[0]) && al16(gn.q[1]) && al16(gn.k[0]) && al16(gn.k[1])) {
+    hipLaunchKernelGGL(qk_norm_rope_bwd8_k, dim3(nc, QK_PARTS), dim3(256), 0, s, (const uint16_t*)dQh,
+                       (const uint16_t*)dKh, (const uint16_t*)dVh, (const uint16_t*)proj, ld, rm, rp, ch, c0, gn,
+                       rinv_q, rinv_k, (uint16_t*)dproj, ld_d, part_gain);
+    LAUNCH_OK("qk_norm_rope_bwd8");
+    return 0;
+  }
 #define QKB(T, TD)                                                                                            \
   hipLaunchKernelGGL((qk_norm_rope_bwd_k<T, TD>), dim3(nc, QK_PARTS), dim3(256), 0, s, (const TD*)dQh, (const TD*)dKh,     \
                      (const TD*)dVh, (const T*)proj, ld, rm, rp, ch, c0, gn, rinv_q, rinv_k, \
