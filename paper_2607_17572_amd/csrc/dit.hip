@@ -245,6 +245,7 @@ struct Ws {
   float* delta = nullptr;
   void* dS = nullptr;  // dS^T of the attention backward (bf16 MFMA path)
   float *p1 = nullptr, *p2 = nullptr;
+  float* pr = nullptr;  // double block: partials of the reductions on the weight-gradient stream
   float* dmod[2] = {nullptr, nullptr};
   float *dmvec = nullptr, *dvec = nullptr, *dsh1 = nullptr, *tmp = nullptr;
   float* slpart = nullptr;
@@ -259,6 +260,16 @@ struct Ws {
 
 static size_t out_elems(const Model& m) {  // per sample
   return m.c.block_only ? (size_t)m.N * m.D : (size_t)m.C * m.c.lat_h * m.c.lat_w;
+}
+
+// Partials of the double block's reductions that run on the weight-gradient
+// stream, one region per producer (none is reused within the block):
+// MLP gate (2 x [nch][D]), fc1 bias ([nch][F]), second LayerNorm (2 x [nlb][D]),
+// attention gate (2 x [nch][D]), q/k gains ([nch * QK_PARTS][2 Dh]), qkv bias
+// ([nch][3D]); nch chunks of RED_ROWS rows, nlb of LN_ROWS rows.
+static size_t dbl_side_part_floats(const Model& m, int B) {
+  const size_t nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count(), nlb = Chunks{B, m.nt, m.ni, LN_ROWS}.count();
+  return nch * (4 * (size_t)m.D + m.F + QK_PARTS * 2 * (size_t)m.Dh + 3 * (size_t)m.D) + 2 * nlb * m.D;
 }
 
 static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
@@ -293,6 +304,7 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   W.p1 = a.f32((size_t)nch * W.maxcols);
   W.p2 = a.f32((size_t)nch * W.maxcols);
+  if (m.c.n_double) W.pr = a.f32(dbl_side_part_floats(m, B));
   W.dmod[0] = a.f32((size_t)B * 6 * m.D);
   W.dmod[1] = a.f32((size_t)B * 6 * m.D);
   W.dmvec = a.f32((size_t)B * m.D);
@@ -326,7 +338,7 @@ struct jagg_ctx {
   // second stream for the weight-gradient products of the backward, created on
   // first use (default priority), with its fork and join events
   hipStream_t side = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr, mark = nullptr;
 };
 
 namespace jg {
@@ -340,7 +352,7 @@ struct Ctx {
   // weight-gradient stream of the backward (nullptr: everything on s) and
   // its fork / join events
   hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_mark = nullptr;
   const void* P(size_t off) const { return th + off * es; }
   // the stream the next weight-gradient product goes to: the side stream,
   // after everything issued on s so far
@@ -348,6 +360,24 @@ struct Ctx {
     if (!side) return s;
     if (hipEventRecord(ev_fork, s) != hipSuccess || hipStreamWaitEvent(side, ev_fork, 0) != hipSuccess) return s;
     return side;
+  }
+  // mark(): an event after the work issued on the side stream so far;
+  // wait_mark(): s waits for that work only (not for what was issued later)
+  int mark() const {
+    if (!side) return 0;
+    if (hipEventRecord(ev_mark, side) != hipSuccess) {
+      set_error("backward: marking the weight-gradient stream failed");
+      return 3;
+    }
+    return 0;
+  }
+  int wait_mark() const {
+    if (!side) return 0;
+    if (hipStreamWaitEvent(s, ev_mark, 0) != hipSuccess) {
+      set_error("backward: waiting for the weight-gradient stream failed");
+      return 3;
+    }
+    return 0;
   }
   // s waits for every weight-gradient product issued so far
   int join() const {
@@ -582,6 +612,19 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   int c0[2], nc[2];
   for (int s = 0; s < 2; ++s) TRY(chunk_range(rm, r0[s], nr[s], &c0[s], &nc[s]));
   const hipStream_t S = cx.s;
+  // regions of the reductions that go to the weight-gradient stream (their
+  // results are needed only at the block's end): MLP gate, fc1 bias, second
+  // LayerNorm, attention gate, q/k gains, qkv bias
+  const size_t nch = nchunk, nlb = Chunks{B, m.nt, m.ni, LN_ROWS}.count();
+  float* const g2a = W.pr;
+  float* const g2b = g2a + nch * D;
+  float* const cf1 = g2b + nch * D;
+  float* const l2a = cf1 + nch * F;
+  float* const l2b = l2a + nlb * D;
+  float* const g1a = l2b + nlb * D;
+  float* const g1b = g1a + nch * D;
+  float* const qkg = g1b + nch * D;
+  float* const cqkv = qkg + nch * QK_PARTS * 2 * m.Dh;
   auto wg2 = [&](void* dY, int ld_dy, void* X, int ldx, int Nout, int Kin, size_t w0, size_t w1) {
     const GemmArgs a = wgrad_args(cx, row(dY, r0[0], ld_dy), ld_dy, act, row(X, r0[0], ldx), ldx, nr[0], Nout, Kin,
                                   G(dth, m, w0), beta);
@@ -602,45 +645,47 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
     return gemm2(a, b, S);
   };
   // MLP branch: x_out = xm + gate2 * y2
-  TRY(gate_bwd(W.g, A.y2, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, W.p1, W.p2, S));
+  TRY(gate_bwd(W.g, A.y2, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, g2a, g2b, S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
-      j[s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 5 * D);
-      j[2 + s] = to_grad_job(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].fc2.b), m.grad, beta);
+      j[s] = per_sample_job(g2a, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 5 * D);
+      j[2 + s] = to_grad_job(g2b, D, c0[s], nc[s], D, G(dth, m, st[s].fc2.b), m.grad, beta);
     }
-    TRY(reduce_jobs(j, 4, S));
+    TRY(reduce_jobs(j, 4, cx.fork()));
   }
   TRY(wg2(W.dY, D, A.h, F, D, F, st[0].fc2.w, st[1].fc2.w));
   TRY(dg2(W.dY, D, st[0].fc2.w, st[1].fc2.w, F, D, F, W.dbig, F, act, EPI_GELU_BWD, A.pre, F));
-  TRY(colsum_partials(W.dbig, act, F, F, rm, 0, R, W.p1, S));
+  TRY(colsum_partials(W.dbig, act, F, F, rm, 0, R, cf1, S));
   {
     RedJob j[2];
-    for (int s = 0; s < 2; ++s) j[s] = to_grad_job(W.p1, F, c0[s], nc[s], F, G(dth, m, st[s].fc1.b), m.grad, beta);
-    TRY(reduce_jobs(j, 2, S));
+    for (int s = 0; s < 2; ++s) j[s] = to_grad_job(cf1, F, c0[s], nc[s], F, G(dth, m, st[s].fc1.b), m.grad, beta);
+    TRY(reduce_jobs(j, 2, cx.fork()));
   }
   TRY(wg2(W.dbig, F, A.a2, D, F, D, st[0].fc1.w, st[1].fc1.w));
   TRY(dg2(W.dbig, F, st[0].fc1.w, st[1].fc1.w, D, F, D, W.dA, D, F32));
-  TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, 0, R, A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, W.g, W.p1, W.p2, S));
+  TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, 0, R, A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, W.g, l2a, l2b, S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
-      j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D, LN_ROWS);
-      j[2 * s + 1] = per_sample_job(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D, LN_ROWS);
+      j[2 * s] = per_sample_job(l2a, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 4 * D, LN_ROWS);
+      j[2 * s + 1] = per_sample_job(l2b, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 3 * D, LN_ROWS);
     }
-    TRY(reduce_jobs(j, 4, S));
+    TRY(reduce_jobs(j, 4, cx.fork()));
   }
   // attention branch: xm = x + gate1 * y1 (W.dY and W.dbig are rewritten
   // from here on: the fc2 and fc1 weight gradients that read them are done)
   TRY(cx.join());
-  TRY(gate_bwd(W.g, A.y1, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, W.p1, W.p2, S));
+  TRY(gate_bwd(W.g, A.y1, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, g1a, g1b, S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
-      j[s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 2 * D);
-      j[2 + s] = to_grad_job(W.p2, D, c0[s], nc[s], D, G(dth, m, st[s].o.b), m.grad, beta);
+      j[s] = per_sample_job(g1a, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 2 * D);
+      j[2 + s] = to_grad_job(g1b, D, c0[s], nc[s], D, G(dth, m, st[s].o.b), m.grad, beta);
     }
-    TRY(reduce_jobs(j, 4, S));
+    TRY(reduce_jobs(j, 4, cx.fork()));
+    // the last modulation sums on that stream: the block's end waits for them
+    TRY(cx.mark());
   }
   TRY(wg2(W.dY, D, A.O, D, D, D, st[0].o.w, st[1].o.w));
   TRY(dg2(W.dY, D, st[0].o.w, st[1].o.w, D, D, D, W.dO, D, act));
@@ -649,32 +694,33 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   TRY(attention_bwd(ab, S));
   Gains gn{{cx.P(st[0].qg), cx.P(st[1].qg)}, {cx.P(st[0].kg), cx.P(st[1].kg)}};
   TRY(qk_norm_rope_bwd(W.dQh, W.dKh, W.dVh, act, A.qkv, 3 * D, act, rm, Rope{m.H, m.Dh, m.nt, m.ni, m.gw}, gn, A.rq,
-                       A.rk, W.dbig, 3 * D, W.p2, S));
-  // the gain partials (W.p2) wait for the qkv bias partials (W.p1): one launch
-  TRY(colsum_partials(W.dbig, act, 3 * D, 3 * D, rm, 0, R, W.p1, S));
+                       A.rk, W.dbig, 3 * D, qkg, S));
+  // the gain partials wait for the qkv bias partials: one launch
+  TRY(colsum_partials(W.dbig, act, 3 * D, 3 * D, rm, 0, R, cqkv, S));
   {
     RedJob j[6];
     for (int s = 0; s < 2; ++s) {
-      j[3 * s] = to_grad_job(W.p2, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh, G(dth, m, st[s].qg), m.grad,
+      j[3 * s] = to_grad_job(qkg, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh, G(dth, m, st[s].qg), m.grad,
                              beta);
-      j[3 * s + 1] = to_grad_job(W.p2 + m.Dh, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh,
+      j[3 * s + 1] = to_grad_job(qkg + m.Dh, 2 * m.Dh, c0[s] * QK_PARTS, nc[s] * QK_PARTS, m.Dh,
                                  G(dth, m, st[s].kg), m.grad, beta);
-      j[3 * s + 2] = to_grad_job(W.p1, 3 * D, c0[s], nc[s], 3 * D, G(dth, m, st[s].qkv.b), m.grad, beta);
+      j[3 * s + 2] = to_grad_job(cqkv, 3 * D, c0[s], nc[s], 3 * D, G(dth, m, st[s].qkv.b), m.grad, beta);
     }
-    TRY(reduce_jobs(j, 6, S));
+    TRY(reduce_jobs(j, 6, cx.fork()));
   }
   TRY(wg2(W.dbig, 3 * D, A.a1, D, 3 * D, D, st[0].qkv.w, st[1].qkv.w));
   TRY(dg2(W.dbig, 3 * D, st[0].qkv.w, st[1].qkv.w, D, 3 * D, D, W.dA, D, F32));
-  float* const p2s = W.p2 + (size_t)nchunk * QK_PARTS * 2 * m.Dh;
-  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, W.p1, p2s, S));
+  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, W.p1, W.p2, S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
       j[2 * s] = per_sample_job(W.p1, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, D, LN_ROWS);
-      j[2 * s + 1] = per_sample_job(p2s, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0, LN_ROWS);
+      j[2 * s + 1] = per_sample_job(W.p2, D, rm, r0[s], nr[s], W.dmod[s], 6 * D, 0, LN_ROWS);
     }
     TRY(reduce_jobs(j, 4, S));
   }
+  // the modulation sums of the two gates and the second LayerNorm
+  TRY(cx.wait_mark());
   // adaLN modulation: mod = SiLU(vec) W_mod^T + b, per stream; d SiLU(vec) in the order text, image
   for (int s = 0; s < 2; ++s) {
     TRY(small_linear_bwd(W.dmod[s], mvec, 0, B, D, cx.P(st[s].mod.w), m.act, 6 * D, G(dth, m, st[s].mod.w),
@@ -738,15 +784,18 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
 static bool side_stream(jagg_ctx* ctx) {
   if (ctx->side) return true;
   hipStream_t st = nullptr;
-  hipEvent_t f = nullptr, j = nullptr;
+  hipEvent_t f = nullptr, j = nullptr, k = nullptr;
   if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) == hipSuccess &&
       hipEventCreateWithFlags(&f, hipEventDisableTiming) == hipSuccess &&
-      hipEventCreateWithFlags(&j, hipEventDisableTiming) == hipSuccess) {
+      hipEventCreateWithFlags(&j, hipEventDisableTiming) == hipSuccess &&
+      hipEventCreateWithFlags(&k, hipEventDisableTiming) == hipSuccess) {
     ctx->side = st;
     ctx->fork = f;
     ctx->join = j;
+    ctx->mark = k;
     return true;
   }
+  if (k) (void)hipEventDestroy(k);
   if (j) (void)hipEventDestroy(j);
   if (f) (void)hipEventDestroy(f);
   if (st) (void)hipStreamDestroy(st);
@@ -763,6 +812,7 @@ static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const
     cx.side = ctx->side;
     cx.ev_fork = ctx->fork;
     cx.ev_join = ctx->join;
+    cx.ev_mark = ctx->mark;
   }
   const int act = m.act, D = m.D;
   const size_t es = dsize(act);
@@ -941,6 +991,7 @@ void jagg_ctx_destroy(jagg_ctx* ctx) {
     (void)hipStreamSynchronize(ctx->side);
     (void)hipEventDestroy(ctx->fork);
     (void)hipEventDestroy(ctx->join);
+    (void)hipEventDestroy(ctx->mark);
     (void)hipStreamDestroy(ctx->side);
   }
   delete ctx;
