@@ -598,7 +598,11 @@ static GemmArgs dgrad_args(const Ctx& cx, const void* dY, int ld_dy, int rows, c
 // kernel in one launch (the modulation vectors are picked per row), and the
 // two streams' products of each layer run as one grouped GEMM; only the
 // per-stream reductions of the column partials are separate launches.
-static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int B, Ws& W, void* dth, float beta) {
+// gin (gin_dt): the gradient arriving at the block's output, W.g itself or
+// (the model's first backward block) the cotangent in the activation dtype;
+// W.g holds the gradient at the block's input on return.
+static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int B, Ws& W, void* dth, float beta,
+                   const void* gin, int gin_dt) {
   const Model& m = cx.m;
   const int D = m.D, F = m.F, act = m.act;
   const RowMap rm{B, m.nt, m.ni};
@@ -645,7 +649,7 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
     return gemm2(a, b, S);
   };
   // MLP branch: x_out = xm + gate2 * y2
-  TRY(gate_bwd(W.g, A.y2, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, g2a, g2b, S));
+  TRY(gate_bwd(gin, gin_dt, A.y2, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 5 * D, W.dY, D, g2a, g2b, S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
@@ -664,7 +668,8 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   }
   TRY(wg2(W.dbig, F, A.a2, D, F, D, st[0].fc1.w, st[1].fc1.w));
   TRY(dg2(W.dbig, F, st[0].fc1.w, st[1].fc1.w, D, F, D, W.dA, D, F32));
-  TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, 0, R, A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, W.g, l2a, l2b, S));
+  TRY(ln_mod_bwd(W.dA, A.xm, act, D, rm, 0, R, A.m2, A.r2, A.mod[0], A.mod[1], 6 * D, 4 * D, gin, gin_dt, W.g, l2a,
+                 l2b, S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
@@ -676,7 +681,7 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   // attention branch: xm = x + gate1 * y1 (W.dY and W.dbig are rewritten
   // from here on: the fc2 and fc1 weight gradients that read them are done)
   TRY(cx.join());
-  TRY(gate_bwd(W.g, A.y1, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, g1a, g1b, S));
+  TRY(gate_bwd(W.g, F32, A.y1, act, D, rm, 0, R, A.mod[0], A.mod[1], 6 * D, 2 * D, W.dY, D, g1a, g1b, S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
@@ -710,7 +715,8 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   }
   TRY(wg2(W.dbig, 3 * D, A.a1, D, 3 * D, D, st[0].qkv.w, st[1].qkv.w));
   TRY(dg2(W.dbig, 3 * D, st[0].qkv.w, st[1].qkv.w, D, 3 * D, D, W.dA, D, F32));
-  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, W.p1, W.p2, S));
+  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m1, A.r1, A.mod[0], A.mod[1], 6 * D, D, W.g, F32, W.g, W.p1, W.p2,
+                 S));
   {
     RedJob j[4];
     for (int s = 0; s < 2; ++s) {
@@ -740,7 +746,7 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   const size_t es = dsize(act);
   const SBlock& L = m.sgl[i];
   const int nchunk = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
-  TRY(gate_bwd(W.g, A.y, act, D, rm, 0, R, A.mod, A.mod, 3 * D, 2 * D, W.dY, D, W.p1, W.p2, cx.s));
+  TRY(gate_bwd(W.g, F32, A.y, act, D, rm, 0, R, A.mod, A.mod, 3 * D, 2 * D, W.dY, D, W.p1, W.p2, cx.s));
   {
     const RedJob j[2] = {per_sample_job(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, 2 * D),
                          to_grad_job(W.p2, D, 0, nchunk, D, G(dth, m, L.out.b), m.grad, beta)};
@@ -767,7 +773,7 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
   }
   TRY(wgrad(cx, W.dbig, LD, act, A.a, D, R, LD, D, G(dth, m, L.in.w), beta));
   TRY(dgrad(cx, W.dbig, LD, R, cx.P(L.in.w), D, LD, D, W.dA, D, F32));
-  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m, A.r, A.mod, A.mod, 3 * D, D, W.g, W.p1, W.p2, cx.s));
+  TRY(ln_mod_bwd(W.dA, A.x_in, act, D, rm, 0, R, A.m, A.r, A.mod, A.mod, 3 * D, D, W.g, F32, W.g, W.p1, W.p2, cx.s));
   {
     const RedJob j[2] = {per_sample_job(W.p1, D, rm, 0, R, W.dmod[0], 3 * D, D, LN_ROWS),
                          per_sample_job(W.p2, D, rm, 0, R, W.dmod[0], 3 * D, 0, LN_ROWS)};
@@ -825,7 +831,15 @@ static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const
   plan_saved(m, B, (void*)saved, S);
   const Global& gl = S.g;
   TRY(fill_zero(W.dmvec, (size_t)B * D * 4, cx.s));
-  if (m.c.block_only) {
+  // the gradient arriving at the last block: the cotangent itself when that
+  // block is a double block of a block-only model (its gate and second
+  // LayerNorm backward read it in the activation dtype), else W.g
+  const void* gin = W.g;
+  int gin_dt = F32;
+  if (m.c.block_only && m.c.n_single == 0 && m.c.n_double > 0) {
+    gin = cot;
+    gin_dt = act;
+  } else if (m.c.block_only) {
     TRY(convert(cot, act, W.g, F32, (size_t)R * D, cx.s));
   } else {
     // final layer: v = unpatchify((LN(x_img)(1 + scale) + shift) W_f^T + b_f)
@@ -839,8 +853,8 @@ static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const
     TRY(dgrad(cx, W.fout, m.pd, Mi, cx.P(m.fin.w), D, m.pd, D, W.dfa + (size_t)rt * D, D, F32));
     TRY(fill_zero(W.g, (size_t)R * D * 4, cx.s));
     void* xl = m.sgl.empty() ? (m.dbl.empty() ? gl.x0 : S.d.back().x_out) : S.s.back().x_out;
-    TRY(ln_mod_bwd(W.dfa, xl, act, D, rm, rt, R - rt, gl.fm, gl.fr, gl.fmod, gl.fmod, 2 * D, D, W.g, W.p1, W.p2,
-                   cx.s));
+    TRY(ln_mod_bwd(W.dfa, xl, act, D, rm, rt, R - rt, gl.fm, gl.fr, gl.fmod, gl.fmod, 2 * D, D, W.g, F32, W.g, W.p1,
+                   W.p2, cx.s));
     TRY(reduce_per_sample(W.p1, D, rm, rt, R - rt, W.dmod[0], 2 * D, D, cx.s, LN_ROWS));
     TRY(reduce_per_sample(W.p2, D, rm, rt, R - rt, W.dmod[0], 2 * D, 0, cx.s, LN_ROWS));
     TRY(small_linear_bwd(W.dmod[0], gl.mvec, 0, B, D, cx.P(m.fmod.w), act, 2 * D, G(dth, m, m.fmod.w),
@@ -867,7 +881,9 @@ static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const
       TRY(dbl_fwd(cx, i, R2, gl.mvec, B));
       A = R2;
     }
-    TRY(dbl_bwd(cx, i, A, gl.mvec, B, W, dth, beta));
+    TRY(dbl_bwd(cx, i, A, gl.mvec, B, W, dth, beta, gin, gin_dt));
+    gin = W.g;
+    gin_dt = F32;
   }
   if (!m.c.block_only) {
     // input embeddings (no gradient to the inputs themselves)

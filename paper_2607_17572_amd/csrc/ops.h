@@ -55,11 +55,13 @@ int mul_silu_grad(float* y, const float* x, size_t n, hipStream_t s);
 int ln_mod_fwd(const void* x, int act_dt, int D, RowMap rm, int row0, int nrows, const float* mod_txt,
                const float* mod_img, int mod_w, int sh_off, int sc_off, void* a, float* mean, float* rstd,
                hipStream_t s);
-// g[r] += LN_bwd(dA * (1 + scale)) and partials of sum dA*xhat (-> part_scale)
-// and sum dA (-> part_shift) per chunk of LN_ROWS rows, [chunk][D].
+// g[r] = g_in[r] + LN_bwd(dA * (1 + scale)) and partials of sum dA*xhat
+// (-> part_scale) and sum dA (-> part_shift) per chunk of LN_ROWS rows,
+// [chunk][D].  g_in is fp32 (it may be g itself) or, with bf16 activations, bf16.
 int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int row0, int nrows,
                const float* mean, const float* rstd, const float* mod_txt, const float* mod_img, int mod_w,
-               int sc_off, float* g, float* part_scale, float* part_shift, hipStream_t s);
+               int sc_off, const void* g_in, int g_in_dt, float* g, float* part_scale, float* part_shift,
+               hipStream_t s);
 
 // ---- gated residual ----
 // xo = xi + gate[b] * y  (rows [row0, row0+nrows))
@@ -67,7 +69,8 @@ int gated_residual(const void* xi, const void* y, int act_dt, int D, int ld_y, R
                    const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* xo,
                    hipStream_t s);
 // dY = g * gate[b] (act dtype), partials: part_gate = sum g*y, part_bias = sum dY.
-int gate_bwd(const float* g, const void* y, int act_dt, int D, RowMap rm, int row0, int nrows,
+// g is fp32 or, with bf16 activations, bf16 (g_dt).
+int gate_bwd(const void* g, int g_dt, const void* y, int act_dt, int D, RowMap rm, int row0, int nrows,
              const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* dY, int ld_dy,
              float* part_gate, float* part_bias, hipStream_t s);
 

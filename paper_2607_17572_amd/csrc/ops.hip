@@ -539,12 +539,12 @@ int ln_mod_fwd(const void* x, int act_dt, int D, RowMap rm, int row0, int nrows,
   return 0;
 }
 
-template <typename T>
+template <typename T, typename TG>
 __global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA, const T* __restrict__ x, int D,
                                                     Chunks ch, int c0, const float* __restrict__ mean,
                                                     const float* __restrict__ rstd, const float* __restrict__ mt,
                                                     const float* __restrict__ mi, int mod_w, int sc_off,
-                                                    float* __restrict__ g, float* __restrict__ psc,
+                                                    const TG* gin, float* g, float* __restrict__ psc,
                                                     float* __restrict__ psh) {
   __shared__ float sh[16];
   const int q = c0 + blockIdx.x;
@@ -585,7 +585,7 @@ __global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA
 #pragma unroll
     for (int i = 0; i < MAXC; ++i) {
       const int c = threadIdx.x + i * 256;
-      if (c < D) g[(size_t)r * D + c] += rs * (dxh[i] - m1 - xh[i] * m2);
+      if (c < D) g[(size_t)r * D + c] = ldf(gin, (size_t)r * D + c) + rs * (dxh[i] - m1 - xh[i] * m2);
     }
   }
 #pragma unroll
@@ -606,11 +606,11 @@ __global__ __launch_bounds__(256) void ln_mod_bwd_k(const float* __restrict__ dA
 // rows, so the many blocks spread evenly over the CUs.  The per-column partial
 // sums of the waves are combined through LDS in wave order.
 constexpr int LN_W = 4;
-template <typename T, int NV>
+template <typename T, typename TG, int NV>
 __global__ __launch_bounds__(64 * LN_W) __attribute__((amdgpu_waves_per_eu(2, 2))) void ln_mod_bwd_vec_k(
     const float* __restrict__ dA, const T* __restrict__ x, Chunks ch, int c0, const float* __restrict__ mean,
     const float* __restrict__ rstd, const float* __restrict__ mt, const float* __restrict__ mi, int mod_w,
-    int sc_off, float* __restrict__ g, float* __restrict__ psc, float* __restrict__ psh) {
+    int sc_off, const TG* gin, float* g, float* __restrict__ psc, float* __restrict__ psh) {
   constexpr int D = NV * 512;
   extern __shared__ float red[];  // [LN_W][D] column sums per wave, then [D] factors 1 + scale
   float* const ms = red + LN_W * D;
@@ -668,7 +668,7 @@ __global__ __launch_bounds__(64 * LN_W) __attribute__((amdgpu_waves_per_eu(2, 2)
       const int c = 8 * lane + 512 * i;
       float m[8], gv[8];
       ld8f(ms + mo + 512 * i, m);
-      ld8f(g + (size_t)r * D + c, gv);
+      ld8f(gin + (size_t)r * D + c, gv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xhat = (xr[i][e] - mu) * rs;
@@ -700,42 +700,44 @@ __global__ __launch_bounds__(64 * LN_W) __attribute__((amdgpu_waves_per_eu(2, 2)
 
 int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int row0, int nrows,
                const float* mean, const float* rstd, const float* mod_txt, const float* mod_img, int mod_w,
-               int sc_off, float* g, float* part_scale, float* part_shift, hipStream_t s) {
+               int sc_off, const void* g_in, int g_in_dt, float* g, float* part_scale, float* part_shift,
+               hipStream_t s) {
   if (D > 256 * MAXC) { set_error("ln_mod_bwd: hidden too large"); return 1; }
+  if (g_in_dt == BF16 && act_dt != BF16) { set_error("ln_mod_bwd: a bf16 incoming gradient needs bf16 activations"); return 1; }
   int c0, nc;
   if (chunk_range(rm, row0, nrows, &c0, &nc, LN_ROWS)) return 1;
   if (nc == 0) return 0;
   Chunks ch{rm.B, rm.nt, rm.ni, LN_ROWS};
-  if (D % 512 == 0 && D <= 3584 && al16(dA) && al16(x) && al16(g)) {
+  if (D % 512 == 0 && D <= 3584 && al16(dA) && al16(x) && al16(g) && al16(g_in)) {
     const size_t lds = (LN_W + 1) * (size_t)D * sizeof(float);
-#define LNB(T, NV)                                                                                             \
+#define LNB(T, TG, NV)                                                                                         \
   case NV: {                                                                                                   \
-    auto k = ln_mod_bwd_vec_k<T, NV>;                                                                          \
+    auto k = ln_mod_bwd_vec_k<T, TG, NV>;                                                                      \
     if (lds > 65536 &&                                                                                         \
         hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) { \
       set_error("ln_mod_bwd: cannot reserve the row buffers in LDS");                                          \
       return 3;                                                                                                \
     }                                                                                                          \
     hipLaunchKernelGGL(k, dim3(nc), dim3(64 * LN_W), lds, s, dA, (const T*)x, ch, c0, mean, rstd, mod_txt, mod_img, \
-                       mod_w, sc_off, g, part_scale, part_shift);                                              \
+                       mod_w, sc_off, (const TG*)g_in, g, part_scale, part_shift);                              \
   } break;
-    if (act_dt == BF16) {
-      switch (D / 512) { LNB(uint16_t, 1) LNB(uint16_t, 2) LNB(uint16_t, 3) LNB(uint16_t, 4) LNB(uint16_t, 5)
-                         LNB(uint16_t, 6) LNB(uint16_t, 7) }
-    } else {
-      switch (D / 512) { LNB(float, 1) LNB(float, 2) LNB(float, 3) LNB(float, 4) LNB(float, 5) LNB(float, 6)
-                         LNB(float, 7) }
-    }
+#define LNS(T, TG) \
+  switch (D / 512) { LNB(T, TG, 1) LNB(T, TG, 2) LNB(T, TG, 3) LNB(T, TG, 4) LNB(T, TG, 5) LNB(T, TG, 6) LNB(T, TG, 7) }
+    if (act_dt == BF16 && g_in_dt == BF16) LNS(uint16_t, uint16_t)
+    else if (act_dt == BF16) LNS(uint16_t, float)
+    else LNS(float, float)
+#undef LNS
 #undef LNB
     LAUNCH_OK("ln_mod_bwd_vec");
     return 0;
   }
-  if (act_dt == BF16)
-    hipLaunchKernelGGL(ln_mod_bwd_k<uint16_t>, dim3(nc), dim3(256), 0, s, dA, (const uint16_t*)x, D, ch, c0, mean,
-                       rstd, mod_txt, mod_img, mod_w, sc_off, g, part_scale, part_shift);
-  else
-    hipLaunchKernelGGL(ln_mod_bwd_k<float>, dim3(nc), dim3(256), 0, s, dA, (const float*)x, D, ch, c0, mean, rstd,
-                       mod_txt, mod_img, mod_w, sc_off, g, part_scale, part_shift);
+#define LNK(T, TG)                                                                                              \
+  hipLaunchKernelGGL((ln_mod_bwd_k<T, TG>), dim3(nc), dim3(256), 0, s, dA, (const T*)x, D, ch, c0, mean, rstd, \
+                     mod_txt, mod_img, mod_w, sc_off, (const TG*)g_in, g, part_scale, part_shift)
+  if (act_dt == BF16 && g_in_dt == BF16) LNK(uint16_t, uint16_t);
+  else if (act_dt == BF16) LNK(uint16_t, float);
+  else LNK(float, float);
+#undef LNK
   LAUNCH_OK("ln_mod_bwd");
   return 0;
 }
@@ -803,8 +805,8 @@ int gated_residual(const void* xi, const void* y, int act_dt, int D, int ld_y, R
   return 0;
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void gate_bwd_k(const float* __restrict__ g, const T* __restrict__ y, int D,
+template <typename T, typename TG>
+__global__ __launch_bounds__(256) void gate_bwd_k(const TG* __restrict__ g, const T* __restrict__ y, int D,
                                                   Chunks ch, int c0, const float* __restrict__ mt,
                                                   const float* __restrict__ mi, int mod_w, int gate_off,
                                                   T* __restrict__ dY, int ld_dy, float* __restrict__ pg,
@@ -818,7 +820,7 @@ __global__ __launch_bounds__(256) void gate_bwd_k(const float* __restrict__ g, c
     float sg = 0.f, sb = 0.f;
     for (int rr = 0; rr < n; ++rr) {
       const int r = r0 + rr;
-      const float gv = g[(size_t)r * D + c];
+      const float gv = ldf(g, (size_t)r * D + c);
       sg = fmaf(gv, ldf(y, (size_t)r * D + c), sg);
       const float d = gv * gt;
       sb += d;
@@ -829,8 +831,8 @@ __global__ __launch_bounds__(256) void gate_bwd_k(const float* __restrict__ g, c
   }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void gate_bwd_vec_k(const float* __restrict__ g, const T* __restrict__ y, int D,
+template <typename T, typename TG>
+__global__ __launch_bounds__(256) void gate_bwd_vec_k(const TG* __restrict__ g, const T* __restrict__ y, int D,
                                                       Chunks ch, int c0, const float* __restrict__ mt,
                                                       const float* __restrict__ mi, int mod_w, int gate_off,
                                                       T* __restrict__ dY, int ld_dy, float* __restrict__ pg,
@@ -862,9 +864,10 @@ __global__ __launch_bounds__(256) void gate_bwd_vec_k(const float* __restrict__ 
   st8f(pb + (size_t)q * D + c, sb);
 }
 
-int gate_bwd(const float* g, const void* y, int act_dt, int D, RowMap rm, int row0, int nrows,
+int gate_bwd(const void* g, int g_dt, const void* y, int act_dt, int D, RowMap rm, int row0, int nrows,
              const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* dY, int ld_dy,
              float* part_gate, float* part_bias, hipStream_t s) {
+  if (g_dt == BF16 && act_dt != BF16) { set_error("gate_bwd: a bf16 incoming gradient needs bf16 activations"); return 1; }
   int c0, nc;
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   if (nc == 0) return 0;
@@ -872,21 +875,23 @@ int gate_bwd(const float* g, const void* y, int act_dt, int D, RowMap rm, int ro
   if (D % 8 == 0 && ld_dy % 8 == 0 && mod_w % 4 == 0 && gate_off % 4 == 0 && al16(g) && al16(y) && al16(dY) &&
       al16(mod_txt) && al16(mod_img) && al16(part_gate) && al16(part_bias)) {
     dim3 grid(nc, (D + 2047) / 2048);
-    if (act_dt == BF16)
-      hipLaunchKernelGGL(gate_bwd_vec_k<uint16_t>, grid, dim3(256), 0, s, g, (const uint16_t*)y, D, ch, c0, mod_txt,
-                         mod_img, mod_w, gate_off, (uint16_t*)dY, ld_dy, part_gate, part_bias);
-    else
-      hipLaunchKernelGGL(gate_bwd_vec_k<float>, grid, dim3(256), 0, s, g, (const float*)y, D, ch, c0, mod_txt,
-                         mod_img, mod_w, gate_off, (float*)dY, ld_dy, part_gate, part_bias);
+#define GBV(T, TG)                                                                                             \
+  hipLaunchKernelGGL((gate_bwd_vec_k<T, TG>), grid, dim3(256), 0, s, (const TG*)g, (const T*)y, D, ch, c0, mod_txt, \
+                     mod_img, mod_w, gate_off, (T*)dY, ld_dy, part_gate, part_bias)
+    if (act_dt == BF16 && g_dt == BF16) GBV(uint16_t, uint16_t);
+    else if (act_dt == BF16) GBV(uint16_t, float);
+    else GBV(float, float);
+#undef GBV
     LAUNCH_OK("gate_bwd_vec");
     return 0;
   }
-  if (act_dt == BF16)
-    hipLaunchKernelGGL(gate_bwd_k<uint16_t>, dim3(nc), dim3(256), 0, s, g, (const uint16_t*)y, D, ch, c0, mod_txt,
-                       mod_img, mod_w, gate_off, (uint16_t*)dY, ld_dy, part_gate, part_bias);
-  else
-    hipLaunchKernelGGL(gate_bwd_k<float>, dim3(nc), dim3(256), 0, s, g, (const float*)y, D, ch, c0, mod_txt,
-                       mod_img, mod_w, gate_off, (float*)dY, ld_dy, part_gate, part_bias);
+#define GBK(T, TG)                                                                                              \
+  hipLaunchKernelGGL((gate_bwd_k<T, TG>), dim3(nc), dim3(256), 0, s, (const TG*)g, (const T*)y, D, ch, c0, mod_txt, \
+                     mod_img, mod_w, gate_off, (T*)dY, ld_dy, part_gate, part_bias)
+  if (act_dt == BF16 && g_dt == BF16) GBK(uint16_t, uint16_t);
+  else if (act_dt == BF16) GBK(uint16_t, float);
+  else GBK(float, float);
+#undef GBK
   LAUNCH_OK("gate_bwd");
   return 0;
 }
