@@ -832,7 +832,7 @@ __global__ __launch_bounds__(256) void gate_bwd_k(const TG* __restrict__ g, cons
 }
 
 template <typename T, typename TG>
-__global__ __launch_bounds__(256) void gate_bwd_vec_k(const TG* __restrict__ g, const T* __restrict__ y, int D,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) void gate_bwd_vec_k(const TG* __restrict__ g, const T* __restrict__ y, int D,
                                                       Chunks ch, int c0, const float* __restrict__ mt,
                                                       const float* __restrict__ mi, int mod_w, int gate_off,
                                                       T* __restrict__ dY, int ld_dy, float* __restrict__ pg,
@@ -846,12 +846,8 @@ __global__ __launch_bounds__(256) void gate_bwd_vec_k(const TG* __restrict__ g, 
   float gt[8], sg[8], sb[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) { gt[e] = m[e]; sg[e] = 0.f; sb[e] = 0.f; }
-#pragma unroll 2
-  for (int rr = 0; rr < n; ++rr) {
-    const int r = r0 + rr;
-    float gv[8], yv[8], d[8];
-    ld8f(g + (size_t)r * D + c, gv);
-    ld8f(y + (size_t)r * D + c, yv);
+  auto row = [&](const Raw8<TG>& gv, const Raw8<T>& yv, int r) {
+    float d[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       sg[e] = fmaf(gv[e], yv[e], sg[e]);
@@ -859,6 +855,26 @@ __global__ __launch_bounds__(256) void gate_bwd_vec_k(const TG* __restrict__ g, 
       sb[e] += d[e];
     }
     st8f(dY + (size_t)r * ld_dy + c, d);
+  };
+  // four rows' loads issued together, then the rows in order
+  int rr = 0;
+  for (; rr + 4 <= n; rr += 4) {
+    Raw8<TG> gv[4];
+    Raw8<T> yv[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      gv[k].load(g + (size_t)(r0 + rr + k) * D + c);
+      yv[k].load(y + (size_t)(r0 + rr + k) * D + c);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) row(gv[k], yv[k], r0 + rr + k);
+  }
+  for (; rr < n; ++rr) {
+    Raw8<TG> gv;
+    Raw8<T> yv;
+    gv.load(g + (size_t)(r0 + rr) * D + c);
+    yv.load(y + (size_t)(r0 + rr) * D + c);
+    row(gv, yv, r0 + rr);
   }
   st8f(pg + (size_t)q * D + c, sg);
   st8f(pb + (size_t)q * D + c, sb);
