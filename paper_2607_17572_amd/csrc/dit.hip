@@ -298,9 +298,9 @@ static size_t plan_ws(const Model& m, int B, void* base, Ws& W) {
   W.delta = a.f32(2 * hn);  // delta, then the log-sum-exp in log2 units
   if (m.act == BF16 && m.Dh == 128)
     W.dS = a.take((size_t)B * m.H * attn_ds_rows(m.N) * attn_ds_ld(m.N) * 2);
-  // per 32-row chunk: the widest partials of one launch, or the q/k gain
-  // partials followed by the LayerNorm partials (RED_ROWS / LN_ROWS blocks)
-  W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, QK_PARTS * 2 * m.Dh + RED_ROWS / LN_ROWS * m.D, m.pd});
+  // per 32-row chunk: the widest partials of one launch (the LayerNorm
+  // backward's come per block of LN_ROWS rows, RED_ROWS / LN_ROWS per chunk)
+  W.maxcols = std::max({3 * m.D + m.F, m.D + m.F, QK_PARTS * 2 * m.Dh, RED_ROWS / LN_ROWS * m.D, m.pd});
   const int nch = Chunks{B, m.nt, m.ni, RED_ROWS}.count();
   W.p1 = a.f32((size_t)nch * W.maxcols);
   W.p2 = a.f32((size_t)nch * W.maxcols);
