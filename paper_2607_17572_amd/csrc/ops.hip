@@ -703,7 +703,10 @@ int ln_mod_bwd(const float* dA, const void* x, int act_dt, int D, RowMap rm, int
                int sc_off, const void* g_in, int g_in_dt, float* g, float* part_scale, float* part_shift,
                hipStream_t s) {
   if (D > 256 * MAXC) { set_error("ln_mod_bwd: hidden too large"); return 1; }
-  if (g_in_dt == BF16 && act_dt != BF16) { set_error("ln_mod_bwd: a bf16 incoming gradient needs bf16 activations"); return 1; }
+  if (g_in_dt == BF16 && act_dt != BF16) {
+    set_error("ln_mod_bwd: a bf16 incoming gradient needs bf16 activations");
+    return 1;
+  }
   int c0, nc;
   if (chunk_range(rm, row0, nrows, &c0, &nc, LN_ROWS)) return 1;
   if (nc == 0) return 0;
@@ -831,12 +834,13 @@ __global__ __launch_bounds__(256) void gate_bwd_k(const TG* __restrict__ g, cons
   }
 }
 
+// At most 4 waves per SIMD, so that the compiler may keep four rows' loads in
+// registers (at 8 waves it reused the load registers and waited per load).
 template <typename T, typename TG>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) void gate_bwd_vec_k(const TG* __restrict__ g, const T* __restrict__ y, int D,
-                                                      Chunks ch, int c0, const float* __restrict__ mt,
-                                                      const float* __restrict__ mi, int mod_w, int gate_off,
-                                                      T* __restrict__ dY, int ld_dy, float* __restrict__ pg,
-                                                      float* __restrict__ pb) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) void gate_bwd_vec_k(
+    const TG* __restrict__ g, const T* __restrict__ y, int D, Chunks ch, int c0, const float* __restrict__ mt,
+    const float* __restrict__ mi, int mod_w, int gate_off, T* __restrict__ dY, int ld_dy, float* __restrict__ pg,
+    float* __restrict__ pb) {
   const int q = c0 + blockIdx.x;
   int r0, n, b;
   chunk_rows(ch, q, r0, n, b);
@@ -883,7 +887,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) voi
 int gate_bwd(const void* g, int g_dt, const void* y, int act_dt, int D, RowMap rm, int row0, int nrows,
              const float* mod_txt, const float* mod_img, int mod_w, int gate_off, void* dY, int ld_dy,
              float* part_gate, float* part_bias, hipStream_t s) {
-  if (g_dt == BF16 && act_dt != BF16) { set_error("gate_bwd: a bf16 incoming gradient needs bf16 activations"); return 1; }
+  if (g_dt == BF16 && act_dt != BF16) {
+    set_error("gate_bwd: a bf16 incoming gradient needs bf16 activations");
+    return 1;
+  }
   int c0, nc;
   if (chunk_range(rm, row0, nrows, &c0, &nc)) return 1;
   if (nc == 0) return 0;
