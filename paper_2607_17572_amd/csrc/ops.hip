@@ -987,11 +987,92 @@ __global__ void qk_norm_rope_fwd_row_k(const T* __restrict__ proj, int ld, RowMa
                                        T* __restrict__ Qh, T* __restrict__ Kh, T* __restrict__ Vh,
                                        float* __restrict__ rq, float* __restrict__ rk);
 
+// Forward for bf16 and head_dim 128 with 16-byte accesses, one wave per row:
+// per step the wave takes four heads, 16 lanes per head, each lane 4 RoPE
+// pairs (8 consecutive elements).  The rotation of pair p is computed once per
+// row by lane p and handed to the lanes that use it; the RMS sums run over the
+// 16 lanes of a head.
+__global__ __launch_bounds__(256) void qk_norm_rope_fwd8_k(const uint16_t* __restrict__ proj, int ld, RowMap rm,
+                                                           Rope rp, Gains gn, uint16_t* __restrict__ Qh,
+                                                           uint16_t* __restrict__ Kh, uint16_t* __restrict__ Vh,
+                                                           float* __restrict__ rq, float* __restrict__ rk) {
+  constexpr int Dh = 128;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rm.rows()) return;
+  const int lane = threadIdx.x & 63, hq = lane >> 4, lp = lane & 15, e0 = 8 * lp;
+  const int H = rp.H, D = H * Dh, N = rm.nt + rm.ni;
+  const int st = r < rm.B * rm.nt ? 0 : 1;
+  float qg[8], kg[8];
+  ld8f((const uint16_t*)gn.q[st] + e0, qg);
+  ld8f((const uint16_t*)gn.k[st] + e0, kg);
+  int b, j;
+  tok_of_row(rm, r, b, j);
+  float sn0, cs0;
+  sincosf(rope_angle(rp, j, lane), &sn0, &cs0);
+  float cs[4], sn[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    cs[k] = __shfl(cs0, 4 * lp + k, 64);
+    sn[k] = __shfl(sn0, 4 * lp + k, 64);
+  }
+  const uint16_t* pr = proj + (size_t)r * ld + e0;
+  const size_t ob = ((size_t)b * H * N + j) * Dh + e0;  // head h adds h * N * Dh
+  for (int h0 = 0; h0 < H; h0 += 4) {
+    const int h = h0 + hq;
+    const bool hv = h < H;
+    const int hh = hv ? h : 0;  // lanes past the last head compute on head 0, store nothing
+    float x[8], y[8];
+    ld8f(pr + hh * Dh, x);
+    ld8f(pr + D + hh * Dh, y);
+    const uint4 vv = *(const uint4*)(pr + 2 * D + hh * Dh);
+    float sq = 0.f, sk = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      sq = fmaf(x[e], x[e], sq);
+      sk = fmaf(y[e], y[e], sk);
+    }
+#pragma unroll
+    for (int m = 8; m > 0; m >>= 1) {
+      sq += __shfl_xor(sq, m, 16);
+      sk += __shfl_xor(sk, m, 16);
+    }
+    const float riq = rsqrtf(sq / Dh + 1e-6f), rik = rsqrtf(sk / Dh + 1e-6f);
+    float oq[8], ok[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float qa = x[2 * k] * riq * qg[2 * k], qb = x[2 * k + 1] * riq * qg[2 * k + 1];
+      const float ka = y[2 * k] * rik * kg[2 * k], kb = y[2 * k + 1] * rik * kg[2 * k + 1];
+      oq[2 * k] = qa * cs[k] - qb * sn[k];
+      oq[2 * k + 1] = qa * sn[k] + qb * cs[k];
+      ok[2 * k] = ka * cs[k] - kb * sn[k];
+      ok[2 * k + 1] = ka * sn[k] + kb * cs[k];
+    }
+    if (hv) {
+      const size_t o = ob + (size_t)h * N * Dh;
+      st8f(Qh + o, oq);
+      st8f(Kh + o, ok);
+      *(uint4*)(Vh + o) = vv;
+      if (lp == 0) {
+        rq[(size_t)r * H + h] = riq;
+        rk[(size_t)r * H + h] = rik;
+      }
+    }
+  }
+}
+
 int qk_norm_rope_fwd(const void* proj, int ld, int act_dt, RowMap rm, Rope rp, Gains gn,
                      void* Qh, void* Kh, void* Vh, float* rinv_q, float* rinv_k, hipStream_t s) {
   if (rp.Dh > 128 || rp.Dh % 4) { set_error("qk_norm_rope: head_dim must be <= 128 and a multiple of 4"); return 1; }
   // RoPE pairs as one access each: even leading dimension, 8-byte aligned bases
   auto al8 = [](const void* p) { return ((uintptr_t)p & 7u) == 0; };
+  if (act_dt == BF16 && rp.Dh == 128 && !(ld & 7) && al16(proj) && al16(Qh) && al16(Kh) && al16(Vh) &&
+      al16(gn.q[0]) && al16(gn.q[1]) && al16(gn.k[0]) && al16(gn.k[1])) {
+    hipLaunchKernelGGL(qk_norm_rope_fwd8_k, dim3((unsigned)((rm.rows() + 3) / 4)), dim3(256), 0, s,
+                       (const uint16_t*)proj, ld, rm, rp, gn, (uint16_t*)Qh, (uint16_t*)Kh, (uint16_t*)Vh, rinv_q,
+                       rinv_k);
+    LAUNCH_OK("qk_norm_rope_fwd8");
+    return 0;
+  }
   if (!(ld & 1) && al8(proj) && al8(Qh) && al8(Kh) && al8(Vh)) {
     const dim3 grid((unsigned)((rm.rows() + 3) / 4));
     if (act_dt == BF16)
