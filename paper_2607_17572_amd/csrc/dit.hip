@@ -730,8 +730,7 @@ static int dbl_bwd(const Ctx& cx, int i, const DblAct& A, const float* mvec, int
   // adaLN modulation: mod = SiLU(vec) W_mod^T + b, per stream; d SiLU(vec) in the order text, image
   for (int s = 0; s < 2; ++s) {
     TRY(small_linear_bwd(W.dmod[s], mvec, 0, B, D, cx.P(st[s].mod.w), m.act, 6 * D, G(dth, m, st[s].mod.w),
-                         G(dth, m, st[s].mod.b), m.grad, beta, W.tmp, W.slpart, S));
-    TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, S));
+                         G(dth, m, st[s].mod.b), m.grad, beta, W.dmvec, W.slpart, S, true));
   }
   TRY(cx.join());  // the next block reuses W.dY and W.dbig
   (void)rowf;
@@ -780,8 +779,7 @@ static int sgl_bwd(const Ctx& cx, int i, const SglAct& A, const float* mvec, int
     TRY(reduce_jobs(j, 2, cx.s));
   }
   TRY(small_linear_bwd(W.dmod[0], mvec, 0, B, D, cx.P(L.mod.w), m.act, 3 * D, G(dth, m, L.mod.w), G(dth, m, L.mod.b),
-                       m.grad, beta, W.tmp, W.slpart, cx.s));
-  TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, cx.s));
+                       m.grad, beta, W.dmvec, W.slpart, cx.s, true));
   return 0;
 }
 
@@ -858,8 +856,7 @@ static int vjp(jagg_ctx* ctx, const void* theta, const void* saved, int B, const
     TRY(reduce_per_sample(W.p1, D, rm, rt, R - rt, W.dmod[0], 2 * D, D, cx.s, LN_ROWS));
     TRY(reduce_per_sample(W.p2, D, rm, rt, R - rt, W.dmod[0], 2 * D, 0, cx.s, LN_ROWS));
     TRY(small_linear_bwd(W.dmod[0], gl.mvec, 0, B, D, cx.P(m.fmod.w), act, 2 * D, G(dth, m, m.fmod.w),
-                         G(dth, m, m.fmod.b), m.grad, beta, W.tmp, W.slpart, cx.s));
-    TRY(add_into(W.dmvec, W.tmp, (size_t)B * D, cx.s));
+                         G(dth, m, m.fmod.b), m.grad, beta, W.dmvec, W.slpart, cx.s, true));
   }
   for (int i = m.c.n_single - 1; i >= 0; --i) {
     SglAct A = S.s[i];

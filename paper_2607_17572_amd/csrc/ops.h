@@ -34,12 +34,13 @@ constexpr int LN_ROWS = 8;
 int small_linear_fwd(const float* in, int act, int B, int Din, const void* W, const void* bias, int w_dt,
                      float* out, int Dout, hipStream_t s);
 // dW[j][d] (+)= sum_b dout[b][j] act(in[b][d]) ; db[j] (+)= sum_b dout[b][j];
-// din[b][d] = sum_j dout[b][j] W[j][d]  (fp32, overwritten; nullptr to skip).
+// din[b][d] (+)= sum_j dout[b][j] W[j][d]  (fp32, overwritten, or added to
+// when din_acc; nullptr to skip).
 // `part` is workspace of small_linear_bwd_part_floats() floats.
 size_t small_linear_bwd_part_floats(int B, int Din, int Dout);
 int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din, const void* W, int w_dt,
                      int Dout, void* dW, void* db, int g_dt, float beta, float* din, float* part,
-                     hipStream_t s);
+                     hipStream_t s, bool din_acc = false);
 
 // ---- time embedding: temb[b][k] = cos(1000 t_b w_k), temb[b][F/2+k] = sin(...) ----
 struct TVals { float t[64]; };
@@ -133,7 +134,6 @@ int patchify(const void* z, int dt, int B, int C, int Hh, int Ww, int p, void* o
 int unpatchify(const void* x, int dt, int B, int C, int Hh, int Ww, int p, void* z, hipStream_t s);
 int convert(const void* x, int dt_in, void* y, int dt_out, size_t n, hipStream_t s);
 int fill_zero(void* x, size_t bytes, hipStream_t s);
-int add_into(float* y, const float* x, size_t n, hipStream_t s);
 
 // ---- JAGG aggregation (Eq. s_base / s_corr) ----
 struct AggArgs {

@@ -249,11 +249,12 @@ __global__ __launch_bounds__(256) void small_linear_bwd_k(const float* __restric
     for (int b = 0; b < B; ++b) part[((size_t)jt * B + b) * Din + d] = acc[b];
 }
 
-// out[i] = sum over p of part[p * n + i], parts added in a fixed order: 64
+// out[i] (+)= sum over p of part[p * n + i], parts added in a fixed order: 64
 // consecutive outputs per block, 4 slices of the parts per output (slice q
-// sums parts q, q+4, ...), slices combined in order in LDS.
+// sums parts q, q+4, ...), slices combined in order in LDS; acc: the sum is
+// added to out's old value.
 __global__ __launch_bounds__(256) void sum_parts_k(const float* __restrict__ part, int nparts, size_t n,
-                                                   float* __restrict__ out) {
+                                                   float* __restrict__ out, bool acc_out) {
   __shared__ float sl[4][64];
   const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
   const size_t i = (size_t)blockIdx.x * 64 + c;
@@ -264,7 +265,10 @@ __global__ __launch_bounds__(256) void sum_parts_k(const float* __restrict__ par
   }
   sl[q][c] = acc;
   __syncthreads();
-  if (q == 0 && i < n) out[i] = ((sl[0][c] + sl[1][c]) + sl[2][c]) + sl[3][c];
+  if (q == 0 && i < n) {
+    const float t = ((sl[0][c] + sl[1][c]) + sl[2][c]) + sl[3][c];
+    out[i] = acc_out ? out[i] + t : t;
+  }
 }
 
 // Small batches: 8 consecutive input columns per thread (16-byte loads and
@@ -338,7 +342,7 @@ __global__ __launch_bounds__(128) void small_linear_bwd_vec_k(const float* __res
 
 int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din, const void* W, int w_dt,
                      int Dout, void* dW, void* db, int g_dt, float beta, float* din, float* part,
-                     hipStream_t s) {
+                     hipStream_t s, bool din_acc) {
   if (act != 0 || B <= 0 || B > SL_MAXB) { set_error("small_linear_bwd: batch must be 1..32"); return 1; }
   const int njt = (Dout + SL_JT - 1) / SL_JT;
   if (B <= 4 && Din % 8 == 0 && al16(in) && al16(W) && al16(dW) && (!din || al16(part))) {
@@ -356,7 +360,7 @@ int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din
     LAUNCH_OK("small_linear_bwd_vec");
     if (din) {
       const size_t n = (size_t)B * Din;
-      hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njv, n, din);
+      hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njv, n, din, din_acc);
       LAUNCH_OK("small_linear_bwd_sum");
     }
     return 0;
@@ -374,7 +378,7 @@ int small_linear_bwd(const float* dout, const float* in, int act, int B, int Din
   LAUNCH_OK("small_linear_bwd");
   if (din) {
     const size_t n = (size_t)B * Din;
-    hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njt, n, din);
+    hipLaunchKernelGGL(sum_parts_k, dim3((n + 63) / 64), dim3(256), 0, s, part, njt, n, din, din_acc);
     LAUNCH_OK("small_linear_bwd_sum");
   }
   return 0;
@@ -1734,17 +1738,6 @@ int fill_zero(void* x, size_t bytes, hipStream_t s) {
   if (!n) return 0;
   hipLaunchKernelGGL(fill_zero_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (uint32_t*)x, n);
   LAUNCH_OK("fill_zero");
-  return 0;
-}
-
-__global__ void add_into_k(float* y, const float* x, size_t n) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) y[i] += x[i];
-}
-int add_into(float* y, const float* x, size_t n, hipStream_t s) {
-  if (!n) return 0;
-  hipLaunchKernelGGL(add_into_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, y, x, n);
-  LAUNCH_OK("add_into");
   return 0;
 }
 
