@@ -57,7 +57,7 @@ HBM_PEAK = 8.0e12
 # on a 1 GiB device copy (FETCH_SIZE reads 0.5x, WRITE_SIZE 1.0x the bytes);
 # valid only for the GEMM source it was measured on (sha256 of gemm.hip,
 # first 16 hex digits).
-WGRAD_TRAFFIC = {"gemm_src": "93aef00644e157f4", "bytes_per_launch": 1437.2e6}
+WGRAD_TRAFFIC = {"gemm_src": "93aef00644e157f4", "bytes_per_launch": 1440.0e6}
 
 CLASSES = {"gemm_fwd": 1, "gemm_dgrad": 2, "gemm_wgrad": 3, "attn_fwd": 4, "attn_bwd_kv": 5, "attn_bwd_q": 6,
            "aggregate": 7}
